@@ -1,0 +1,210 @@
+"""ctypes wrapper of the C oracle (oracle.c): exact top-k sparse decode attention
+in float64 on the CPU.
+
+Test infrastructure only: the tests, the package smoke check and the
+benchmark's CPU-baseline leg may call it; the product path never does.
+It imports nothing from the HIP package.  Inputs are duck-typed: any object
+with the attributes of a decode-step description (B, Hq, Hkv, d, dtype, q, k,
+v, seq_lens, layout, ncap, ratio, rounding, group_shared, page_size,
+block_table) works.  bfloat16 arrays are uint16 arrays of bfloat16 bits.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# Test hook: the mutation tests point this at a deliberately broken copy.
+_LIB_OVERRIDE = os.environ.get("ORACLE_LIB_OVERRIDE")
+
+
+class _Cache(C.Structure):
+    _fields_ = [("data", C.c_void_p), ("dtype", C.c_int32), ("paged", C.c_int32),
+                ("ncap", C.c_int64), ("num_pages", C.c_int64), ("page_size", C.c_int32),
+                ("max_pages", C.c_int32), ("block_table", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load liboracle.so, compiling it first if it has not been built."""
+    global _lib
+    if _lib is None:
+        path = _LIB_OVERRIDE or _LIB_PATH
+        if not _LIB_OVERRIDE and not os.path.exists(_LIB_PATH):
+            from . import build
+            build.build()
+        L = C.CDLL(path)
+        L.oracle_budget.restype = C.c_int64
+        L.oracle_budget.argtypes = [C.c_int64, C.c_double, C.c_int32]
+        L.oracle_select_row.restype = C.c_int32
+        L.oracle_select_row.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_int64,
+                                        C.c_void_p, C.c_void_p]
+        L.oracle_scores.restype = C.c_int32
+        L.oracle_scores.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int32,
+                                    C.POINTER(_Cache), C.c_void_p, C.c_int32, C.c_int64,
+                                    C.c_void_p, C.c_int]
+        L.oracle_select_f32.restype = C.c_int32
+        L.oracle_select_f32.argtypes = [C.c_int, C.c_int, C.c_int64, C.c_void_p, C.c_void_p,
+                                        C.c_double, C.c_int32, C.c_void_p, C.c_int64,
+                                        C.c_void_p, C.c_void_p, C.c_int]
+        L.oracle_attend.restype = C.c_int32
+        L.oracle_attend.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int32,
+                                    C.POINTER(_Cache), C.POINTER(_Cache), C.c_void_p, C.c_int32,
+                                    C.c_double, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
+                                    C.c_int]
+        L.oracle_sparse_attention.restype = C.c_int32
+        L.oracle_sparse_attention.argtypes = [
+            C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int32, C.POINTER(_Cache),
+            C.POINTER(_Cache), C.c_void_p, C.c_double, C.c_int32, C.c_int32, C.c_double,
+            C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int]
+        L.oracle_max_threads.restype = C.c_int32
+        L.oracle_max_threads.argtypes = [C.c_int]
+        _lib = L
+    return _lib
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != 0:
+        raise OracleError(f"{what} failed with code {rc}")
+
+
+def _ptr(a) -> int | None:
+    return None if a is None else a.ctypes.data
+
+
+def _dtype_code(dtype: str) -> int:
+    return {"f32": 0, "bf16": 1}[dtype]
+
+
+def _cache(inp, arr: np.ndarray, keep: list) -> _Cache:
+    c = _Cache()
+    arr = np.ascontiguousarray(arr)
+    keep.append(arr)
+    c.data = arr.ctypes.data
+    c.dtype = _dtype_code(inp.dtype)
+    if inp.layout == "paged":
+        bt = np.ascontiguousarray(inp.block_table, dtype=np.int32)
+        keep.append(bt)
+        c.paged = 1
+        c.ncap = 0
+        c.num_pages = arr.shape[0]
+        c.page_size = inp.page_size
+        c.max_pages = bt.shape[1]
+        c.block_table = bt.ctypes.data
+    else:
+        c.paged = 0
+        c.ncap = arr.shape[2]
+        c.num_pages = 0
+        c.page_size = 0
+        c.max_pages = 0
+        c.block_table = None
+    return c
+
+
+def budget(L: int, ratio: float, rounding: int = 0) -> int:
+    """k for a sequence of L positions at sparsity ``ratio`` (0 nearest, 1 ceil)."""
+    return int(lib().oracle_budget(int(L), float(ratio), int(rounding)))
+
+
+def max_threads(nthreads: int = 0) -> int:
+    return int(lib().oracle_max_threads(int(nthreads)))
+
+
+def select_row(scores: np.ndarray, k: int, k_max: int | None = None):
+    """Exact top-k of one row of float64 scores; returns (ascending idx padded
+    with -1 to k_max, tau = k-th largest score)."""
+    s = np.ascontiguousarray(scores, dtype=np.float64)
+    k_max = k if k_max is None else k_max
+    idx = np.empty(max(k_max, 1), dtype=np.int32)
+    tau = np.empty(1, dtype=np.float64)
+    _check(lib().oracle_select_row(s.ctypes.data, len(s), int(k), int(k_max),
+                                   idx.ctypes.data, tau.ctypes.data), "select_row")
+    return idx[:k_max], float(tau[0])
+
+
+def scores(inp, nthreads: int = 0) -> np.ndarray:
+    """float64 selection scores [B, R, ncap] (NaN at j >= L_b)."""
+    keep: list = []
+    K = _cache(inp, inp.k, keep)
+    q = np.ascontiguousarray(inp.q)
+    lens = np.ascontiguousarray(inp.seq_lens, dtype=np.int32)
+    out = np.empty((inp.B, inp.rows, inp.ncap), dtype=np.float64)
+    _check(lib().oracle_scores(inp.B, inp.Hq, inp.Hkv, inp.d, q.ctypes.data,
+                               _dtype_code(inp.dtype), C.byref(K), lens.ctypes.data,
+                               int(inp.group_shared), inp.ncap, out.ctypes.data, nthreads),
+           "scores")
+    return out
+
+
+def k_max_for(inp) -> int:
+    """Largest budget any sequence of this cache capacity can need."""
+    return budget(inp.ncap, inp.ratio, inp.rounding)
+
+
+def select_f32(scores_f32: np.ndarray, seq_lens, ratio: float, rounding: int, k_max: int,
+               k_override=None, nthreads: int = 0):
+    """Exact top-k over given float32 scores [B, R, ncap]; returns (idx, tau)."""
+    s = np.ascontiguousarray(scores_f32, dtype=np.float32)
+    B, R, ncap = s.shape
+    lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
+    ko = None if k_override is None else np.ascontiguousarray(k_override, dtype=np.int32)
+    idx = np.empty((B, R, k_max), dtype=np.int32)
+    tau = np.empty((B, R), dtype=np.float64)
+    _check(lib().oracle_select_f32(B, R, ncap, s.ctypes.data, lens.ctypes.data, float(ratio),
+                                   int(rounding), _ptr(ko), int(k_max), idx.ctypes.data,
+                                   tau.ctypes.data, nthreads), "select_f32")
+    return idx, tau
+
+
+def attend(inp, idx: np.ndarray, scale: float = 0.0, nthreads: int = 0):
+    """Softmax attention over given index sets idx [B, R, k_max]; returns
+    (out [B,Hq,d], absw [B,Hq,d]) in float64."""
+    keep: list = []
+    K = _cache(inp, inp.k, keep)
+    V = _cache(inp, inp.v, keep)
+    q = np.ascontiguousarray(inp.q)
+    lens = np.ascontiguousarray(inp.seq_lens, dtype=np.int32)
+    ix = np.ascontiguousarray(idx, dtype=np.int32)
+    out = np.empty((inp.B, inp.Hq, inp.d), dtype=np.float64)
+    absw = np.empty_like(out)
+    _check(lib().oracle_attend(inp.B, inp.Hq, inp.Hkv, inp.d, q.ctypes.data,
+                               _dtype_code(inp.dtype), C.byref(K), C.byref(V), lens.ctypes.data,
+                               int(inp.group_shared), float(scale), ix.shape[2], ix.ctypes.data,
+                               out.ctypes.data, absw.ctypes.data, nthreads), "attend")
+    return out, absw
+
+
+def sparse_attention(inp, k_max: int | None = None, k_override=None, scale: float = 0.0,
+                     nthreads: int = 0) -> dict:
+    """The whole method: returns dict(idx, tau, out, absw)."""
+    keep: list = []
+    K = _cache(inp, inp.k, keep)
+    V = _cache(inp, inp.v, keep)
+    q = np.ascontiguousarray(inp.q)
+    lens = np.ascontiguousarray(inp.seq_lens, dtype=np.int32)
+    k_max = k_max_for(inp) if k_max is None else k_max
+    ko = None if k_override is None else np.ascontiguousarray(k_override, dtype=np.int32)
+    idx = np.empty((inp.B, inp.rows, k_max), dtype=np.int32)
+    tau = np.empty((inp.B, inp.rows), dtype=np.float64)
+    out = np.empty((inp.B, inp.Hq, inp.d), dtype=np.float64)
+    absw = np.empty_like(out)
+    _check(lib().oracle_sparse_attention(
+        inp.B, inp.Hq, inp.Hkv, inp.d, q.ctypes.data, _dtype_code(inp.dtype), C.byref(K),
+        C.byref(V), lens.ctypes.data, float(inp.ratio), int(inp.rounding),
+        int(inp.group_shared), float(scale), _ptr(ko), int(k_max), idx.ctypes.data,
+        tau.ctypes.data, out.ctypes.data, absw.ctypes.data, nthreads), "sparse_attention")
+    return {"idx": idx, "tau": tau, "out": out, "absw": absw}
+
+
+def default_scale(d: int) -> float:
+    return 1.0 / math.sqrt(d)
