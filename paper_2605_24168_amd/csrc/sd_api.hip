@@ -1,0 +1,512 @@
+// sd_api.hip -- the C ABI of libsparse_decode.so (declared in
+// include/sparse_decode.h): argument checks, workspace carving and the
+// ordering of the kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <mutex>
+
+#include "../../include/sparse_decode.h"
+#include "sd_internal.hpp"
+#include "sd_launch.hpp"
+
+namespace {
+
+using sd::kHeadDim;
+
+constexpr int kMaxDevices = 64;
+constexpr size_t kAlign = 256;
+constexpr int kLdsCapMax = 18000;  // candidate keys held in LDS by the selection
+constexpr int kRing = 64;          // profiled calls remembered per device
+// Longest cache (positions per sequence): the selection keeps one prefix
+// entry per 2048-key candidate list in LDS.
+constexpr int64_t kMaxCapacity = int64_t(1) << 24;
+constexpr size_t kSelectLdsBudget = 150 * 1024;  // dynamic LDS of the selection kernel
+
+struct DevState {
+  void *ws = nullptr;
+  size_t ws_bytes = 0;
+  bool user_ws = false;
+  bool events = false;
+  hipEvent_t ev[kRing][6];
+  int64_t n_calls = 0;  // profiled calls in the current series
+  int32_t *stats = nullptr;
+};
+
+std::mutex g_mu;
+DevState g_dev[kMaxDevices];
+std::atomic<int> g_profiling{0};
+std::atomic<int> g_debug{0};
+
+struct Shape {
+  int B, Hq, Hkv, G, R;
+  int64_t ncap;
+  int bf16;
+  int64_t k_max;
+};
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool is_dtype_float(int32_t d) { return d == SD_F32 || d == SD_BF16; }
+
+sd_status check_q(const sd_tensor *q, Shape &s) {
+  if (!q || !q->data || q->ndim != 3) return SD_ERR_INVALID_ARG;
+  if (!is_dtype_float(q->dtype)) return SD_ERR_INVALID_ARG;
+  if (q->shape[0] < 0 || q->shape[1] <= 0 || q->shape[2] <= 0) return SD_ERR_INVALID_ARG;
+  if (q->shape[2] != kHeadDim) return SD_ERR_UNSUPPORTED;
+  if (q->shape[0] > 65535 || q->shape[1] > 65535) return SD_ERR_UNSUPPORTED;
+  s.B = (int)q->shape[0];
+  s.Hq = (int)q->shape[1];
+  s.bf16 = q->dtype == SD_BF16;
+  return SD_OK;
+}
+
+// Checks a key/value cache against q's batch and dtype; fills Hkv and ncap.
+sd_status check_kv(const sd_kv *kv, const Shape &s, int dtype, int &hkv, int64_t &ncap) {
+  if (!kv || !kv->t.data || kv->t.ndim != 4) return SD_ERR_INVALID_ARG;
+  if (kv->t.dtype != dtype) return SD_ERR_INVALID_ARG;
+  for (int i = 0; i < 4; ++i)
+    if (kv->t.shape[i] < 0) return SD_ERR_INVALID_ARG;
+  if (kv->t.shape[3] != kHeadDim) return SD_ERR_UNSUPPORTED;
+  if (kv->layout == SD_KV_BHND) {
+    if (kv->t.shape[0] != s.B) return SD_ERR_INVALID_ARG;
+    hkv = (int)kv->t.shape[1];
+    ncap = kv->t.shape[2];
+  } else if (kv->layout == SD_KV_PAGED_NHD) {
+    if (kv->page_size != sd::kTile) return SD_ERR_UNSUPPORTED;
+    if (kv->t.shape[1] != kv->page_size) return SD_ERR_INVALID_ARG;
+    if (!kv->block_table || kv->max_pages_per_seq < 0) return SD_ERR_INVALID_ARG;
+    hkv = (int)kv->t.shape[2];
+    ncap = (int64_t)kv->max_pages_per_seq * kv->page_size;
+  } else {
+    return SD_ERR_INVALID_ARG;
+  }
+  if (hkv <= 0) return SD_ERR_INVALID_ARG;
+  if (ncap > kMaxCapacity) return SD_ERR_UNSUPPORTED;
+  return SD_OK;
+}
+
+sd_status check_problem(const sd_tensor *q, const sd_kv *K, const sd_kv *V, const sd_sparsity *sp,
+                        Shape &s) {
+  if (!sp) return SD_ERR_INVALID_ARG;
+  sd_status st = check_q(q, s);
+  if (st) return st;
+  int hkv = 0;
+  int64_t ncap = 0;
+  st = check_kv(K, s, q->dtype, hkv, ncap);
+  if (st) return st;
+  if (V) {
+    int hv = 0;
+    int64_t nv = 0;
+    st = check_kv(V, s, q->dtype, hv, nv);
+    if (st) return st;
+    if (V->layout != K->layout || hv != hkv || nv != ncap) return SD_ERR_INVALID_ARG;
+  }
+  if (s.Hq % hkv) return SD_ERR_INVALID_ARG;
+  s.Hkv = hkv;
+  s.G = s.Hq / hkv;
+  if (s.G > sd::kMaxGroup) return SD_ERR_UNSUPPORTED;
+  s.ncap = ncap;
+  s.R = sp->group_shared ? hkv : s.Hq;
+  if (sp->k_rounding != 0 && sp->k_rounding != 1) return SD_ERR_INVALID_ARG;
+  if (!sp->k_override && !(sp->ratio > 0.0 && std::isfinite(sp->ratio))) return SD_ERR_INVALID_ARG;
+  if (!std::isfinite(sp->softmax_scale)) return SD_ERR_INVALID_ARG;
+  return SD_OK;
+}
+
+// idx [B, R, k_max] int32 large enough for a full-capacity sequence.
+sd_status check_idx(const sd_tensor *idx, const Shape &s, const sd_sparsity *sp, int64_t &k_max) {
+  if (!idx || idx->ndim != 3 || idx->dtype != SD_I32) return SD_ERR_INVALID_ARG;
+  if (idx->shape[0] != s.B || idx->shape[1] != s.R || idx->shape[2] < 0) return SD_ERR_INVALID_ARG;
+  k_max = idx->shape[2];
+  if (k_max > 0 && !idx->data) return SD_ERR_INVALID_ARG;
+  if (k_max > INT32_MAX / 2) return SD_ERR_UNSUPPORTED;
+  if (!sp->k_override && k_max < sd::budget_rule(s.ncap, sp->ratio, sp->k_rounding))
+    return SD_ERR_INVALID_ARG;
+  return SD_OK;
+}
+
+sd_status check_out(const sd_tensor *out, const Shape &s, int dtype) {
+  if (!out || !out->data || out->ndim != 3 || out->dtype != dtype) return SD_ERR_INVALID_ARG;
+  if (out->shape[0] != s.B || out->shape[1] != s.Hq || out->shape[2] != kHeadDim)
+    return SD_ERR_INVALID_ARG;
+  return SD_OK;
+}
+
+sd::KvView kv_view(const sd_kv *kv, int hkv, int64_t ncap) {
+  sd::KvView v;
+  v.base = kv->t.data;
+  v.block_table = kv->layout == SD_KV_PAGED_NHD ? kv->block_table : nullptr;
+  v.ncap = ncap;
+  v.paged = kv->layout == SD_KV_PAGED_NHD;
+  v.hkv = hkv;
+  v.max_pages = kv->layout == SD_KV_PAGED_NHD ? kv->max_pages_per_seq : 0;
+  return v;
+}
+
+sd::Params make_params(const sd_tensor *q, const sd_kv *K, const sd_kv *V, const int32_t *seq_lens,
+                       const sd_sparsity *sp, const Shape &s, int64_t k_max) {
+  sd::Params p{};
+  p.q = q->data;
+  p.K = kv_view(K, s.Hkv, s.ncap);
+  p.V = V ? kv_view(V, s.Hkv, s.ncap) : p.K;
+  p.seq_lens = seq_lens;
+  p.k_override = sp->k_override;
+  p.ratio = sp->ratio > 0.0 ? sp->ratio : 1.0;
+  p.scale = sp->softmax_scale > 0.f ? sp->softmax_scale : (float)(1.0 / std::sqrt((double)kHeadDim));
+  p.B = s.B;
+  p.Hq = s.Hq;
+  p.Hkv = s.Hkv;
+  p.G = s.G;
+  p.R = s.R;
+  p.bf16 = s.bf16;
+  p.group_shared = sp->group_shared ? 1 : 0;
+  p.rounding = sp->k_rounding;
+  p.k_max = (int32_t)k_max;
+  p.ncap = s.ncap;
+  return p;
+}
+
+// Workspace layout.  Sizes depend only on the shapes, so the same layout is
+// recomputed on every call.
+struct Layout {
+  size_t sample, theta, counts, cand, flags, dense, sigma, part, done, stats, total;
+  int nsub, capw, nsplit;
+};
+
+Layout layout_for(const Shape &s, int64_t k_max, bool fused) {
+  Layout L{};
+  const int64_t rows = (int64_t)s.B * s.R;
+  L.nsub = (int)((s.ncap + sd::kWaveKeys - 1) / sd::kWaveKeys);
+  // Expected passes per list are about 2.5 k/L of its keys; keep 4x that plus slack.
+  const double expect = s.ncap > 0 ? 2.5 * (double)k_max / (double)s.ncap * sd::kWaveKeys : 0.0;
+  int capw = (int)std::ceil(4.0 * expect) + 64;
+  capw = (capw + 15) / 16 * 16;
+  if (capw > sd::kWaveKeys) capw = sd::kWaveKeys;
+  L.capw = capw;
+  L.nsplit = (int)((k_max + sd::kSplit - 1) / sd::kSplit);
+  if (L.nsplit < 1) L.nsplit = 1;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes);
+    return o;
+  };
+  if (fused) {
+    L.sample = take((size_t)rows * sd::kSampleMax * 4);
+    L.theta = take((size_t)rows * 4);
+    L.counts = take((size_t)rows * L.nsub * 4);
+    L.cand = take((size_t)rows * L.nsub * L.capw * 8);
+    L.flags = take((size_t)rows * 4);
+    L.dense = take((size_t)rows * s.ncap * 4);
+    L.sigma = take((size_t)rows * k_max * 4);
+  }
+  L.part = take((size_t)s.B * s.Hq * L.nsplit * sd::kPartStride * 4);
+  L.done = take((size_t)rows * 4);
+  L.stats = take(64);
+  L.total = off;
+  return L;
+}
+
+sd_status hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
+
+// The current device's workspace, at least `bytes` long.
+sd_status get_workspace(size_t bytes, DevState *&ds, char *&base) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SD_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SD_ERR_UNSUPPORTED;
+  ds = &g_dev[dev];
+  if (ds->ws_bytes < bytes) {
+    if (ds->user_ws) return SD_ERR_WORKSPACE;
+    if (ds->ws) {
+      if (hipFree(ds->ws) != hipSuccess) return SD_ERR_HIP;
+      ds->ws = nullptr;
+      ds->ws_bytes = 0;
+    }
+    void *ptr = nullptr;
+    if (hipMalloc(&ptr, bytes) != hipSuccess) return SD_ERR_WORKSPACE;
+    ds->ws = ptr;
+    ds->ws_bytes = bytes;
+  }
+  base = (char *)ds->ws;
+  return SD_OK;
+}
+
+sd::Work carve(char *base, const Layout &L, bool fused) {
+  sd::Work w{};
+  if (fused) {
+    w.sample = (float *)(base + L.sample);
+    w.theta = (float *)(base + L.theta);
+    w.counts = (int32_t *)(base + L.counts);
+    w.cand = (uint2 *)(base + L.cand);
+    w.flags = (int32_t *)(base + L.flags);
+    w.dense = (float *)(base + L.dense);
+    w.sigma = (float *)(base + L.sigma);
+  }
+  w.part = (float *)(base + L.part);
+  w.done = (int32_t *)(base + L.done);
+  w.stats = (int32_t *)(base + L.stats);
+  w.nsub = L.nsub;
+  w.capw = L.capw;
+  w.nsplit = L.nsplit;
+  w.force_repair = (g_debug.load() & 1) ? 1 : 0;
+  return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *sparse_decode_status_string(sd_status status) {
+  switch (status) {
+    case SD_OK: return "ok";
+    case SD_ERR_INVALID_ARG: return "invalid argument";
+    case SD_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SD_ERR_WORKSPACE: return "workspace too small or allocation failed";
+    case SD_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+int64_t sparse_decode_budget(int64_t L, const sd_sparsity *sp) {
+  if (!sp || !(sp->ratio > 0.0) || !std::isfinite(sp->ratio)) return -1;
+  return sd::budget_rule(L, sp->ratio, sp->k_rounding);
+}
+
+sd_status sparse_decode_set_profiling(int32_t enable) {
+  std::lock_guard<std::mutex> lk(g_mu);
+  g_profiling.store(enable ? 1 : 0);
+  if (enable)
+    for (auto &d : g_dev) d.n_calls = 0;
+  return SD_OK;
+}
+
+sd_status sparse_decode_set_debug(int32_t flags) {
+  g_debug.store(flags);
+  return SD_OK;
+}
+
+sd_status sparse_decode_workspace_size(const sd_tensor *q, const sd_kv *K, const sd_sparsity *sp,
+                                       const sd_tensor *idx, size_t *bytes) {
+  if (!bytes) return SD_ERR_INVALID_ARG;
+  Shape s{};
+  sd_status st = check_problem(q, K, nullptr, sp, s);
+  if (st) return st;
+  int64_t k_max = 0;
+  st = check_idx(idx, s, sp, k_max);
+  if (st) return st;
+  *bytes = layout_for(s, k_max, true).total;
+  return SD_OK;
+}
+
+sd_status sparse_decode_set_workspace(void *dev_ptr, size_t bytes) {
+  if (dev_ptr && ((uintptr_t)dev_ptr % kAlign)) return SD_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_mu);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SD_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SD_ERR_UNSUPPORTED;
+  DevState &ds = g_dev[dev];
+  if (ds.ws && !ds.user_ws) {
+    if (hipFree(ds.ws) != hipSuccess) return SD_ERR_HIP;
+  }
+  ds.ws = dev_ptr;
+  ds.ws_bytes = dev_ptr ? bytes : 0;
+  ds.user_ws = dev_ptr != nullptr;
+  return SD_OK;
+}
+
+sd_status sparse_decode_score(const sd_tensor *q, const sd_kv *K, const int32_t *seq_lens,
+                              const sd_sparsity *sp, sd_tensor *scores, void *stream) {
+  Shape s{};
+  sd_status st = check_problem(q, K, nullptr, sp, s);
+  if (st) return st;
+  if (!seq_lens && s.B > 0) return SD_ERR_INVALID_ARG;
+  if (!scores || scores->ndim != 3 || scores->dtype != SD_F32) return SD_ERR_INVALID_ARG;
+  if (scores->shape[0] != s.B || scores->shape[1] != s.R || scores->shape[2] != s.ncap)
+    return SD_ERR_INVALID_ARG;
+  if (s.B == 0 || s.ncap == 0) return SD_OK;
+  if (!scores->data) return SD_ERR_INVALID_ARG;
+  const sd::Params p = make_params(q, K, nullptr, seq_lens, sp, s, 0);
+  return hip_status(sd::launch_score_dense(p, (float *)scores->data, (hipStream_t)stream));
+}
+
+sd_status sparse_decode_topk(const sd_tensor *scores, const int32_t *seq_lens, const sd_sparsity *sp,
+                             sd_tensor *idx, sd_tensor *vals, void *stream) {
+  if (!sp || !scores || scores->ndim != 3 || scores->dtype != SD_F32) return SD_ERR_INVALID_ARG;
+  for (int i = 0; i < 3; ++i)
+    if (scores->shape[i] < 0) return SD_ERR_INVALID_ARG;
+  if (scores->shape[0] > 65535 || scores->shape[1] > 65535) return SD_ERR_UNSUPPORTED;
+  if (sp->k_rounding != 0 && sp->k_rounding != 1) return SD_ERR_INVALID_ARG;
+  if (!sp->k_override && !(sp->ratio > 0.0 && std::isfinite(sp->ratio))) return SD_ERR_INVALID_ARG;
+  Shape s{};
+  s.B = (int)scores->shape[0];
+  s.R = (int)scores->shape[1];
+  s.ncap = scores->shape[2];
+  if (s.ncap > kMaxCapacity) return SD_ERR_UNSUPPORTED;
+  int64_t k_max = 0;
+  sd_status st = check_idx(idx, s, sp, k_max);
+  if (st) return st;
+  if (vals) {
+    if (vals->ndim != 3 || vals->dtype != SD_F32 || vals->shape[0] != s.B ||
+        vals->shape[1] != s.R || vals->shape[2] != k_max || (k_max > 0 && !vals->data))
+      return SD_ERR_INVALID_ARG;
+  }
+  if (s.B == 0 || s.R == 0) return SD_OK;
+  if (!seq_lens || (s.ncap > 0 && !scores->data)) return SD_ERR_INVALID_ARG;
+  sd::Params p{};
+  p.seq_lens = seq_lens;
+  p.k_override = sp->k_override;
+  p.ratio = sp->ratio > 0.0 ? sp->ratio : 1.0;
+  p.rounding = sp->k_rounding;
+  p.B = s.B;
+  p.R = s.R;
+  p.k_max = (int32_t)k_max;
+  p.ncap = s.ncap;
+  return hip_status(sd::launch_topk(p, (const float *)scores->data, (int32_t *)idx->data,
+                                    vals ? (float *)vals->data : nullptr, (hipStream_t)stream));
+}
+
+sd_status sparse_decode_attend(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                               const int32_t *seq_lens, const sd_tensor *idx, const sd_sparsity *sp,
+                               sd_tensor *out, void *stream) {
+  Shape s{};
+  sd_status st = check_problem(q, K, V, sp, s);
+  if (st) return st;
+  if (!V) return SD_ERR_INVALID_ARG;
+  if (!idx || idx->ndim != 3 || idx->dtype != SD_I32 || idx->shape[0] != s.B ||
+      idx->shape[1] != s.R || idx->shape[2] < 0)
+    return SD_ERR_INVALID_ARG;
+  const int64_t k_max = idx->shape[2];
+  if (k_max > INT32_MAX / 2) return SD_ERR_UNSUPPORTED;
+  st = check_out(out, s, q->dtype);
+  if (st) return st;
+  if (s.B == 0) return SD_OK;
+  if (!seq_lens || (k_max > 0 && !idx->data)) return SD_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_mu);
+  const Layout L = layout_for(s, k_max, false);
+  DevState *ds = nullptr;
+  char *base = nullptr;
+  st = get_workspace(L.total, ds, base);
+  if (st) return st;
+  const sd::Work w = carve(base, L, false);
+  const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
+  return hip_status(sd::launch_attend(p, w, (const int32_t *)idx->data, out->data, false,
+                                      (hipStream_t)stream));
+}
+
+sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                  const int32_t *seq_lens, const sd_sparsity *sp, sd_tensor *out,
+                                  sd_tensor *idx, void *stream) {
+  Shape s{};
+  sd_status st = check_problem(q, K, V, sp, s);
+  if (st) return st;
+  if (!V) return SD_ERR_INVALID_ARG;
+  int64_t k_max = 0;
+  st = check_idx(idx, s, sp, k_max);
+  if (st) return st;
+  st = check_out(out, s, q->dtype);
+  if (st) return st;
+  if (s.B == 0) return SD_OK;
+  if (!seq_lens) return SD_ERR_INVALID_ARG;
+  const hipStream_t stream_h = (hipStream_t)stream;
+  std::lock_guard<std::mutex> lk(g_mu);
+  const Layout L = layout_for(s, k_max, true);
+  DevState *ds = nullptr;
+  char *base = nullptr;
+  st = get_workspace(L.total, ds, base);
+  if (st) return st;
+  const sd::Work w = carve(base, L, true);
+  const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
+  int32_t *idx_ptr = (int32_t *)idx->data;
+
+  const bool prof = g_profiling.load() != 0;
+  if (prof && !ds->events) {
+    for (auto &set : ds->ev)
+      for (auto &e : set)
+        if (hipEventCreate(&e) != hipSuccess) return SD_ERR_HIP;
+    ds->events = true;
+  }
+  hipEvent_t *ev = ds->ev[ds->n_calls % kRing];
+  auto mark = [&](int i) -> hipError_t {
+    return prof ? hipEventRecord(ev[i], stream_h) : hipSuccess;
+  };
+  int lds_cap = (int)(4 * k_max + 1024);
+  if (lds_cap > kLdsCapMax) lds_cap = kLdsCapMax;
+  const size_t pre_bytes = sd::select_lds_bytes(p, 0);
+  const int lds_room = (int)((kSelectLdsBudget - pre_bytes) / 8);
+  if (lds_cap > lds_room) lds_cap = lds_room;
+  hipError_t e = mark(0);
+  if (e == hipSuccess) e = sd::launch_pilot(p, w, stream_h);
+  if (e == hipSuccess) e = mark(1);
+  if (e == hipSuccess && s.ncap > 0) e = sd::launch_score_filter(p, w, stream_h);
+  if (e == hipSuccess) e = mark(2);
+  if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, stream_h);
+  if (e == hipSuccess) e = mark(3);
+  if (e == hipSuccess && s.ncap > 0) e = sd::launch_repair(p, w, idx_ptr, stream_h);
+  if (e == hipSuccess) e = mark(4);
+  if (e == hipSuccess) e = sd::launch_attend(p, w, idx_ptr, out->data, true, stream_h);
+  if (e == hipSuccess) e = mark(5);
+  if (prof && e == hipSuccess) ds->n_calls++;
+  ds->stats = w.stats;
+  return hip_status(e);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Stage times of ring slot `slot` (its events must be complete).
+sd_status read_slot(DevState &ds, int slot, float t[6]) {
+  hipEvent_t *ev = ds.ev[slot];
+  if (hipEventSynchronize(ev[5]) != hipSuccess) return SD_ERR_HIP;
+  for (int i = 0; i < 5; ++i)
+    if (hipEventElapsedTime(&t[i], ev[i], ev[i + 1]) != hipSuccess) return SD_ERR_HIP;
+  if (hipEventElapsedTime(&t[5], ev[0], ev[5]) != hipSuccess) return SD_ERR_HIP;
+  return SD_OK;
+}
+
+sd_status summarize(sd_profile *out, int32_t *n_out, bool mean) {
+  if (!out) return SD_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_mu);
+  *out = sd_profile{};
+  if (n_out) *n_out = 0;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return SD_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return SD_ERR_UNSUPPORTED;
+  DevState &ds = g_dev[dev];
+  if (ds.n_calls == 0) return SD_OK;
+  const int64_t n = mean ? (ds.n_calls < kRing ? ds.n_calls : kRing) : 1;
+  double acc[6] = {0, 0, 0, 0, 0, 0};
+  for (int64_t c = ds.n_calls - n; c < ds.n_calls; ++c) {
+    float t[6];
+    const sd_status st = read_slot(ds, (int)(c % kRing), t);
+    if (st) return st;
+    for (int i = 0; i < 6; ++i) acc[i] += t[i];
+  }
+  out->pilot_ms = (float)(acc[0] / n);
+  out->score_ms = (float)(acc[1] / n);
+  out->select_ms = (float)(acc[2] / n);
+  out->repair_ms = (float)(acc[3] / n);
+  out->attend_ms = (float)(acc[4] / n);
+  out->total_ms = (float)(acc[5] / n);
+  int32_t repaired = 0;
+  if (ds.stats && hipMemcpy(&repaired, ds.stats, sizeof repaired, hipMemcpyDeviceToHost) != hipSuccess)
+    return SD_ERR_HIP;
+  out->repaired_rows = repaired;
+  out->valid = 1;
+  if (n_out) *n_out = (int32_t)n;
+  return SD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+sd_status sparse_decode_last_profile(sd_profile *out) { return summarize(out, nullptr, false); }
+
+sd_status sparse_decode_profile_mean(sd_profile *out, int32_t *n_calls) {
+  return summarize(out, n_calls, true);
+}
+
+}  // extern "C"

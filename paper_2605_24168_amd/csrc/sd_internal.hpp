@@ -1,0 +1,413 @@
+// sd_internal.hpp -- device-side building blocks of libsparse_decode.so
+// (exact top-k context-sparse decode attention on gfx950).
+//
+// Everything here is written for CDNA4: 64-lane wavefronts, the
+// v_mfma_f32_16x16x32_bf16 matrix instruction, LDS, and 16-byte vector loads.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace sd {
+
+constexpr int kHeadDim = 128;
+constexpr int kTile = 16;          // keys per scoring tile (= KV page size)
+constexpr int kBlock = 256;        // threads per workgroup of every kernel
+constexpr int kWaves = kBlock / 64;
+constexpr int kMaxGroup = 16;      // query heads per KV head handled by one MFMA tile
+constexpr int kChunkKeys = 8192;   // keys one scoring workgroup streams
+constexpr int kWaveKeys = kChunkKeys / kWaves;
+constexpr int kSampleMax = 4096;   // pilot samples per row
+constexpr int kSplit = 256;        // kept positions per attend workgroup
+constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
+constexpr int kRepairParts = 64;   // workgroups per (sequence, KV head) in the repair stream
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// Problem description passed by value to every kernel.
+// ---------------------------------------------------------------------------
+struct KvView {
+  const void *base;
+  const int32_t *block_table;  // paged only: [B, max_pages]
+  int64_t ncap;                // positions addressable per sequence
+  int32_t paged;
+  int32_t hkv;
+  int32_t max_pages;
+};
+
+struct Params {
+  const void *q;               // [B, Hq, 128]
+  KvView K, V;
+  const int32_t *seq_lens;     // [B]
+  const int32_t *k_override;   // [B] or null
+  double ratio;
+  float scale;
+  int32_t B, Hq, Hkv, G, R;
+  int32_t bf16;
+  int32_t group_shared;
+  int32_t rounding;
+  int32_t k_max;
+  int64_t ncap;
+};
+
+// Scratch carved from the library workspace (see the host orchestration).
+struct Work {
+  float *sample;     // [rows][kSampleMax] pilot sample scores
+  float *theta;      // [rows] candidate threshold
+  int32_t *counts;   // [rows][nsub] candidates found by each scoring wave
+  uint2 *cand;       // [rows][nsub][capw] (order-preserving key, position)
+  int32_t *flags;    // [rows] 1 = the row needs the exact fallback
+  float *dense;      // [rows][ncap] fallback scores
+  float *sigma;      // [rows][k_max] kept scores, aligned with idx
+  float *part;       // [B*Hq][nsplit][kPartStride] attend partials
+  int32_t *done;     // [rows] attend arrival counters (zeroed by the pilot)
+  int32_t *stats;    // [4]: [0] rows repaired in the last call
+  int32_t nsub;
+  int32_t capw;
+  int32_t nsplit;
+  int32_t force_repair;
+};
+
+// ---------------------------------------------------------------------------
+// Small helpers.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
+__device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+
+// k for a sequence of L positions (Table 1 caption: 1/S of the tokens).
+__host__ __device__ inline int64_t budget_rule(int64_t L, double ratio, int rounding) {
+  if (L <= 0) return 0;
+  double x = (double)L / ratio;
+  double k = rounding == 1 ? ceil(x) : floor(x + 0.5);
+  if (k < 1.0) k = 1.0;
+  if (k > (double)L) k = (double)L;
+  return (int64_t)k;
+}
+
+__device__ __forceinline__ int seq_len(const Params &p, int b) {
+  int64_t L = p.seq_lens[b];
+  if (L < 0) L = 0;
+  if (L > p.ncap) L = p.ncap;
+  return (int)L;
+}
+
+__device__ __forceinline__ int row_budget(const Params &p, int b, int L) {
+  int64_t k;
+  if (p.k_override) {
+    k = p.k_override[b];
+    if (k < 0) k = 0;
+    if (k > L) k = L;
+  } else {
+    k = budget_rule(L, p.ratio, p.rounding);
+  }
+  if (k > p.k_max) k = p.k_max;
+  return (int)k;
+}
+
+// Element offset of channel 0 of (sequence b, KV head g, position j).
+__device__ __forceinline__ int64_t kv_offset(const KvView &kv, int b, int g, int64_t j) {
+  if (!kv.paged) return (((int64_t)b * kv.hkv + g) * kv.ncap + j) * kHeadDim;
+  int64_t page = kv.block_table[(int64_t)b * kv.max_pages + (j >> 4)];
+  return ((page * kTile + (j & 15)) * kv.hkv + g) * kHeadDim;
+}
+
+// Order-preserving 32-bit key of a float: larger float <=> larger key.
+// -0 is folded onto +0 so that equal floats give equal keys.
+__device__ __forceinline__ uint32_t f2key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u << 1) == 0) u = 0;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key2f(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// ---------------------------------------------------------------------------
+// Scoring tile: 16 keys x up to 16 query heads of one KV group.
+//
+// MFMA 16x16x32 bf16 layout (gfx950): operand A row i / operand B column j
+// come from lanes with (lane & 15) == i / j, and lane group s = lane >> 4
+// supplies elements 8s..8s+7 of the 32-long contraction slice.  The result
+// lane l holds C[4*(l>>4) + r][l & 15], r = 0..3.  A = the group's queries
+// (rows = heads), B = the key tile (columns = keys); the four MFMAs of one
+// tile walk d in slices of 32 channels, so lane group s reads channels
+// 32*kk + 8s .. +7 of its key: per instruction the wave touches 16 keys x
+// 64 contiguous bytes, and the tile's 4 KB exactly once.
+// After the tile, lane l holds the scores of heads 4*(l>>4)+r for key l&15.
+// ---------------------------------------------------------------------------
+struct QFrag {
+  u32x4 v[4];
+};
+
+__device__ __forceinline__ void load_q_bf16(const Params &p, int b, int g, QFrag &qf) {
+  const int l = lane_id();
+  const int h = l & 15, s = l >> 4;
+  if (h < p.G) {
+    const uint16_t *qp =
+        (const uint16_t *)p.q + ((int64_t)b * p.Hq + (int64_t)g * p.G + h) * kHeadDim + 8 * s;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) qf.v[kk] = *(const u32x4 *)(qp + 32 * kk);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) qf.v[kk] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+struct KFrag {
+  u32x4 v[4];
+};
+
+// Load this lane's slices of key row `off` (element offset of channel 0).
+__device__ __forceinline__ void load_k_bf16(const KvView &K, int64_t off, KFrag &kf) {
+  const uint16_t *kp = (const uint16_t *)K.base + off + 8 * (lane_id() >> 4);
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) kf.v[kk] = __builtin_nontemporal_load((const u32x4 *)(kp + 32 * kk));
+}
+
+__device__ __forceinline__ f32x4 mfma_scores(const QFrag &qf, const KFrag &kf) {
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk)
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, qf.v[kk]),
+                                                  __builtin_bit_cast(bf16x8, kf.v[kk]), acc, 0,
+                                                  0, 0);
+  return acc;
+}
+
+// float32 caches: the same result layout computed on the vector ALUs.
+// q_lds holds the group's queries [16][128] (rows >= G are zero).  Each dot
+// product runs over d in ascending order with fused multiply-adds.
+__device__ __forceinline__ f32x4 valu_scores_f32(const float *q_lds, const float *krow, int G) {
+  const int s = lane_id() >> 4;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < kHeadDim / 4; ++c) {
+    const float4 kv = ((const float4 *)krow)[c];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int h = 4 * s + r;
+      if (h < G) {
+        const float4 qv = ((const float4 *)(q_lds + h * kHeadDim))[c];
+        float a = acc[r];
+        a = fmaf(qv.x, kv.x, a);
+        a = fmaf(qv.y, kv.y, a);
+        a = fmaf(qv.z, kv.z, a);
+        a = fmaf(qv.w, kv.w, a);
+        acc[r] = a;
+      }
+    }
+  }
+  return acc;
+}
+
+__device__ __forceinline__ void load_q_f32_lds(const Params &p, int b, int g, float *q_lds) {
+  for (int e = threadIdx.x; e < kMaxGroup * kHeadDim; e += blockDim.x) {
+    const int h = e / kHeadDim;
+    q_lds[e] = h < p.G ? ((const float *)p.q)[((int64_t)b * p.Hq + (int64_t)g * p.G + h) * kHeadDim +
+                                               (e % kHeadDim)]
+                       : 0.f;
+  }
+}
+
+// Group-summed score of the tile's key for this lane: heads beyond G hold
+// exact zeros, so summing all 16 rows equals summing the group.  The sum is
+// formed the same way in every kernel, hence bit-identical everywhere.
+__device__ __forceinline__ float group_sum(f32x4 acc) {
+  float s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  s += __shfl_xor(s, 16);
+  s += __shfl_xor(s, 32);
+  return s;
+}
+
+// ---------------------------------------------------------------------------
+// Block-wide primitives (blockDim.x == kBlock).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(v, o);
+    if (l >= o) v += t;
+  }
+  return v;
+}
+
+// Exclusive prefix sum over the block in thread order; *total gets the sum.
+// tmp: LDS int[kWaves].  Must be reached by every thread of the block.
+__device__ __forceinline__ int block_excl_scan(int v, int *tmp, int *total) {
+  const int inc = wave_incl_scan(v);
+  if (lane_id() == 63) tmp[wave_id()] = inc;
+  __syncthreads();
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const int t = tmp[w];
+    before += (w < wave_id()) ? t : 0;
+    tot += t;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + inc - v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+
+__device__ __forceinline__ float block_max(float v, float *tmp) {
+  v = wave_max(v);
+  if (lane_id() == 0) tmp[wave_id()] = v;
+  __syncthreads();
+  float m = tmp[0];
+#pragma unroll
+  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, tmp[w]);
+  __syncthreads();
+  return m;
+}
+
+// Add 1 to hist[dig] for every active lane with act set, one LDS atomic per
+// distinct digit in the wave (lanes sharing a digit are counted by ballot).
+__device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t dig, bool act) {
+  uint64_t pending = __ballot(act);
+  while (pending) {
+    const int leader = __ffsll((unsigned long long)pending) - 1;
+    const uint32_t v = __shfl(dig, leader);
+    const uint64_t same = __ballot(act && dig == v);
+    if (lane_id() == leader) atomicAdd(&hist[v], (uint32_t)__popcll(same));
+    pending &= ~same;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exact selection of the k-th largest key among n items by three histogram
+// passes over 11, 11 and 10 key bits.  src.key(p) returns item p's key.
+// On return T is the k-th largest key and need_eq the number of items equal
+// to T that belong to the top k (the others with key == T are the later ones
+// in item order).  hist: LDS uint32[2048]; sh: LDS scratch.
+// ---------------------------------------------------------------------------
+struct SelShared {
+  int scan[kWaves];
+  uint32_t digit;
+  int above;
+};
+
+template <class Src>
+__device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelShared *sh,
+                             uint32_t &T, int &need_eq) {
+  uint32_t prefix = 0, mask = 0;
+  int krem = k;
+  const int tid = threadIdx.x;
+#pragma unroll 1
+  for (int pass = 0; pass < 3; ++pass) {
+    const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+    const int nb = pass == 2 ? 1024 : 2048;
+    const uint32_t dmask = (uint32_t)nb - 1u;
+    for (int i = tid; i < nb; i += kBlock) hist[i] = 0;
+    __syncthreads();
+    for (int base = 0; base < n; base += kBlock) {
+      const int p = base + tid;
+      uint32_t key = 0;
+      bool act = false;
+      if (p < n) {
+        key = src.key(p);
+        act = (key & mask) == prefix;
+      }
+      hist_add(hist, (key >> shift) & dmask, act);
+    }
+    __syncthreads();
+    // Thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top.
+    const int bpt = nb / kBlock;
+    const int hi = nb - tid * bpt;
+    int mine = 0;
+    for (int i = 1; i <= bpt; ++i) mine += (int)hist[hi - i];
+    int tot;
+    const int before = block_excl_scan(mine, sh->scan, &tot);
+    if (before < krem && krem <= before + mine) {
+      int cum = before;
+      for (int i = 1; i <= bpt; ++i) {
+        const int c = (int)hist[hi - i];
+        if (cum + c >= krem) {
+          sh->digit = (uint32_t)(hi - i);
+          sh->above = cum;
+          break;
+        }
+        cum += c;
+      }
+    }
+    __syncthreads();
+    prefix |= sh->digit << shift;
+    mask |= dmask << shift;
+    krem -= sh->above;
+    __syncthreads();
+  }
+  T = prefix;
+  need_eq = krem;
+}
+
+// ---------------------------------------------------------------------------
+// Order-preserving compaction of the selection: walk items in order and keep
+// those with key > T plus the first need_eq with key == T.  emit(pos, item)
+// is called with the output slot of every kept item (slots 0..k-1 in item
+// order).  Each thread handles kIpt consecutive items per round.
+// ---------------------------------------------------------------------------
+constexpr int kIpt = 8;
+
+template <class Src, class Emit>
+__device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int need_eq, int *scan,
+                                 Emit emit) {
+  int eq_before = 0, sel_before = 0;
+  const int tid = threadIdx.x;
+#pragma unroll 1
+  for (int base = 0; base < n && sel_before < k; base += kBlock * kIpt) {
+    const int p0 = base + tid * kIpt;
+    uint2 it[kIpt];
+    int n_eq = 0;
+#pragma unroll
+    for (int u = 0; u < kIpt; ++u) {
+      const int p = p0 + u;
+      it[u] = p < n ? src.get(p) : make_uint2(0u, 0u);
+      n_eq += (p < n && it[u].x == T) ? 1 : 0;
+    }
+    int eq_tot;
+    int eq_rank = block_excl_scan(n_eq, scan, &eq_tot) + eq_before;
+    unsigned sel_mask = 0;
+    int n_sel = 0;
+#pragma unroll
+    for (int u = 0; u < kIpt; ++u) {
+      const int p = p0 + u;
+      bool sel = false;
+      if (p < n) {
+        if (it[u].x > T) {
+          sel = true;
+        } else if (it[u].x == T) {
+          sel = eq_rank < need_eq;
+          ++eq_rank;
+        }
+      }
+      sel_mask |= sel ? (1u << u) : 0u;
+      n_sel += sel ? 1 : 0;
+    }
+    int sel_tot;
+    int pos = block_excl_scan(n_sel, scan, &sel_tot) + sel_before;
+#pragma unroll
+    for (int u = 0; u < kIpt; ++u)
+      if (sel_mask & (1u << u)) emit(pos++, it[u]);
+    eq_before += eq_tot;
+    sel_before += sel_tot;
+  }
+}
+
+}  // namespace sd

@@ -1,0 +1,704 @@
+// sd_kernels.hip -- gfx950 kernels of exact top-k context-sparse decode
+// attention (arXiv 2605.24168, Section 3: exact "oracle" top-k at decode
+// time; Table 1: k = N/S per query head; per-query, per-head, token-level
+// sparsity under GQA).
+//
+// Fused pipeline for one decode step, all on the caller's stream:
+//   k_pilot_score   scores a strided sample of <= 4096 keys per row
+//   k_pilot_select  picks a per-row threshold from the sample (aimed at about
+//                   2.5 k candidates) and clears the per-row state
+//   k_score_filter  streams every key once (MFMA scoring, one K tile shared
+//                   by all query heads of the group) and appends the keys at
+//                   or above the threshold to per-wave candidate lists, in
+//                   position order, with ballots instead of atomics
+//   k_select        exact top-k over the candidates; a row whose candidates
+//                   cannot prove exactness is flagged for the fallback
+//   k_score_dense   (fallback) full scores of the flagged rows' groups
+//   k_select        (fallback) exact top-k over those full scores
+//   k_attend        gathers the kept value rows, split over workgroups, and
+//                   merges the (max, sum, output) partials by log-sum-exp
+// The threshold is only a filter: the selection is exact whenever every
+// kept position passed it, which holds iff at least k candidates passed
+// (then the k-th largest candidate is >= the threshold, so nothing above
+// the true k-th largest score was filtered out) and no candidate list
+// overflowed.  Otherwise the row takes the exact fallback.
+#include "sd_internal.hpp"
+#include "sd_launch.hpp"
+
+namespace sd {
+
+// ---------------------------------------------------------------------------
+// Scoring of one key per lane, in the MFMA result layout.
+// ---------------------------------------------------------------------------
+template <bool BF16>
+struct Scorer {
+  QFrag qf;
+  float *q_lds;
+  __device__ __forceinline__ f32x4 score(const Params &p, int b, int g, int64_t j) const {
+    if constexpr (BF16) {
+      KFrag kf;
+      load_k_bf16(p.K, kv_offset(p.K, b, g, j), kf);
+      return mfma_scores(qf, kf);
+    } else {
+      return valu_scores_f32(q_lds, (const float *)p.K.base + kv_offset(p.K, b, g, j), p.G);
+    }
+  }
+};
+
+// Shared prologue: query fragments (bf16) or the group's queries in LDS (f32).
+// Every thread of the block must call it.
+template <bool BF16>
+__device__ __forceinline__ void scorer_init(const Params &p, int b, int g, Scorer<BF16> &sc,
+                                            float *q_lds) {
+  sc.q_lds = q_lds;
+  if constexpr (BF16) {
+    load_q_bf16(p, b, g, sc.qf);
+  } else {
+    load_q_f32_lds(p, b, g, q_lds);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pilot: scores of a strided sample of each sequence.
+// grid = (parts, B*Hkv).  Sample i of a sequence of length L is position
+// floor(i*L/m), m = min(L, kSampleMax), so m = L samples every position.
+// ---------------------------------------------------------------------------
+template <bool BF16>
+__global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
+  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
+  const int bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
+  const int L = seq_len(p, b);
+  Scorer<BF16> sc;
+  scorer_init<BF16>(p, b, g, sc, q_lds);
+  const int m = L < kSampleMax ? L : kSampleMax;
+  const int ntiles = (m + kTile - 1) / kTile;
+  const int l = lane_id(), col = l & 15, s = l >> 4;
+  for (int t = blockIdx.x * kWaves + wave_id(); t < ntiles; t += gridDim.x * kWaves) {
+    const int si = t * kTile + col;
+    const bool valid = si < m;
+    const int64_t pos = valid ? ((int64_t)si * L) / m : 0;
+    const f32x4 acc = sc.score(p, b, g, pos);
+    if (!p.group_shared) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int h = 4 * s + r;
+        if (valid && h < p.G)
+          w.sample[((int64_t)b * p.R + (int64_t)g * p.G + h) * kSampleMax + si] = acc[r];
+      }
+    } else {
+      const float gs = group_sum(acc);
+      if (valid && s == 0) w.sample[((int64_t)b * p.R + g) * kSampleMax + si] = gs;
+    }
+  }
+}
+
+struct LdsKeys {
+  const uint32_t *keys;
+  __device__ __forceinline__ uint32_t key(int i) const { return keys[i]; }
+};
+
+// Per-row threshold = the r-th largest sample score, r = ceil(2.5 k m / L)
+// (so about 2.5 k of the L keys are expected to pass), or r = k when the
+// sample is the whole sequence.  Also clears the row's flags and counters.
+__global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
+  __shared__ uint32_t keys[kSampleMax];
+  __shared__ uint32_t hist[2048];
+  __shared__ SelShared sh;
+  const int row = blockIdx.x, b = row / p.R;
+  const int L = seq_len(p, b);
+  const int k = row_budget(p, b, L);
+  if (threadIdx.x == 0) {
+    w.flags[row] = 0;
+    w.done[row] = 0;
+    if (row == 0) w.stats[0] = 0;
+  }
+  if (k == 0 || w.force_repair) {
+    if (threadIdx.x == 0) w.theta[row] = __builtin_inff();
+    return;
+  }
+  const int m = L < kSampleMax ? L : kSampleMax;
+  int r;
+  if (m == L) {
+    r = k;
+  } else {
+    const int64_t rr = (5LL * k * m + 2LL * L - 1) / (2LL * L);
+    r = (int)(rr < m ? rr : m);
+    if (r < 1) r = 1;
+  }
+  for (int i = threadIdx.x; i < m; i += kBlock) keys[i] = f2key(w.sample[(int64_t)row * kSampleMax + i]);
+  __syncthreads();
+  uint32_t T;
+  int need_eq;
+  radix_select(LdsKeys{keys}, m, r, hist, &sh, T, need_eq);
+  if (threadIdx.x == 0) w.theta[row] = key2f(T);
+}
+
+// ---------------------------------------------------------------------------
+// The scoring stream.  grid = (ceil(ncap / kChunkKeys), B*Hkv).  Wave v of
+// workgroup c streams keys [c*kChunkKeys + v*kWaveKeys, +kWaveKeys) of one
+// (sequence, KV head) in 16-key MFMA tiles, one tile ahead in registers, and
+// writes its candidates of every row of the group to its own list
+// cand[row][c*4+v][0..capw) in position order; counts[row][c*4+v] gets the
+// number that passed (which may exceed capw: overflow).
+// ---------------------------------------------------------------------------
+template <bool BF16>
+__global__ __launch_bounds__(kBlock) void k_score_filter(Params p, Work w) {
+  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
+  const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
+  const int L = seq_len(p, b);
+  const int64_t c0 = (int64_t)chunk * kChunkKeys;
+  if (c0 >= L) return;  // whole workgroup: no barrier follows
+  Scorer<BF16> sc;
+  scorer_init<BF16>(p, b, g, sc, q_lds);
+  const int wv = wave_id();
+  const int64_t w0 = c0 + (int64_t)wv * kWaveKeys;
+  if (w0 >= L) return;
+  const int64_t w1 = (w0 + kWaveKeys < (int64_t)L) ? w0 + kWaveKeys : (int64_t)L;
+  const int sub = chunk * kWaves + wv;
+  const int l = lane_id(), col = l & 15, s = l >> 4;
+  const uint32_t below = (1u << col) - 1u;
+
+  // Rows served by this lane: heads 4s..4s+3 of the group (per-head mode) or
+  // the group itself (group-shared mode, lanes 0..15).
+  float th[4];
+  uint2 *cl[4];
+  int cnt[4] = {0, 0, 0, 0};
+  if (!p.group_shared) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int h = 4 * s + r;
+      const int64_t row = (int64_t)b * p.R + (int64_t)g * p.G + (h < p.G ? h : 0);
+      th[r] = w.theta[row];
+      cl[r] = w.cand + (row * w.nsub + sub) * (int64_t)w.capw;
+    }
+  } else {
+    const int64_t row = (int64_t)b * p.R + g;
+    th[0] = w.theta[row];
+    cl[0] = w.cand + (row * w.nsub + sub) * (int64_t)w.capw;
+  }
+
+  auto filter = [&](const f32x4 &acc, int64_t j0) {
+    const int64_t j = j0 + col;
+    const bool valid = j < w1;
+    if (!p.group_shared) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const bool pass = valid && (4 * s + r) < p.G && acc[r] >= th[r];
+        const uint64_t bal = __ballot(pass);
+        const uint32_t gm = (uint32_t)(bal >> (16 * s)) & 0xFFFFu;
+        if (pass) {
+          const int slot = cnt[r] + __popc(gm & below);
+          if (slot < w.capw) cl[r][slot] = make_uint2(f2key(acc[r]), (uint32_t)j);
+        }
+        cnt[r] += __popc(gm);
+      }
+    } else {
+      const float gs = group_sum(acc);
+      const bool pass = valid && s == 0 && gs >= th[0];
+      const uint32_t gm = (uint32_t)__ballot(pass) & 0xFFFFu;
+      if (pass) {
+        const int slot = cnt[0] + __popc(gm & below);
+        if (slot < w.capw) cl[0][slot] = make_uint2(f2key(gs), (uint32_t)j);
+      }
+      cnt[0] += __popc(gm);
+    }
+  };
+
+  if constexpr (BF16) {
+    KFrag cur, nxt;
+    int64_t jl = w0 + col < w1 ? w0 + col : w1 - 1;
+    load_k_bf16(p.K, kv_offset(p.K, b, g, jl), cur);
+    nxt = cur;
+    for (int64_t j0 = w0; j0 < w1; j0 += kTile) {
+      const int64_t jn = j0 + kTile;
+      if (jn < w1) {
+        jl = jn + col < w1 ? jn + col : w1 - 1;
+        load_k_bf16(p.K, kv_offset(p.K, b, g, jl), nxt);
+      }
+      const f32x4 acc = mfma_scores(sc.qf, cur);
+      filter(acc, j0);
+      cur = nxt;
+    }
+  } else {
+    for (int64_t j0 = w0; j0 < w1; j0 += kTile) {
+      const int64_t jl = j0 + col < w1 ? j0 + col : w1 - 1;
+      filter(sc.score(p, b, g, jl), j0);
+    }
+  }
+
+  if (col == 0) {
+    if (!p.group_shared) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int h = 4 * s + r;
+        if (h < p.G)
+          w.counts[((int64_t)b * p.R + (int64_t)g * p.G + h) * w.nsub + sub] = cnt[r];
+      }
+    } else if (s == 0) {
+      w.counts[((int64_t)b * p.R + g) * w.nsub + sub] = cnt[0];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Full scores.  grid = (parts, B*Hkv).  dst[row][j] for j < L_b; with
+// FILL_TAIL, -inf for L_b <= j < ncap.  With ONLY_FLAGGED the workgroup does
+// nothing unless a row of its group is flagged (the exact fallback).
+// ---------------------------------------------------------------------------
+template <bool BF16, bool ONLY_FLAGGED, bool FILL_TAIL>
+__global__ __launch_bounds__(kBlock) void k_score_dense(Params p, Work w, float *dst, int64_t ld) {
+  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
+  const int bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
+  const int L = seq_len(p, b);
+  const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
+  const int nrows = p.group_shared ? 1 : p.G;
+  if constexpr (ONLY_FLAGGED) {
+    int any = 0;
+    for (int r = 0; r < nrows; ++r) any |= w.flags[row0 + r];
+    if (!any) return;  // uniform over the workgroup
+  }
+  Scorer<BF16> sc;
+  scorer_init<BF16>(p, b, g, sc, q_lds);
+  const int64_t end = FILL_TAIL ? p.ncap : (int64_t)L;
+  const int64_t ntiles = (end + kTile - 1) / kTile;
+  const int l = lane_id(), col = l & 15, s = l >> 4;
+  for (int64_t t = (int64_t)blockIdx.x * kWaves + wave_id(); t < ntiles;
+       t += (int64_t)gridDim.x * kWaves) {
+    const int64_t j = t * kTile + col;
+    const bool in_seq = j < L;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    if (t * kTile < L) acc = sc.score(p, b, g, in_seq ? j : (int64_t)L - 1);
+    const float ninf = -__builtin_inff();
+    if (!p.group_shared) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int h = 4 * s + r;
+        if (h < p.G && j < end) dst[(row0 + h) * ld + j] = in_seq ? acc[r] : ninf;
+      }
+    } else {
+      const float gs = group_sum(acc);
+      if (s == 0 && j < end) dst[row0 * ld + j] = in_seq ? gs : ninf;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Exact top-k of one row per workgroup.
+//   MODE 0: over the row's candidate lists (fused path); flags the row when
+//           the candidates do not prove exactness.
+//   MODE 1: over a full score row (sparse_decode_topk).
+//   MODE 2: over a full fallback score row, flagged rows only.
+// Output: idx[row][0..k) ascending positions, then -1; vals[row][...] the
+// kept scores (or -inf), when vals is not null.
+// ---------------------------------------------------------------------------
+struct DenseSrc {
+  const float *row;
+  __device__ __forceinline__ uint32_t key(int i) const { return f2key(row[i]); }
+  __device__ __forceinline__ uint2 get(int i) const { return make_uint2(f2key(row[i]), (uint32_t)i); }
+};
+
+struct LdsCands {
+  const uint32_t *keys;
+  const uint32_t *pos;
+  __device__ __forceinline__ uint32_t key(int i) const { return keys[i]; }
+  __device__ __forceinline__ uint2 get(int i) const { return make_uint2(keys[i], pos[i]); }
+};
+
+// Candidate lists read in place: item i lives in the last list s with
+// pre[s] <= i (empty lists share their successor's prefix value).
+struct GlobalCands {
+  const uint2 *lists;  // this row's lists, capw entries apart
+  const int *pre;      // LDS prefix sums, n_lists + 1 entries
+  int n_lists;
+  int capw;
+  __device__ __forceinline__ uint2 get(int i) const {
+    int lo = 0, hi = n_lists - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (pre[mid] <= i) lo = mid; else hi = mid - 1;
+    }
+    return lists[(int64_t)lo * capw + (i - pre[lo])];
+  }
+  __device__ __forceinline__ uint32_t key(int i) const { return get(i).x; }
+};
+
+template <class Src>
+__device__ __forceinline__ void select_and_write(const Src &src, int n, int k, uint32_t *hist,
+                                                 SelShared *sh, int32_t *irow, float *vrow) {
+  uint32_t T;
+  int need_eq;
+  radix_select(src, n, k, hist, sh, T, need_eq);
+  compact_selected(src, n, k, T, need_eq, sh->scan, [&](int pos, uint2 it) {
+    irow[pos] = (int32_t)it.y;
+    if (vrow) vrow[pos] = key2f(it.x);
+  });
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float *dense, int64_t ld,
+                                                   int32_t *idx, float *vals, int lds_cap) {
+  extern __shared__ uint32_t dyn[];
+  __shared__ uint32_t hist[2048];
+  __shared__ SelShared sh;
+  __shared__ int status;
+  const int row = blockIdx.x, b = row / p.R;
+  if (MODE == 2 && w.flags[row] == 0) return;
+  const int L = seq_len(p, b);
+  const int k = row_budget(p, b, L);
+  int32_t *irow = idx + (int64_t)row * p.k_max;
+  float *vrow = vals ? vals + (int64_t)row * p.k_max : nullptr;
+  const int tid = threadIdx.x;
+  if (k > 0) {
+    if (MODE == 0) {
+      const int n_lists = (L + kWaveKeys - 1) / kWaveKeys;
+      int *pre = (int *)dyn;  // n_lists + 1
+      uint32_t *ckey = dyn + (n_lists + 1);
+      uint32_t *cpos = ckey + lds_cap;
+      const int32_t *counts = w.counts + (int64_t)row * w.nsub;
+      if (tid == 0) status = 0;
+      __syncthreads();
+      int carry = 0;
+      for (int base = 0; base < n_lists; base += kBlock) {
+        const int s = base + tid;
+        const int c = s < n_lists ? counts[s] : 0;
+        if (c > w.capw) status = 1;  // a list overflowed
+        int tot;
+        const int e = block_excl_scan(c, sh.scan, &tot);
+        if (s < n_lists) pre[s] = carry + e;
+        carry += tot;
+      }
+      if (tid == 0) pre[n_lists] = carry;
+      __syncthreads();
+      const int total = carry;
+      if (status || total < k) {
+        if (tid == 0) {
+          w.flags[row] = 1;
+          atomicAdd(&w.stats[0], 1);
+        }
+        return;
+      }
+      const uint2 *lists = w.cand + (int64_t)row * w.nsub * w.capw;
+      GlobalCands gsrc{lists, pre, n_lists, w.capw};
+      if (total <= lds_cap) {
+        for (int i = tid; i < total; i += kBlock) {
+          const uint2 it = gsrc.get(i);
+          ckey[i] = it.x;
+          cpos[i] = it.y;
+        }
+        __syncthreads();
+        select_and_write(LdsCands{ckey, cpos}, total, k, hist, &sh, irow, vrow);
+      } else {
+        select_and_write(gsrc, total, k, hist, &sh, irow, vrow);
+      }
+    } else {
+      select_and_write(DenseSrc{dense + (int64_t)row * ld}, L, k, hist, &sh, irow, vrow);
+    }
+  }
+  for (int i = k + tid; i < p.k_max; i += kBlock) {
+    irow[i] = -1;
+    if (vrow) vrow[i] = -__builtin_inff();
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Gather-attend.  grid = (splits, rows).  Workgroup s of row (b, r) takes
+// list entries [s*kSplit, +kSplit) of idx[b][r]; in per-head mode the row is
+// query head r, in group-shared mode it serves the G heads of KV head r.
+// FUSED: the list holds exactly k_b valid positions and sigma their scores;
+// otherwise entries outside [0, L_b) are skipped and the logits recomputed.
+// Each wave walks four positions per step (16 lanes x 16 bytes = one 256-byte
+// bf16 value row); partials (m, l, o) of a split are merged by the last
+// workgroup of the row to arrive.
+// ---------------------------------------------------------------------------
+constexpr int kAttHeads = 8;  // heads accumulated per pass over the value rows
+
+template <bool BF16>
+__device__ __forceinline__ void load_row8(const void *base, int64_t off, int col, float v[8]) {
+  if constexpr (BF16) {
+    const u32x4 raw = *(const u32x4 *)((const uint16_t *)base + off + 8 * col);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = bf16_to_f32(raw[e] & 0xFFFFu);
+      v[2 * e + 1] = bf16_to_f32(raw[e] >> 16);
+    }
+  } else {
+    const float4 a = *(const float4 *)((const float *)base + off + 8 * col);
+    const float4 c = *(const float4 *)((const float *)base + off + 8 * col + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = c.x; v[5] = c.y; v[6] = c.z; v[7] = c.w;
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ void store_out(const Params &p, void *out, int64_t off, float v) {
+  if constexpr (BF16) ((uint16_t *)out)[off] = f32_to_bf16_rne(v);
+  else ((float *)out)[off] = v;
+}
+
+template <bool BF16, bool FUSED>
+__global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32_t *idx, void *out) {
+  __shared__ int32_t pos_l[kSplit];
+  __shared__ float z_l[kMaxGroup][kSplit];
+  __shared__ float q_l[kMaxGroup][kHeadDim];
+  __shared__ float red[kWaves][kAttHeads][kHeadDim];
+  __shared__ float lred[kWaves][kAttHeads];
+  __shared__ float mh[kMaxGroup];
+  __shared__ float ftmp[kWaves];
+  __shared__ int last;
+
+  const int s = blockIdx.x, row = blockIdx.y;
+  const int b = row / p.R, r = row % p.R;
+  const bool grp = p.group_shared;
+  const int nh = grp ? p.G : 1;
+  const int h0 = grp ? r * p.G : r;
+  const int g = grp ? r : r / p.G;
+  const int L = seq_len(p, b);
+  const int n_list = FUSED ? row_budget(p, b, L) : p.k_max;
+  const int nsp = (n_list + kSplit - 1) / kSplit;
+  const int tid = threadIdx.x, l = lane_id(), col = l & 15, sub = l >> 4, wv = wave_id();
+
+  if (n_list == 0) {  // nothing kept: zero output
+    if (s == 0)
+      for (int e = tid; e < nh * kHeadDim; e += kBlock)
+        store_out<BF16>(p, out, ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim, 0.f);
+    return;
+  }
+  if (s >= nsp) return;
+  const int e0 = s * kSplit;
+  const int n = (n_list - e0) < kSplit ? (n_list - e0) : kSplit;
+  const int32_t *irow = idx + (int64_t)row * p.k_max + e0;
+
+  // Positions of this split.
+  if (tid < kSplit) {
+    int32_t j = -1;
+    if (tid < n) {
+      j = irow[tid];
+      if (j < 0 || j >= L) j = -1;
+    }
+    pos_l[tid] = j;
+  }
+  const bool recompute = !FUSED || grp;
+  if (recompute) {
+    for (int e = tid; e < nh * kHeadDim; e += kBlock) {
+      const int64_t qo = ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim;
+      q_l[e / kHeadDim][e % kHeadDim] =
+          BF16 ? bf16_to_f32(((const uint16_t *)p.q)[qo]) : ((const float *)p.q)[qo];
+    }
+  }
+  __syncthreads();
+
+  // Logits z[h][t] = scale * q_h . K_j.
+  if (!recompute) {
+    if (tid < kSplit)
+      z_l[0][tid] = (tid < n && pos_l[tid] >= 0)
+                        ? p.scale * w.sigma[(int64_t)row * p.k_max + e0 + tid]
+                        : -__builtin_inff();
+  } else {
+    for (int t = wv * 4 + sub; t < kSplit; t += kWaves * 4) {
+      const int32_t j = pos_l[t];
+      if (j < 0) {  // uniform over the 16 lanes of this position
+        if (col == 0)
+          for (int h = 0; h < nh; ++h) z_l[h][t] = -__builtin_inff();
+        continue;
+      }
+      float kv[8];
+      load_row8<BF16>(p.K.base, kv_offset(p.K, b, g, j), col, kv);
+      for (int h = 0; h < nh; ++h) {
+        float d = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) d = fmaf(q_l[h][8 * col + e], kv[e], d);
+        d += __shfl_xor(d, 1);
+        d += __shfl_xor(d, 2);
+        d += __shfl_xor(d, 4);
+        d += __shfl_xor(d, 8);
+        if (col == 0) z_l[h][t] = p.scale * d;
+      }
+    }
+  }
+  __syncthreads();
+  for (int h = 0; h < nh; ++h) {
+    const float v = tid < kSplit ? z_l[h][tid] : -__builtin_inff();
+    const float m = block_max(v, ftmp);
+    if (tid == 0) mh[h] = m;
+  }
+  __syncthreads();
+
+  float *part = w.part;
+  for (int hb = 0; hb < nh; hb += kAttHeads) {
+    const int nb = (nh - hb) < kAttHeads ? (nh - hb) : kAttHeads;
+    float acc[kAttHeads][8];
+    float lsum[kAttHeads];
+#pragma unroll
+    for (int h = 0; h < kAttHeads; ++h) {
+      lsum[h] = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+    }
+    for (int t = wv * 4 + sub; t < n; t += kWaves * 4) {
+      const int32_t j = pos_l[t];
+      if (j < 0) continue;
+      float vv[8];
+      load_row8<BF16>(p.V.base, kv_offset(p.V, b, g, j), col, vv);
+#pragma unroll
+      for (int h = 0; h < kAttHeads; ++h) {
+        if (h < nb) {
+          const float e = expf(z_l[hb + h][t] - mh[hb + h]);
+          lsum[h] += e;
+#pragma unroll
+          for (int c = 0; c < 8; ++c) acc[h][c] = fmaf(e, vv[c], acc[h][c]);
+        }
+      }
+    }
+    // Reduce over the four positions a wave handles per step, then over waves.
+#pragma unroll
+    for (int h = 0; h < kAttHeads; ++h) {
+      if (h < nb) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          float v = acc[h][c];
+          v += __shfl_xor(v, 16);
+          v += __shfl_xor(v, 32);
+          acc[h][c] = v;
+        }
+        float ls = lsum[h];
+        ls += __shfl_xor(ls, 16);
+        ls += __shfl_xor(ls, 32);
+        if (sub == 0) {
+#pragma unroll
+          for (int c = 0; c < 8; ++c) red[wv][h][8 * col + c] = acc[h][c];
+          if (col == 0) lred[wv][h] = ls;
+        }
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < nb * kHeadDim; e += kBlock) {
+      const int h = e / kHeadDim, c = e % kHeadDim;
+      float o = 0.f, ls = 0.f;
+#pragma unroll
+      for (int v = 0; v < kWaves; ++v) {
+        o += red[v][h][c];
+        ls += lred[v][h];
+      }
+      const int hq = h0 + hb + h;
+      if (nsp == 1) {
+        store_out<BF16>(p, out, ((int64_t)b * p.Hq + hq) * kHeadDim + c, ls > 0.f ? o / ls : 0.f);
+      } else {
+        float *pp = part + (((int64_t)b * p.Hq + hq) * w.nsplit + s) * kPartStride;
+        if (c == 0) {
+          pp[0] = mh[hb + h];
+          pp[1] = ls;
+        }
+        pp[2 + c] = o;
+      }
+    }
+    __syncthreads();
+  }
+  if (nsp == 1) return;
+
+  // The last split of the row to finish merges all partials.
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) {
+    const int prev = __hip_atomic_fetch_add(&w.done[row], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    last = prev == nsp - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  for (int e = tid; e < nh * kHeadDim; e += kBlock) {
+    const int h = e / kHeadDim, c = e % kHeadDim;
+    const float *pp = part + ((int64_t)b * p.Hq + h0 + h) * w.nsplit * kPartStride;
+    float M = -__builtin_inff();
+    for (int q = 0; q < nsp; ++q) M = fmaxf(M, pp[q * kPartStride]);
+    float o = 0.f, ls = 0.f;
+    if (M != -__builtin_inff()) {
+      for (int q = 0; q < nsp; ++q) {
+        const float f = expf(pp[q * kPartStride] - M);
+        ls += f * pp[q * kPartStride + 1];
+        o += f * pp[q * kPartStride + 2 + c];
+      }
+    }
+    store_out<BF16>(p, out, ((int64_t)b * p.Hq + h0 + h) * kHeadDim + c, ls > 0.f ? o / ls : 0.f);
+  }
+  if (tid == 0) w.done[row] = 0;
+}
+
+__global__ void k_fill_i32(int32_t *dst, int64_t n, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = v;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (host).
+// ---------------------------------------------------------------------------
+static inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+
+hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
+  const dim3 g1(8, p.B * p.Hkv);
+  if (p.bf16) k_pilot_score<true><<<g1, kBlock, 0, st>>>(p, w);
+  else k_pilot_score<false><<<g1, kBlock, 0, st>>>(p, w);
+  k_pilot_select<<<p.B * p.R, kBlock, 0, st>>>(p, w);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_filter(const Params &p, const Work &w, hipStream_t st) {
+  const dim3 grid(cdiv(p.ncap, kChunkKeys), p.B * p.Hkv);
+  if (p.bf16) k_score_filter<true><<<grid, kBlock, 0, st>>>(p, w);
+  else k_score_filter<false><<<grid, kBlock, 0, st>>>(p, w);
+  return hipGetLastError();
+}
+
+size_t select_lds_bytes(const Params &p, int lds_cap) {
+  const int n_lists = (int)cdiv(p.ncap, kWaveKeys);
+  return (size_t)(n_lists + 1) * 4 + (size_t)lds_cap * 8;
+}
+
+hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
+                                    hipStream_t st) {
+  const size_t lds = select_lds_bytes(p, lds_cap);
+  k_select<0><<<p.B * p.R, kBlock, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
+  return hipGetLastError();
+}
+
+hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream_t st) {
+  const dim3 grid(kRepairParts, p.B * p.Hkv);
+  if (p.bf16) k_score_dense<true, true, false><<<grid, kBlock, 0, st>>>(p, w, w.dense, p.ncap);
+  else k_score_dense<false, true, false><<<grid, kBlock, 0, st>>>(p, w, w.dense, p.ncap);
+  k_select<2><<<p.B * p.R, kBlock, 0, st>>>(p, w, w.dense, p.ncap, idx, w.sigma, 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
+                         hipStream_t st) {
+  if (!fused) {
+    const int64_t rows = (int64_t)p.B * p.R;
+    k_fill_i32<<<cdiv(rows, 256), 256, 0, st>>>(w.done, rows, 0);
+  }
+  const dim3 grid(w.nsplit, p.B * p.R);
+  if (p.bf16) {
+    if (fused) k_attend<true, true><<<grid, kBlock, 0, st>>>(p, w, idx, out);
+    else k_attend<true, false><<<grid, kBlock, 0, st>>>(p, w, idx, out);
+  } else {
+    if (fused) k_attend<false, true><<<grid, kBlock, 0, st>>>(p, w, idx, out);
+    else k_attend<false, false><<<grid, kBlock, 0, st>>>(p, w, idx, out);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st) {
+  const dim3 grid(cdiv(p.ncap, kChunkKeys), p.B * p.Hkv);
+  Work none{};
+  if (p.bf16) k_score_dense<true, false, true><<<grid, kBlock, 0, st>>>(p, none, scores, p.ncap);
+  else k_score_dense<false, false, true><<<grid, kBlock, 0, st>>>(p, none, scores, p.ncap);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk(const Params &p, const float *scores, int32_t *idx, float *vals,
+                       hipStream_t st) {
+  Work none{};
+  k_select<1><<<p.B * p.R, kBlock, 0, st>>>(p, none, scores, p.ncap, idx, vals, 0);
+  return hipGetLastError();
+}
+
+}  // namespace sd

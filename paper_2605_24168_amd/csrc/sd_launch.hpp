@@ -1,0 +1,22 @@
+// sd_launch.hpp -- host launchers of the kernels in sd_kernels.hip.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "sd_internal.hpp"
+
+namespace sd {
+
+hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st);
+hipError_t launch_score_filter(const Params &p, const Work &w, hipStream_t st);
+size_t select_lds_bytes(const Params &p, int lds_cap);
+hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
+                                    hipStream_t st);
+hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream_t st);
+hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
+                         hipStream_t st);
+hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st);
+hipError_t launch_topk(const Params &p, const float *scores, int32_t *idx, float *vals,
+                       hipStream_t st);
+
+}  // namespace sd
