@@ -171,11 +171,11 @@ sd::Params make_params(const sd_tensor *q, const sd_kv *K, const sd_kv *V, const
 // Workspace layout.  Sizes depend only on the shapes, so the same layout is
 // recomputed on every call.
 struct Layout {
-  size_t sample, theta, counts, cand, flags, dense, sigma, part, done, stats, total;
+  size_t sample, theta, counts, cand, flags, dense, sigma, part, stats, total;
   int nsub, capw, nsplit;
 };
 
-Layout layout_for(const Shape &s, int64_t k_max, bool fused) {
+Layout layout_for(const Shape &s, int64_t k_max, bool fused, int group_shared) {
   Layout L{};
   const int64_t rows = (int64_t)s.B * s.R;
   L.nsub = (int)((s.ncap + sd::kWaveKeys - 1) / sd::kWaveKeys);
@@ -185,8 +185,13 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused) {
   capw = (capw + 15) / 16 * 16;
   if (capw > sd::kWaveKeys) capw = sd::kWaveKeys;
   L.capw = capw;
-  L.nsplit = (int)((k_max + sd::kSplit - 1) / sd::kSplit);
-  if (L.nsplit < 1) L.nsplit = 1;
+  sd::Params shape_only{};
+  shape_only.B = s.B;
+  shape_only.R = s.R;
+  shape_only.G = s.G;
+  shape_only.group_shared = group_shared;
+  shape_only.k_max = (int32_t)k_max;
+  L.nsplit = sd::attend_nsplit(shape_only);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -203,7 +208,6 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused) {
     L.sigma = take((size_t)rows * k_max * 4);
   }
   L.part = take((size_t)s.B * s.Hq * L.nsplit * sd::kPartStride * 4);
-  L.done = take((size_t)rows * 4);
   L.stats = take(64);
   L.total = off;
   return L;
@@ -245,7 +249,6 @@ sd::Work carve(char *base, const Layout &L, bool fused) {
     w.sigma = (float *)(base + L.sigma);
   }
   w.part = (float *)(base + L.part);
-  w.done = (int32_t *)(base + L.done);
   w.stats = (int32_t *)(base + L.stats);
   w.nsub = L.nsub;
   w.capw = L.capw;
@@ -296,7 +299,7 @@ sd_status sparse_decode_workspace_size(const sd_tensor *q, const sd_kv *K, const
   int64_t k_max = 0;
   st = check_idx(idx, s, sp, k_max);
   if (st) return st;
-  *bytes = layout_for(s, k_max, true).total;
+  *bytes = layout_for(s, k_max, true, sp->group_shared ? 1 : 0).total;
   return SD_OK;
 }
 
@@ -384,7 +387,7 @@ sd_status sparse_decode_attend(const sd_tensor *q, const sd_kv *K, const sd_kv *
   if (s.B == 0) return SD_OK;
   if (!seq_lens || (k_max > 0 && !idx->data)) return SD_ERR_INVALID_ARG;
   std::lock_guard<std::mutex> lk(g_mu);
-  const Layout L = layout_for(s, k_max, false);
+  const Layout L = layout_for(s, k_max, false, sp->group_shared ? 1 : 0);
   DevState *ds = nullptr;
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
@@ -411,7 +414,7 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   if (!seq_lens) return SD_ERR_INVALID_ARG;
   const hipStream_t stream_h = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_mu);
-  const Layout L = layout_for(s, k_max, true);
+  const Layout L = layout_for(s, k_max, true, sp->group_shared ? 1 : 0);
   DevState *ds = nullptr;
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);

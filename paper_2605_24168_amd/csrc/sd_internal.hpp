@@ -18,7 +18,6 @@ constexpr int kMaxGroup = 16;      // query heads per KV head handled by one MFM
 constexpr int kChunkKeys = 8192;   // keys one scoring workgroup streams
 constexpr int kWaveKeys = kChunkKeys / kWaves;
 constexpr int kSampleMax = 4096;   // pilot samples per row
-constexpr int kSplit = 256;        // kept positions per attend workgroup
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
 constexpr int kRepairParts = 64;   // workgroups per (sequence, KV head) in the repair stream
 
@@ -63,7 +62,6 @@ struct Work {
   float *dense;      // [rows][ncap] fallback scores
   float *sigma;      // [rows][k_max] kept scores, aligned with idx
   float *part;       // [B*Hq][nsplit][kPartStride] attend partials
-  int32_t *done;     // [rows] attend arrival counters (zeroed by the pilot)
   int32_t *stats;    // [4]: [0] rows repaired in the last call
   int32_t nsub;
   int32_t capw;
@@ -296,7 +294,9 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t dig, bool act)
 // passes over 11, 11 and 10 key bits.  src.key(p) returns item p's key.
 // On return T is the k-th largest key and need_eq the number of items equal
 // to T that belong to the top k (the others with key == T are the later ones
-// in item order).  hist: LDS uint32[2048]; sh: LDS scratch.
+// in item order).  hist: LDS uint32[2048]; sh: LDS scratch.  With passes < 3
+// only the top bits of T are resolved (the rest are zero): T is then a lower
+// bound of the k-th largest key.
 // ---------------------------------------------------------------------------
 struct SelShared {
   int scan[kWaves];
@@ -306,12 +306,12 @@ struct SelShared {
 
 template <class Src>
 __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelShared *sh,
-                             uint32_t &T, int &need_eq) {
+                             uint32_t &T, int &need_eq, int passes = 3) {
   uint32_t prefix = 0, mask = 0;
   int krem = k;
   const int tid = threadIdx.x;
 #pragma unroll 1
-  for (int pass = 0; pass < 3; ++pass) {
+  for (int pass = 0; pass < passes; ++pass) {
     const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
     const int nb = pass == 2 ? 1024 : 2048;
     const uint32_t dmask = (uint32_t)nb - 1u;

@@ -15,8 +15,9 @@
 //                   cannot prove exactness is flagged for the fallback
 //   k_score_dense   (fallback) full scores of the flagged rows' groups
 //   k_select        (fallback) exact top-k over those full scores
-//   k_attend        gathers the kept value rows, split over workgroups, and
-//                   merges the (max, sum, output) partials by log-sum-exp
+//   k_attend        gathers the kept value rows, split over workgroups
+//   k_merge         combines the splits' (max, sum, output) partials by
+//                   log-sum-exp
 // The threshold is only a filter: the selection is exact whenever every
 // kept position passed it, which holds iff at least k candidates passed
 // (then the k-th largest candidate is >= the threshold, so nothing above
@@ -110,7 +111,6 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   const int k = row_budget(p, b, L);
   if (threadIdx.x == 0) {
     w.flags[row] = 0;
-    w.done[row] = 0;
     if (row == 0) w.stats[0] = 0;
   }
   if (k == 0 || w.force_repair) {
@@ -130,7 +130,9 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __syncthreads();
   uint32_t T;
   int need_eq;
-  radix_select(LdsKeys{keys}, m, r, hist, &sh, T, need_eq);
+  // Two histogram passes fix the top 22 key bits of the r-th largest sample;
+  // the threshold is the lowest key with those bits (at or below it).
+  radix_select(LdsKeys{keys}, m, r, hist, &sh, T, need_eq, 2);
   if (threadIdx.x == 0) w.theta[row] = key2f(T);
 }
 
@@ -381,10 +383,15 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
       const uint2 *lists = w.cand + (int64_t)row * w.nsub * w.capw;
       GlobalCands gsrc{lists, pre, n_lists, w.capw};
       if (total <= lds_cap) {
-        for (int i = tid; i < total; i += kBlock) {
-          const uint2 it = gsrc.get(i);
-          ckey[i] = it.x;
-          cpos[i] = it.y;
+        // One wave per list: the list's entries are contiguous in memory.
+        for (int sl = wave_id(); sl < n_lists; sl += kWaves) {
+          const int c0 = pre[sl], cnt = pre[sl + 1] - c0;
+          const uint2 *src = lists + (int64_t)sl * w.capw;
+          for (int e = lane_id(); e < cnt; e += 64) {
+            const uint2 it = src[e];
+            ckey[c0 + e] = it.x;
+            cpos[c0 + e] = it.y;
+          }
         }
         __syncthreads();
         select_and_write(LdsCands{ckey, cpos}, total, k, hist, &sh, irow, vrow);
@@ -403,15 +410,18 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
 
 // ---------------------------------------------------------------------------
 // Gather-attend.  grid = (splits, rows).  Workgroup s of row (b, r) takes
-// list entries [s*kSplit, +kSplit) of idx[b][r]; in per-head mode the row is
+// list entries [s*split, +split) of idx[b][r]; in per-head mode the row is
 // query head r, in group-shared mode it serves the G heads of KV head r.
 // FUSED: the list holds exactly k_b valid positions and sigma their scores;
-// otherwise entries outside [0, L_b) are skipped and the logits recomputed.
-// Each wave walks four positions per step (16 lanes x 16 bytes = one 256-byte
-// bf16 value row); partials (m, l, o) of a split are merged by the last
-// workgroup of the row to arrive.
+// otherwise entries outside [0, L_b) are skipped and the logits recomputed
+// from the key rows.  The softmax weights exp(z - max) are formed once per
+// position in LDS; each wave then walks sixteen positions per step (four
+// per 16-lane group, loads issued together), 16 lanes x 16 bytes covering one
+// 256-byte bf16 value row.  A row split over several workgroups leaves
+// (max, sum, unnormalised output) partials that k_merge combines.
 // ---------------------------------------------------------------------------
 constexpr int kAttHeads = 8;  // heads accumulated per pass over the value rows
+constexpr int kGatherUnroll = 4;
 
 template <bool BF16>
 __device__ __forceinline__ void load_row8(const void *base, int64_t off, int col, float v[8]) {
@@ -431,21 +441,24 @@ __device__ __forceinline__ void load_row8(const void *base, int64_t off, int col
 }
 
 template <bool BF16>
-__device__ __forceinline__ void store_out(const Params &p, void *out, int64_t off, float v) {
+__device__ __forceinline__ void store_out(void *out, int64_t off, float v) {
   if constexpr (BF16) ((uint16_t *)out)[off] = f32_to_bf16_rne(v);
   else ((float *)out)[off] = v;
 }
 
+__device__ __forceinline__ int attend_list_len(const Params &p, int b, int L, bool fused) {
+  return fused ? row_budget(p, b, L) : p.k_max;
+}
+
 template <bool BF16, bool FUSED>
-__global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32_t *idx, void *out) {
-  __shared__ int32_t pos_l[kSplit];
-  __shared__ float z_l[kMaxGroup][kSplit];
+__global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32_t *idx, void *out,
+                                                   int split) {
+  extern __shared__ float att_dyn[];  // e[nh][split], then pos[split]
   __shared__ float q_l[kMaxGroup][kHeadDim];
   __shared__ float red[kWaves][kAttHeads][kHeadDim];
   __shared__ float lred[kWaves][kAttHeads];
   __shared__ float mh[kMaxGroup];
   __shared__ float ftmp[kWaves];
-  __shared__ int last;
 
   const int s = blockIdx.x, row = blockIdx.y;
   const int b = row / p.R, r = row % p.R;
@@ -454,29 +467,27 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   const int h0 = grp ? r * p.G : r;
   const int g = grp ? r : r / p.G;
   const int L = seq_len(p, b);
-  const int n_list = FUSED ? row_budget(p, b, L) : p.k_max;
-  const int nsp = (n_list + kSplit - 1) / kSplit;
+  const int n_list = attend_list_len(p, b, L, FUSED);
+  const int nsp = (n_list + split - 1) / split;
   const int tid = threadIdx.x, l = lane_id(), col = l & 15, sub = l >> 4, wv = wave_id();
+  float *e_l = att_dyn;
+  int32_t *pos_l = (int32_t *)(att_dyn + nh * split);
 
   if (n_list == 0) {  // nothing kept: zero output
     if (s == 0)
       for (int e = tid; e < nh * kHeadDim; e += kBlock)
-        store_out<BF16>(p, out, ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim, 0.f);
+        store_out<BF16>(out, ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim, 0.f);
     return;
   }
   if (s >= nsp) return;
-  const int e0 = s * kSplit;
-  const int n = (n_list - e0) < kSplit ? (n_list - e0) : kSplit;
+  const int e0 = s * split;
+  const int n = (n_list - e0) < split ? (n_list - e0) : split;
   const int32_t *irow = idx + (int64_t)row * p.k_max + e0;
 
-  // Positions of this split.
-  if (tid < kSplit) {
-    int32_t j = -1;
-    if (tid < n) {
-      j = irow[tid];
-      if (j < 0 || j >= L) j = -1;
-    }
-    pos_l[tid] = j;
+  for (int t = tid; t < n; t += kBlock) {
+    int32_t j = irow[t];
+    if (j < 0 || j >= L) j = -1;
+    pos_l[t] = j;
   }
   const bool recompute = !FUSED || grp;
   if (recompute) {
@@ -488,18 +499,16 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   }
   __syncthreads();
 
-  // Logits z[h][t] = scale * q_h . K_j.
+  // Logits z[h][t] = scale * q_h . K_j (kept in e_l until the max is known).
   if (!recompute) {
-    if (tid < kSplit)
-      z_l[0][tid] = (tid < n && pos_l[tid] >= 0)
-                        ? p.scale * w.sigma[(int64_t)row * p.k_max + e0 + tid]
-                        : -__builtin_inff();
+    const float *srow = w.sigma + (int64_t)row * p.k_max + e0;
+    for (int t = tid; t < n; t += kBlock) e_l[t] = pos_l[t] >= 0 ? p.scale * srow[t] : -__builtin_inff();
   } else {
-    for (int t = wv * 4 + sub; t < kSplit; t += kWaves * 4) {
+    for (int t = wv * 4 + sub; t < n; t += kWaves * 4) {
       const int32_t j = pos_l[t];
       if (j < 0) {  // uniform over the 16 lanes of this position
         if (col == 0)
-          for (int h = 0; h < nh; ++h) z_l[h][t] = -__builtin_inff();
+          for (int h = 0; h < nh; ++h) e_l[h * split + t] = -__builtin_inff();
         continue;
       }
       float kv[8];
@@ -512,19 +521,26 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
         d += __shfl_xor(d, 2);
         d += __shfl_xor(d, 4);
         d += __shfl_xor(d, 8);
-        if (col == 0) z_l[h][t] = p.scale * d;
+        if (col == 0) e_l[h * split + t] = p.scale * d;
       }
     }
   }
   __syncthreads();
   for (int h = 0; h < nh; ++h) {
-    const float v = tid < kSplit ? z_l[h][tid] : -__builtin_inff();
-    const float m = block_max(v, ftmp);
+    float m = -__builtin_inff();
+    for (int t = tid; t < n; t += kBlock) m = fmaxf(m, e_l[h * split + t]);
+    m = block_max(m, ftmp);
     if (tid == 0) mh[h] = m;
   }
   __syncthreads();
+  // Weights exp(z - m); skipped entries (z = -inf) give 0.
+  for (int e = tid; e < nh * n; e += kBlock) {
+    const int h = e / n, t = e % n;
+    const float z = e_l[h * split + t];
+    e_l[h * split + t] = z == -__builtin_inff() ? 0.f : expf(z - mh[h]);
+  }
+  __syncthreads();
 
-  float *part = w.part;
   for (int hb = 0; hb < nh; hb += kAttHeads) {
     const int nb = (nh - hb) < kAttHeads ? (nh - hb) : kAttHeads;
     float acc[kAttHeads][8];
@@ -533,24 +549,32 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     for (int h = 0; h < kAttHeads; ++h) {
       lsum[h] = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[h][e] = 0.f;
+      for (int c = 0; c < 8; ++c) acc[h][c] = 0.f;
     }
-    for (int t = wv * 4 + sub; t < n; t += kWaves * 4) {
-      const int32_t j = pos_l[t];
-      if (j < 0) continue;
-      float vv[8];
-      load_row8<BF16>(p.V.base, kv_offset(p.V, b, g, j), col, vv);
+    for (int t0 = wv * 4 * kGatherUnroll; t0 < n; t0 += kWaves * 4 * kGatherUnroll) {
+      float vv[kGatherUnroll][8];
+      int tt[kGatherUnroll];
 #pragma unroll
-      for (int h = 0; h < kAttHeads; ++h) {
-        if (h < nb) {
-          const float e = expf(z_l[hb + h][t] - mh[hb + h]);
-          lsum[h] += e;
+      for (int u = 0; u < kGatherUnroll; ++u) {
+        const int t = t0 + 4 * u + sub;
+        tt[u] = (t < n && pos_l[t] >= 0) ? t : -1;
+        if (tt[u] >= 0) load_row8<BF16>(p.V.base, kv_offset(p.V, b, g, pos_l[t]), col, vv[u]);
+      }
 #pragma unroll
-          for (int c = 0; c < 8; ++c) acc[h][c] = fmaf(e, vv[c], acc[h][c]);
+      for (int u = 0; u < kGatherUnroll; ++u) {
+        if (tt[u] < 0) continue;
+#pragma unroll
+        for (int h = 0; h < kAttHeads; ++h) {
+          if (h < nb) {
+            const float e = e_l[(hb + h) * split + tt[u]];
+            lsum[h] += e;
+#pragma unroll
+            for (int c = 0; c < 8; ++c) acc[h][c] = fmaf(e, vv[u][c], acc[h][c]);
+          }
         }
       }
     }
-    // Reduce over the four positions a wave handles per step, then over waves.
+    // Reduce over the four position groups of a wave, then over waves.
 #pragma unroll
     for (int h = 0; h < kAttHeads; ++h) {
       if (h < nb) {
@@ -582,9 +606,9 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
       }
       const int hq = h0 + hb + h;
       if (nsp == 1) {
-        store_out<BF16>(p, out, ((int64_t)b * p.Hq + hq) * kHeadDim + c, ls > 0.f ? o / ls : 0.f);
+        store_out<BF16>(out, ((int64_t)b * p.Hq + hq) * kHeadDim + c, ls > 0.f ? o / ls : 0.f);
       } else {
-        float *pp = part + (((int64_t)b * p.Hq + hq) * w.nsplit + s) * kPartStride;
+        float *pp = w.part + (((int64_t)b * p.Hq + hq) * w.nsplit + s) * kPartStride;
         if (c == 0) {
           pp[0] = mh[hb + h];
           pp[1] = ls;
@@ -594,39 +618,32 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     }
     __syncthreads();
   }
-  if (nsp == 1) return;
-
-  // The last split of the row to finish merges all partials.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const int prev = __hip_atomic_fetch_add(&w.done[row], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    last = prev == nsp - 1;
-  }
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  for (int e = tid; e < nh * kHeadDim; e += kBlock) {
-    const int h = e / kHeadDim, c = e % kHeadDim;
-    const float *pp = part + ((int64_t)b * p.Hq + h0 + h) * w.nsplit * kPartStride;
-    float M = -__builtin_inff();
-    for (int q = 0; q < nsp; ++q) M = fmaxf(M, pp[q * kPartStride]);
-    float o = 0.f, ls = 0.f;
-    if (M != -__builtin_inff()) {
-      for (int q = 0; q < nsp; ++q) {
-        const float f = expf(pp[q * kPartStride] - M);
-        ls += f * pp[q * kPartStride + 1];
-        o += f * pp[q * kPartStride + 2 + c];
-      }
-    }
-    store_out<BF16>(p, out, ((int64_t)b * p.Hq + h0 + h) * kHeadDim + c, ls > 0.f ? o / ls : 0.f);
-  }
-  if (tid == 0) w.done[row] = 0;
 }
 
-__global__ void k_fill_i32(int32_t *dst, int64_t n, int32_t v) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) dst[i] = v;
+// Log-sum-exp merge of split partials: grid = B*Hq output rows, 128 threads
+// (one per channel).  Rows that fit one split were written by k_attend.
+template <bool BF16, bool FUSED>
+__global__ __launch_bounds__(kHeadDim) void k_merge(Params p, Work w, void *out, int split) {
+  const int bh = blockIdx.x, b = bh / p.Hq, h = bh % p.Hq;
+  const int r = p.group_shared ? h / p.G : h;
+  (void)r;
+  const int L = seq_len(p, b);
+  const int n_list = attend_list_len(p, b, L, FUSED);
+  const int nsp = (n_list + split - 1) / split;
+  if (nsp <= 1) return;
+  const int c = threadIdx.x;
+  const float *pp = w.part + (int64_t)bh * w.nsplit * kPartStride;
+  float M = -__builtin_inff();
+  for (int q = 0; q < nsp; ++q) M = fmaxf(M, pp[q * kPartStride]);
+  float o = 0.f, ls = 0.f;
+  if (M != -__builtin_inff()) {
+    for (int q = 0; q < nsp; ++q) {
+      const float f = expf(pp[q * kPartStride] - M);
+      ls += f * pp[q * kPartStride + 1];
+      o += f * pp[q * kPartStride + 2 + c];
+    }
+  }
+  store_out<BF16>(out, (int64_t)bh * kHeadDim + c, ls > 0.f ? o / ls : 0.f);
 }
 
 // ---------------------------------------------------------------------------
@@ -669,19 +686,51 @@ hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream
   return hipGetLastError();
 }
 
+int attend_split(const Params &p, int nsplit_max_positions) {
+  // Positions per attend workgroup: enough workgroups to fill the chip
+  // (about 2048), at least 64 positions each, LDS-bounded in group mode.
+  const int64_t rows = (int64_t)p.B * p.R;
+  const int64_t k_max = nsplit_max_positions > 0 ? nsplit_max_positions : 1;
+  int64_t nsplit = (2048 + rows - 1) / rows;
+  const int64_t most = (k_max + 63) / 64;
+  if (nsplit > most) nsplit = most;
+  if (nsplit < 1) nsplit = 1;
+  int64_t split = (k_max + nsplit - 1) / nsplit;
+  split = (split + 63) / 64 * 64;
+  const int nh = p.group_shared ? p.G : 1;
+  const int64_t lds_limit = (48 * 1024 / 4) / (nh + 1) / 64 * 64;  // e[nh][split] + pos[split]
+  if (split > lds_limit) split = lds_limit;
+  return (int)split;
+}
+
+int attend_nsplit(const Params &p) {
+  const int split = attend_split(p, p.k_max);
+  const int64_t k_max = p.k_max > 0 ? p.k_max : 1;
+  return (int)((k_max + split - 1) / split);
+}
+
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st) {
-  if (!fused) {
-    const int64_t rows = (int64_t)p.B * p.R;
-    k_fill_i32<<<cdiv(rows, 256), 256, 0, st>>>(w.done, rows, 0);
-  }
+  const int split = attend_split(p, p.k_max);
+  const int nh = p.group_shared ? p.G : 1;
+  const size_t lds = (size_t)(nh + 1) * split * 4;
   const dim3 grid(w.nsplit, p.B * p.R);
   if (p.bf16) {
-    if (fused) k_attend<true, true><<<grid, kBlock, 0, st>>>(p, w, idx, out);
-    else k_attend<true, false><<<grid, kBlock, 0, st>>>(p, w, idx, out);
+    if (fused) k_attend<true, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    else k_attend<true, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
   } else {
-    if (fused) k_attend<false, true><<<grid, kBlock, 0, st>>>(p, w, idx, out);
-    else k_attend<false, false><<<grid, kBlock, 0, st>>>(p, w, idx, out);
+    if (fused) k_attend<false, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    else k_attend<false, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+  }
+  if (w.nsplit > 1) {
+    const unsigned rows = (unsigned)(p.B * p.Hq);
+    if (p.bf16) {
+      if (fused) k_merge<true, true><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
+      else k_merge<true, false><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
+    } else {
+      if (fused) k_merge<false, true><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
+      else k_merge<false, false><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
+    }
   }
   return hipGetLastError();
 }
