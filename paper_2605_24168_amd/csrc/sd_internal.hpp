@@ -174,6 +174,42 @@ __device__ __forceinline__ void load_k_bf16(const KvView &K, int64_t off, KFrag 
   for (int kk = 0; kk < 4; ++kk) kf.v[kk] = __builtin_nontemporal_load((const u32x4 *)(kp + 32 * kk));
 }
 
+// ---------------------------------------------------------------------------
+// Coalesced tile loads.  Loading a tile straight into the MFMA layout makes
+// every instruction touch 16 rows x 64 bytes; loading it with four fully
+// coalesced 1 KB instructions (one 256-byte key row per 16-lane group) and
+// re-reading it from LDS in the MFMA layout streams measurably faster.
+// Instruction t (0..3), lane l = 16a + lo loads 16-byte chunk
+// c = (lo - 4t - a) mod 16 of tile row 4t + a and stores it to LDS slot
+// 64t + l, so the LDS writes are contiguous, and the MFMA read of chunk c of
+// row 4t + a (slot 64t + 16a + ((4t + a + c) mod 16)) has each 16-lane group
+// spread over all LDS banks.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int swz_chunk(int t) {
+  const int l = lane_id();
+  return ((l & 15) - 4 * t - (l >> 4)) & 15;
+}
+
+// row_ptr(r) is the address of tile row r (0..15) as a byte pointer.
+template <class RowPtr>
+__device__ __forceinline__ void load_tile_coalesced(RowPtr row_ptr, u32x4 v[4]) {
+  const int a = lane_id() >> 4;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    v[t] = __builtin_nontemporal_load((const u32x4 *)(row_ptr(4 * t + a) + 16 * swz_chunk(t)));
+}
+
+__device__ __forceinline__ void stage_tile(u32x4 *wl, const u32x4 v[4]) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) wl[64 * t + lane_id()] = v[t];
+}
+
+__device__ __forceinline__ void read_kfrag(const u32x4 *wl, KFrag &kf) {
+  const int L = lane_id(), r = L & 15, s = L >> 4, t = r >> 2, a = r & 3;
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) kf.v[kk] = wl[64 * t + 16 * a + ((4 * t + a + 4 * kk + s) & 15)];
+}
+
 __device__ __forceinline__ f32x4 mfma_scores(const QFrag &qf, const KFrag &kf) {
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -317,15 +353,21 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
     const uint32_t dmask = (uint32_t)nb - 1u;
     for (int i = tid; i < nb; i += kBlock) hist[i] = 0;
     __syncthreads();
-    for (int base = 0; base < n; base += kBlock) {
-      const int p = base + tid;
-      uint32_t key = 0;
-      bool act = false;
-      if (p < n) {
-        key = src.key(p);
-        act = (key & mask) == prefix;
+    if (pass == 0) {
+      // The leading bits of the items cluster in a few bins: count lanes
+      // sharing a bin with one atomic.
+      for (int base = 0; base < n; base += kBlock) {
+        const int p = base + tid;
+        uint32_t key = 0;
+        if (p < n) key = src.key(p);
+        hist_add(hist, (key >> shift) & dmask, p < n);
       }
-      hist_add(hist, (key >> shift) & dmask, act);
+    } else {
+      // Lower bits spread over many bins: plain LDS atomics.
+      for (int p = tid; p < n; p += kBlock) {
+        const uint32_t key = src.key(p);
+        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1u);
+      }
     }
     __syncthreads();
     // Thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top.

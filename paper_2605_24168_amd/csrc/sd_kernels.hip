@@ -7,7 +7,7 @@
 //   k_pilot_score   scores a strided sample of <= 4096 keys per row
 //   k_pilot_select  picks a per-row threshold from the sample (aimed at about
 //                   2.5 k candidates) and clears the per-row state
-//   k_score_filter  streams every key once (MFMA scoring, one K tile shared
+//   k_score_stream  streams every key once (MFMA scoring, one K tile shared
 //                   by all query heads of the group) and appends the keys at
 //                   or above the threshold to per-wave candidate lists, in
 //                   position order, with ballots instead of atomics
@@ -139,20 +139,179 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
 // ---------------------------------------------------------------------------
 // The scoring stream.  grid = (ceil(ncap / kChunkKeys), B*Hkv).  Wave v of
 // workgroup c streams keys [c*kChunkKeys + v*kWaveKeys, +kWaveKeys) of one
-// (sequence, KV head) in 16-key MFMA tiles, one tile ahead in registers, and
+// (sequence, KV head) in 16-key MFMA tiles, kDepth tiles in flight, and
 // writes its candidates of every row of the group to its own list
 // cand[row][c*4+v][0..capw) in position order; counts[row][c*4+v] gets the
-// number that passed (which may exceed capw: overflow).
+// number that passed (more than capw means the list overflowed).  Passing
+// keys are staged in LDS and written out in batches, so the streaming loop
+// issues no global stores and its load waits stay exact.
 // ---------------------------------------------------------------------------
-template <bool BF16>
-__global__ __launch_bounds__(kBlock) void k_score_filter(Params p, Work w) {
-  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
+constexpr int kDepth = 3;        // tiles in flight per wave
+constexpr int kCandBuf = 1024;   // candidates staged per wave
+constexpr int kWavePages = kWaveKeys / kTile;
+
+struct WaveLds {
+  u32x4 tile[256];
+  uint32_t cval[kCandBuf + 64];   // raw float32 score bits (+64 discard slots)
+  uint32_t cmeta[kCandBuf + 64];  // (head in group << 24) | position within the wave's range
+  int32_t page[kWavePages];
+  int32_t base[kMaxGroup];        // candidates already written to each row's list
+};
+
+__device__ __forceinline__ int mbcnt(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// bfloat16 caches.  The loop body issues a fixed set of loads every step
+// (tile indices past the end are clamped to the last tile, whose rows the
+// filter masks), so the compiler's memory waits stay exact and kDepth tiles
+// stay in flight.  Passing keys are appended to an LDS buffer (one ballot
+// per head row; lanes whose key does not pass write to a discard slot, so
+// the append has no branch) and distributed to the per-row lists when the
+// buffer is nearly full and at the end.  A distribution in mid-stream ends
+// with a full wait on its stores, which keeps the loop's load waits exact.
+template <bool PAGED, bool GRP>
+__global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
+  __shared__ WaveLds wlds[kWaves];
+  const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
+  const int L = seq_len(p, b);
+  const int64_t c0 = (int64_t)chunk * kChunkKeys;
+  if (c0 >= L) return;
+  const int wv = wave_id();
+  const int64_t w0 = c0 + (int64_t)wv * kWaveKeys;
+  if (w0 >= L) return;
+  const int64_t w1 = (w0 + kWaveKeys < (int64_t)L) ? w0 + kWaveKeys : (int64_t)L;
+  const int nvalid = (int)(w1 - w0);
+  const int sub = chunk * kWaves + wv;
+  const int l = lane_id(), col = l & 15, s = l >> 4;
+  constexpr bool grp = GRP;
+  const int64_t row0 = grp ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
+  WaveLds &wl = wlds[wv];
+
+  QFrag qf;
+  load_q_bf16(p, b, g, qf);
+  // Thresholds of the rows this lane serves: heads 4s..4s+3 (per-head mode;
+  // heads beyond the group never pass) or the group (lanes 0..15).
+  float th[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * s + r;
+    if (grp) th[r] = (s == 0 && r == 0) ? w.theta[row0] : __builtin_inff();
+    else th[r] = h < p.G ? w.theta[row0 + h] : __builtin_inff();
+  }
+  const int ntiles = (nvalid + kTile - 1) / kTile;
+  if (PAGED) {
+    const int32_t *bt = p.K.block_table + (int64_t)b * p.K.max_pages + (w0 >> 4);
+    for (int i = l; i < ntiles; i += 64) wl.page[i] = bt[i];
+    __builtin_amdgcn_wave_barrier();  // every lane reads every page id
+  }
+  const char *kbase = (const char *)p.K.base;
+  constexpr int64_t kRowBytes = kHeadDim * 2;
+  const char *slab = kbase + (((int64_t)b * p.K.hkv + g) * p.K.ncap + w0) * kRowBytes;
+  const int64_t page_bytes = (int64_t)kTile * p.K.hkv * kRowBytes;
+  const int a = l >> 4;
+  const int last = nvalid - 1;
+  int lane_row[4], lane_chunk[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    lane_row[t] = 4 * t + a;
+    lane_chunk[t] = 16 * swz_chunk(t);
+  }
+  // Issue the four coalesced loads of tile ti (clamped to the last tile).
+  auto load = [&](int ti, u32x4 v[4]) {
+    ti = ti < ntiles ? ti : ntiles - 1;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      int j = ti * kTile + lane_row[t];
+      j = j < last ? j : last;
+      const char *row;
+      if (PAGED) row = kbase + wl.page[ti] * page_bytes + ((int64_t)(j & 15) * p.K.hkv + g) * kRowBytes;
+      else row = slab + (int64_t)j * kRowBytes;
+      v[t] = __builtin_nontemporal_load((const u32x4 *)(row + lane_chunk[t]));
+    }
+  };
+
+  const int nrows = grp ? 1 : p.G;
+  int nbuf = 0;
+  // Running list lengths.  Every lane stores the same (wave-uniform) value,
+  // so each lane reads back its own store and no lane depends on another's.
+#pragma unroll
+  for (int h = 0; h < kMaxGroup; ++h) wl.base[h] = 0;
+  // Move the staged candidates to the per-row lists, in order: the entries
+  // of one head appear in position order in the buffer.
+  auto distribute = [&]() {
+    __builtin_amdgcn_wave_barrier();  // entries were written by other lanes
+    for (int e0 = 0; e0 < nbuf; e0 += 64) {
+      const int e = e0 + l;
+      const bool in = e < nbuf;
+      const uint32_t meta = in ? wl.cmeta[e] : 0xFFFFFFFFu;
+      const int h = (int)(meta >> 24);
+      for (int hh = 0; hh < nrows; ++hh) {
+        const bool mine = in && h == hh;
+        const uint64_t m = __ballot(mine);
+        const int b0 = wl.base[hh];
+        if (mine) {
+          const int slot = b0 + mbcnt(m);
+          if (slot < w.capw)
+            w.cand[((row0 + hh) * w.nsub + sub) * (int64_t)w.capw + slot] =
+                make_uint2(f2key(__uint_as_float(wl.cval[e])), (uint32_t)(w0 + (meta & 0xFFFFFFu)));
+        }
+        wl.base[hh] = b0 + __popcll(m);
+      }
+    }
+    nbuf = 0;
+  };
+
+  const int nsteps = (ntiles + kDepth - 1) / kDepth * kDepth;
+  u32x4 buf[kDepth][4];
+#pragma unroll
+  for (int d = 0; d < kDepth; ++d) {
+    load(d, buf[d]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int tb = 0; tb < nsteps; tb += kDepth) {
+    if (nbuf > kCandBuf - kDepth * 4 * 64) {  // room for kDepth tiles' worst case
+      distribute();
+      __builtin_amdgcn_s_waitcnt(0);
+    }
+#pragma unroll
+    for (int u = 0; u < kDepth; ++u) {
+      const int ti = tb + u;
+      stage_tile(wl.tile, buf[u]);
+      load(ti + kDepth, buf[u]);
+      __builtin_amdgcn_wave_barrier();  // the tile is read back by other lanes
+      KFrag kf;
+      read_kfrag(wl.tile, kf);
+      __builtin_amdgcn_wave_barrier();  // and overwritten by the next step
+      f32x4 acc = mfma_scores(qf, kf);
+      const int jl = ti * kTile + col;
+      const bool live = jl < nvalid;
+      if (grp) acc[0] = group_sum(acc);
+#pragma unroll
+      for (int r = 0; r < (grp ? 1 : 4); ++r) {
+        const bool pass = live && acc[r] >= th[r];
+        const uint64_t m = __ballot(pass);
+        const int e = pass ? nbuf + mbcnt(m) : kCandBuf + l;
+        wl.cval[e] = __float_as_uint(acc[r]);
+        wl.cmeta[e] = ((uint32_t)(4 * s + r) << 24) | (uint32_t)jl;
+        nbuf += __popcll(m);
+      }
+    }
+  }
+  distribute();
+  for (int hh = 0; hh < nrows; ++hh)
+    if (l == 0) w.counts[(row0 + hh) * w.nsub + sub] = wl.base[hh];
+}
+
+// float32 caches (small problems): vector-ALU scoring, direct list writes.
+__global__ __launch_bounds__(kBlock) void k_score_filter_f32(Params p, Work w) {
+  __shared__ float q_lds[kMaxGroup * kHeadDim];
   const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
   const int L = seq_len(p, b);
   const int64_t c0 = (int64_t)chunk * kChunkKeys;
   if (c0 >= L) return;  // whole workgroup: no barrier follows
-  Scorer<BF16> sc;
-  scorer_init<BF16>(p, b, g, sc, q_lds);
+  Scorer<false> sc;
+  scorer_init<false>(p, b, g, sc, q_lds);
   const int wv = wave_id();
   const int64_t w0 = c0 + (int64_t)wv * kWaveKeys;
   if (w0 >= L) return;
@@ -160,35 +319,27 @@ __global__ __launch_bounds__(kBlock) void k_score_filter(Params p, Work w) {
   const int sub = chunk * kWaves + wv;
   const int l = lane_id(), col = l & 15, s = l >> 4;
   const uint32_t below = (1u << col) - 1u;
-
-  // Rows served by this lane: heads 4s..4s+3 of the group (per-head mode) or
-  // the group itself (group-shared mode, lanes 0..15).
+  const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
   float th[4];
-  uint2 *cl[4];
   int cnt[4] = {0, 0, 0, 0};
-  if (!p.group_shared) {
+  uint2 *cl[4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int h = 4 * s + r;
-      const int64_t row = (int64_t)b * p.R + (int64_t)g * p.G + (h < p.G ? h : 0);
-      th[r] = w.theta[row];
-      cl[r] = w.cand + (row * w.nsub + sub) * (int64_t)w.capw;
-    }
-  } else {
-    const int64_t row = (int64_t)b * p.R + g;
-    th[0] = w.theta[row];
-    cl[0] = w.cand + (row * w.nsub + sub) * (int64_t)w.capw;
+  for (int r = 0; r < 4; ++r) {
+    const int h = 4 * s + r;
+    const int64_t row = p.group_shared ? row0 : row0 + (h < p.G ? h : 0);
+    th[r] = w.theta[row];
+    cl[r] = w.cand + (row * w.nsub + sub) * (int64_t)w.capw;
   }
-
-  auto filter = [&](const f32x4 &acc, int64_t j0) {
+  for (int64_t j0 = w0; j0 < w1; j0 += kTile) {
+    const int64_t jl = j0 + col < w1 ? j0 + col : w1 - 1;
+    const f32x4 acc = sc.score(p, b, g, jl);
     const int64_t j = j0 + col;
     const bool valid = j < w1;
     if (!p.group_shared) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const bool pass = valid && (4 * s + r) < p.G && acc[r] >= th[r];
-        const uint64_t bal = __ballot(pass);
-        const uint32_t gm = (uint32_t)(bal >> (16 * s)) & 0xFFFFu;
+        const uint32_t gm = (uint32_t)(__ballot(pass) >> (16 * s)) & 0xFFFFu;
         if (pass) {
           const int slot = cnt[r] + __popc(gm & below);
           if (slot < w.capw) cl[r][slot] = make_uint2(f2key(acc[r]), (uint32_t)j);
@@ -205,40 +356,16 @@ __global__ __launch_bounds__(kBlock) void k_score_filter(Params p, Work w) {
       }
       cnt[0] += __popc(gm);
     }
-  };
-
-  if constexpr (BF16) {
-    KFrag cur, nxt;
-    int64_t jl = w0 + col < w1 ? w0 + col : w1 - 1;
-    load_k_bf16(p.K, kv_offset(p.K, b, g, jl), cur);
-    nxt = cur;
-    for (int64_t j0 = w0; j0 < w1; j0 += kTile) {
-      const int64_t jn = j0 + kTile;
-      if (jn < w1) {
-        jl = jn + col < w1 ? jn + col : w1 - 1;
-        load_k_bf16(p.K, kv_offset(p.K, b, g, jl), nxt);
-      }
-      const f32x4 acc = mfma_scores(sc.qf, cur);
-      filter(acc, j0);
-      cur = nxt;
-    }
-  } else {
-    for (int64_t j0 = w0; j0 < w1; j0 += kTile) {
-      const int64_t jl = j0 + col < w1 ? j0 + col : w1 - 1;
-      filter(sc.score(p, b, g, jl), j0);
-    }
   }
-
   if (col == 0) {
     if (!p.group_shared) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int h = 4 * s + r;
-        if (h < p.G)
-          w.counts[((int64_t)b * p.R + (int64_t)g * p.G + h) * w.nsub + sub] = cnt[r];
+        if (h < p.G) w.counts[(row0 + h) * w.nsub + sub] = cnt[r];
       }
     } else if (s == 0) {
-      w.counts[((int64_t)b * p.R + g) * w.nsub + sub] = cnt[0];
+      w.counts[row0 * w.nsub + sub] = cnt[0];
     }
   }
 }
@@ -661,8 +788,14 @@ hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
 
 hipError_t launch_score_filter(const Params &p, const Work &w, hipStream_t st) {
   const dim3 grid(cdiv(p.ncap, kChunkKeys), p.B * p.Hkv);
-  if (p.bf16) k_score_filter<true><<<grid, kBlock, 0, st>>>(p, w);
-  else k_score_filter<false><<<grid, kBlock, 0, st>>>(p, w);
+  if (!p.bf16) k_score_filter_f32<<<grid, kBlock, 0, st>>>(p, w);
+  else if (p.K.paged) {
+    if (p.group_shared) k_score_stream<true, true><<<grid, kBlock, 0, st>>>(p, w);
+    else k_score_stream<true, false><<<grid, kBlock, 0, st>>>(p, w);
+  } else {
+    if (p.group_shared) k_score_stream<false, true><<<grid, kBlock, 0, st>>>(p, w);
+    else k_score_stream<false, false><<<grid, kBlock, 0, st>>>(p, w);
+  }
   return hipGetLastError();
 }
 

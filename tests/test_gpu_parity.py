@@ -263,6 +263,17 @@ def test_group_shared_mode_group_sizes(sd, G):
     check_fused(inp, out, idx, label=f"group-shared G={G}")
 
 
+@pytest.mark.parametrize("name,ratio", [("w3", 4.0), ("w2", 6.0), ("w5", 5.0), ("w4", 8.0)])
+def test_long_candidate_lists(sd, name, ratio):
+    # Low sparsity: each scoring wave stages hundreds of candidates per row,
+    # so its lists span several 64-entry batches and the staging buffer is
+    # written out in mid-stream (regression test for both).
+    kw = {"w4": dict(B=2, lmin=6000, lmax=9000, N=9000)}.get(name, dict(B=1, N=12000))
+    inp = make(name, seed=14, ratio=ratio, **kw)
+    out, idx, _ = gpu_fused(sd, inp)
+    check_fused(inp, out, idx, label=f"{name} ratio {ratio}")
+
+
 def test_float32_gqa_and_paged(sd):
     inp = make("w4", seed=10, B=3, lmin=3000, lmax=9000, N=9000, dtype="f32")
     out, idx, _ = gpu_fused(sd, inp)
