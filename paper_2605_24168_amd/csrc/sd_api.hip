@@ -7,7 +7,7 @@
 #include <cmath>
 #include <mutex>
 
-#include "../../include/sparse_decode.h"
+#include "sparse_decode.h"
 #include "sd_internal.hpp"
 #include "sd_launch.hpp"
 

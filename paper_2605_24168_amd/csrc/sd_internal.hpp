@@ -17,9 +17,9 @@ constexpr int kWaves = kBlock / 64;
 constexpr int kMaxGroup = 16;      // query heads per KV head handled by one MFMA tile
 constexpr int kChunkKeys = 8192;   // keys one scoring workgroup streams
 constexpr int kWaveKeys = kChunkKeys / kWaves;
-constexpr int kSampleMax = 4096;   // pilot samples per row
+constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
-constexpr int kRepairParts = 64;   // workgroups per (sequence, KV head) in the repair stream
+constexpr int kRepairParts = 16;   // workgroups per (sequence, KV head) in the repair stream
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -60,7 +60,8 @@ struct Work {
   uint2 *cand;       // [rows][nsub][capw] (order-preserving key, position)
   int32_t *flags;    // [rows] 1 = the row needs the exact fallback
   float *dense;      // [rows][ncap] fallback scores
-  float *sigma;      // [rows][k_max] kept scores, aligned with idx
+  float *sigma;      // [rows][k_max] kept scores (group-shared mode) or softmax
+                     // weights exp(scale*(s - max s)) (per-head mode), aligned with idx
   float *part;       // [B*Hq][nsplit][kPartStride] attend partials
   int32_t *stats;    // [4]: [0] rows repaired in the last call
   int32_t nsub;
@@ -312,17 +313,17 @@ __device__ __forceinline__ float block_max(float v, float *tmp) {
   return m;
 }
 
-// Add 1 to hist[dig] for every active lane with act set, one LDS atomic per
-// distinct digit in the wave (lanes sharing a digit are counted by ballot).
+// Add 1 to hist[dig] for every active lane with act set.  Lanes sharing the
+// first active lane's bin are counted with one atomic (the common case when
+// the leading key bits cluster); the others add their own.
 __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t dig, bool act) {
-  uint64_t pending = __ballot(act);
-  while (pending) {
-    const int leader = __ffsll((unsigned long long)pending) - 1;
-    const uint32_t v = __shfl(dig, leader);
-    const uint64_t same = __ballot(act && dig == v);
-    if (lane_id() == leader) atomicAdd(&hist[v], (uint32_t)__popcll(same));
-    pending &= ~same;
-  }
+  const uint64_t am = __ballot(act);
+  if (!am) return;
+  const int leader = __ffsll((unsigned long long)am) - 1;
+  const uint32_t v = __shfl(dig, leader);
+  const uint64_t same = __ballot(act && dig == v);
+  if (lane_id() == leader) atomicAdd(&hist[v], (uint32_t)__popcll(same));
+  if (act && dig != v) atomicAdd(&hist[dig], 1u);
 }
 
 // ---------------------------------------------------------------------------
@@ -353,21 +354,15 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
     const uint32_t dmask = (uint32_t)nb - 1u;
     for (int i = tid; i < nb; i += kBlock) hist[i] = 0;
     __syncthreads();
-    if (pass == 0) {
-      // The leading bits of the items cluster in a few bins: count lanes
-      // sharing a bin with one atomic.
-      for (int base = 0; base < n; base += kBlock) {
-        const int p = base + tid;
-        uint32_t key = 0;
-        if (p < n) key = src.key(p);
-        hist_add(hist, (key >> shift) & dmask, p < n);
+    for (int base = 0; base < n; base += kBlock) {
+      const int p = base + tid;
+      uint32_t key = 0;
+      bool act = false;
+      if (p < n) {
+        key = src.key(p);
+        act = (key & mask) == prefix;
       }
-    } else {
-      // Lower bits spread over many bins: plain LDS atomics.
-      for (int p = tid; p < n; p += kBlock) {
-        const uint32_t key = src.key(p);
-        if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1u);
-      }
+      hist_add(hist, (key >> shift) & dmask, act);
     }
     __syncthreads();
     // Thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top.

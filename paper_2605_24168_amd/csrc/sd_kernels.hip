@@ -101,7 +101,7 @@ struct LdsKeys {
 
 // Per-row threshold = the r-th largest sample score, r = ceil(2.5 k m / L)
 // (so about 2.5 k of the L keys are expected to pass), or r = k when the
-// sample is the whole sequence.  Also clears the row's flags and counters.
+// sample is the whole sequence.  Also clears the row's fallback flag.
 __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[2048];
@@ -147,29 +147,26 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
 // issues no global stores and its load waits stay exact.
 // ---------------------------------------------------------------------------
 constexpr int kDepth = 3;        // tiles in flight per wave
-constexpr int kCandBuf = 1024;   // candidates staged per wave
+constexpr int kCandBuf = 1024;   // candidates staged per wave, split evenly over its rows
 constexpr int kWavePages = kWaveKeys / kTile;
+static_assert(kCandBuf / kMaxGroup > kDepth * kTile, "a step must fit a row's staging area");
 
 struct WaveLds {
   u32x4 tile[256];
-  uint32_t cval[kCandBuf + 64];   // raw float32 score bits (+64 discard slots)
-  uint32_t cmeta[kCandBuf + 64];  // (head in group << 24) | position within the wave's range
+  uint2 cand[kCandBuf + 64];   // per-row areas of (score bits, position), +64 discard slots
   int32_t page[kWavePages];
-  int32_t base[kMaxGroup];        // candidates already written to each row's list
 };
-
-__device__ __forceinline__ int mbcnt(uint64_t m) {
-  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-}
 
 // bfloat16 caches.  The loop body issues a fixed set of loads every step
 // (tile indices past the end are clamped to the last tile, whose rows the
 // filter masks), so the compiler's memory waits stay exact and kDepth tiles
-// stay in flight.  Passing keys are appended to an LDS buffer (one ballot
-// per head row; lanes whose key does not pass write to a discard slot, so
-// the append has no branch) and distributed to the per-row lists when the
-// buffer is nearly full and at the end.  A distribution in mid-stream ends
-// with a full wait on its stores, which keeps the loop's load waits exact.
+// stay in flight.  Each row served by the wave (a query head, or the KV head
+// in group-shared mode) owns an equal slice of an LDS staging buffer; a
+// passing key goes to its row's slice at the row's running count (lanes
+// whose key does not pass write a discard slot, so the append has no
+// branch).  A slice close to full is copied to the row's list in HBM with
+// coalesced stores; such a copy in mid-stream ends with a full wait on its
+// stores, which keeps the loop's load waits exact.
 template <bool PAGED, bool GRP>
 __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   __shared__ WaveLds wlds[kWaves];
@@ -186,12 +183,14 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   const int l = lane_id(), col = l & 15, s = l >> 4;
   constexpr bool grp = GRP;
   const int64_t row0 = grp ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
+  const int nrows = grp ? 1 : p.G;
+  const int cap = kCandBuf / nrows;  // staging slots per row
   WaveLds &wl = wlds[wv];
 
   QFrag qf;
   load_q_bf16(p, b, g, qf);
-  // Thresholds of the rows this lane serves: heads 4s..4s+3 (per-head mode;
-  // heads beyond the group never pass) or the group (lanes 0..15).
+  // This lane serves rows 4s..4s+3 (heads of the group; heads beyond G never
+  // pass) or, in group-shared mode, lanes 0..15 serve the group's one row.
   float th[4];
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
@@ -231,47 +230,69 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
     }
   };
 
-  const int nrows = grp ? 1 : p.G;
-  int nbuf = 0;
-  // Running list lengths.  Every lane stores the same (wave-uniform) value,
-  // so each lane reads back its own store and no lane depends on another's.
+  // Per-row counts: staged in LDS (cnt) and already written to HBM (done).
+  // Lane group s keeps those of its rows 4s+r (wave-uniform per group).
+  int cnt[4] = {0, 0, 0, 0}, done[4] = {0, 0, 0, 0};
+  // Copy every row's staged slice to its list (row h's counts live in lane
+  // group h >> 2).
+  auto flush = [&]() {
+    __builtin_amdgcn_wave_barrier();  // slices were written by other lanes
+    for (int h = 0; h < nrows; ++h) {
+      const int src_lane = 16 * (h >> 2);
+      int nh = 0, dh = 0;
 #pragma unroll
-  for (int h = 0; h < kMaxGroup; ++h) wl.base[h] = 0;
-  // Move the staged candidates to the per-row lists, in order: the entries
-  // of one head appear in position order in the buffer.
-  auto distribute = [&]() {
-    __builtin_amdgcn_wave_barrier();  // entries were written by other lanes
-    for (int e0 = 0; e0 < nbuf; e0 += 64) {
-      const int e = e0 + l;
-      const bool in = e < nbuf;
-      const uint32_t meta = in ? wl.cmeta[e] : 0xFFFFFFFFu;
-      const int h = (int)(meta >> 24);
-      for (int hh = 0; hh < nrows; ++hh) {
-        const bool mine = in && h == hh;
-        const uint64_t m = __ballot(mine);
-        const int b0 = wl.base[hh];
-        if (mine) {
-          const int slot = b0 + mbcnt(m);
-          if (slot < w.capw)
-            w.cand[((row0 + hh) * w.nsub + sub) * (int64_t)w.capw + slot] =
-                make_uint2(f2key(__uint_as_float(wl.cval[e])), (uint32_t)(w0 + (meta & 0xFFFFFFu)));
-        }
-        wl.base[hh] = b0 + __popcll(m);
+      for (int r = 0; r < 4; ++r) {
+        const int c_ = __shfl(cnt[r], src_lane), d_ = __shfl(done[r], src_lane);
+        if ((h & 3) == r) { nh = c_; dh = d_; }
+      }
+      uint2 *dst = w.cand + ((row0 + h) * w.nsub + sub) * (int64_t)w.capw;
+      const uint2 *srcp = wl.cand + h * cap;
+      for (int e = l; e < nh; e += 64) {
+        const int slot = dh + e;
+        const uint2 it = srcp[e];
+        if (slot < w.capw) dst[slot] = make_uint2(f2key(__uint_as_float(it.x)), (uint32_t)w0 + it.y);
       }
     }
-    nbuf = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      done[r] += cnt[r];
+      cnt[r] = 0;
+    }
+  };
+
+  // Append the passing keys of one scored tile to their rows' slices.
+  auto filter = [&](f32x4 acc, int jl) {
+    const bool live = jl < nvalid;
+    if (grp) acc[0] = group_sum(acc);
+#pragma unroll
+    for (int r = 0; r < (grp ? 1 : 4); ++r) {
+      const bool pass = live && acc[r] >= th[r];
+      const uint32_t gm = (uint32_t)(__ballot(pass) >> (16 * s)) & 0xFFFFu;
+      const int e = pass ? (4 * s + r) * cap + cnt[r] + __popc(gm & ((1u << col) - 1u))
+                         : kCandBuf + l;
+      wl.cand[e] = make_uint2(__float_as_uint(acc[r]), (uint32_t)jl);
+      cnt[r] += __popc(gm);
+    }
   };
 
   const int nsteps = (ntiles + kDepth - 1) / kDepth * kDepth;
+  // A step filters kDepth tiles: at most 16 keys per row each.
+  const int flush_at = cap - kDepth * kTile;
   u32x4 buf[kDepth][4];
 #pragma unroll
   for (int d = 0; d < kDepth; ++d) {
     load(d, buf[d]);
     __builtin_amdgcn_sched_barrier(0);
   }
+  // The scores of a tile are filtered one step later, after the next tile's
+  // loads and matrix ops are issued, so the appends (which wait on the
+  // matrix results) never hold up the stream.
+  f32x4 prev = {0.f, 0.f, 0.f, 0.f};
+  int prev_jl = nvalid;  // nothing to filter before the first tile
   for (int tb = 0; tb < nsteps; tb += kDepth) {
-    if (nbuf > kCandBuf - kDepth * 4 * 64) {  // room for kDepth tiles' worst case
-      distribute();
+    const int most = max(max(cnt[0], cnt[1]), max(cnt[2], cnt[3]));
+    if (__ballot(most > flush_at)) {
+      flush();
       __builtin_amdgcn_s_waitcnt(0);
     }
 #pragma unroll
@@ -283,24 +304,21 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
       KFrag kf;
       read_kfrag(wl.tile, kf);
       __builtin_amdgcn_wave_barrier();  // and overwritten by the next step
-      f32x4 acc = mfma_scores(qf, kf);
-      const int jl = ti * kTile + col;
-      const bool live = jl < nvalid;
-      if (grp) acc[0] = group_sum(acc);
-#pragma unroll
-      for (int r = 0; r < (grp ? 1 : 4); ++r) {
-        const bool pass = live && acc[r] >= th[r];
-        const uint64_t m = __ballot(pass);
-        const int e = pass ? nbuf + mbcnt(m) : kCandBuf + l;
-        wl.cval[e] = __float_as_uint(acc[r]);
-        wl.cmeta[e] = ((uint32_t)(4 * s + r) << 24) | (uint32_t)jl;
-        nbuf += __popcll(m);
-      }
+      const f32x4 acc = mfma_scores(qf, kf);
+      filter(prev, prev_jl);
+      prev = acc;
+      prev_jl = ti * kTile + col;
     }
   }
-  distribute();
-  for (int hh = 0; hh < nrows; ++hh)
-    if (l == 0) w.counts[(row0 + hh) * w.nsub + sub] = wl.base[hh];
+  filter(prev, prev_jl);
+  flush();
+  if (col == 0) {
+#pragma unroll
+    for (int r = 0; r < (grp ? 1 : 4); ++r) {
+      const int h = 4 * s + r;
+      if (h < nrows) w.counts[(row0 + h) * w.nsub + sub] = done[r];
+    }
+  }
 }
 
 // float32 caches (small problems): vector-ALU scoring, direct list writes.
@@ -464,6 +482,18 @@ __device__ __forceinline__ void select_and_write(const Src &src, int n, int k, u
   });
 }
 
+// Per-head rows of the fused path: turn the kept scores (vrow[0..k), written
+// by this workgroup) into softmax weights exp(scale*(s - max s)) in place, so
+// that the attention is a plain weighted gather whose splits all share one
+// reference maximum.
+__device__ __forceinline__ void kept_scores_to_weights(float *vrow, int k, float scale, float *ftmp) {
+  __syncthreads();  // vrow was written by other threads of the block
+  float m = -__builtin_inff();
+  for (int i = threadIdx.x; i < k; i += kBlock) m = fmaxf(m, vrow[i]);
+  m = block_max(m, ftmp);
+  for (int i = threadIdx.x; i < k; i += kBlock) vrow[i] = expf(scale * (vrow[i] - m));
+}
+
 template <int MODE>
 __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float *dense, int64_t ld,
                                                    int32_t *idx, float *vals, int lds_cap) {
@@ -471,8 +501,10 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   __shared__ uint32_t hist[2048];
   __shared__ SelShared sh;
   __shared__ int status;
+  __shared__ float ftmp[kWaves];
   const int row = blockIdx.x, b = row / p.R;
   if (MODE == 2 && w.flags[row] == 0) return;
+  const bool weights = MODE != 1 && !p.group_shared;
   const int L = seq_len(p, b);
   const int k = row_budget(p, b, L);
   int32_t *irow = idx + (int64_t)row * p.k_max;
@@ -528,6 +560,7 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
     } else {
       select_and_write(DenseSrc{dense + (int64_t)row * ld}, L, k, hist, &sh, irow, vrow);
     }
+    if (weights) kept_scores_to_weights(vrow, k, p.scale, ftmp);
   }
   for (int i = k + tid; i < p.k_max; i += kBlock) {
     irow[i] = -1;
@@ -548,7 +581,7 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
 // (max, sum, unnormalised output) partials that k_merge combines.
 // ---------------------------------------------------------------------------
 constexpr int kAttHeads = 8;  // heads accumulated per pass over the value rows
-constexpr int kGatherUnroll = 4;
+constexpr int kGatherUnroll = 8;
 
 template <bool BF16>
 __device__ __forceinline__ void load_row8(const void *base, int64_t off, int col, float v[8]) {
@@ -580,7 +613,7 @@ __device__ __forceinline__ int attend_list_len(const Params &p, int b, int L, bo
 template <bool BF16, bool FUSED>
 __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32_t *idx, void *out,
                                                    int split) {
-  extern __shared__ float att_dyn[];  // e[nh][split], then pos[split]
+  extern __shared__ int64_t att_dyn[];  // voff[split], koff[split], e[nh][split], pos[split]
   __shared__ float q_l[kMaxGroup][kHeadDim];
   __shared__ float red[kWaves][kAttHeads][kHeadDim];
   __shared__ float lred[kWaves][kAttHeads];
@@ -597,10 +630,13 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   const int n_list = attend_list_len(p, b, L, FUSED);
   const int nsp = (n_list + split - 1) / split;
   const int tid = threadIdx.x, l = lane_id(), col = l & 15, sub = l >> 4, wv = wave_id();
-  float *e_l = att_dyn;
-  int32_t *pos_l = (int32_t *)(att_dyn + nh * split);
+  const bool recompute = !FUSED || grp;
+  int64_t *voff_l = att_dyn;                       // element offsets of the value rows
+  int64_t *koff_l = att_dyn + split;               // and of the key rows (recompute only)
+  float *e_l = (float *)(att_dyn + (recompute ? 2 : 1) * split);
+  int32_t *pos_l = (int32_t *)(e_l + nh * split);
 
-  if (n_list == 0) {  // nothing kept: zero output
+  if (n_list == 0 || L == 0) {  // nothing kept: zero output
     if (s == 0)
       for (int e = tid; e < nh * kHeadDim; e += kBlock)
         store_out<BF16>(out, ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim, 0.f);
@@ -611,12 +647,16 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   const int n = (n_list - e0) < split ? (n_list - e0) : split;
   const int32_t *irow = idx + (int64_t)row * p.k_max + e0;
 
+  // Resolve every entry to its row offsets once (page-table reads in
+  // parallel); skipped entries point at position 0 and get weight 0.
   for (int t = tid; t < n; t += kBlock) {
     int32_t j = irow[t];
     if (j < 0 || j >= L) j = -1;
     pos_l[t] = j;
+    const int64_t jc = j >= 0 ? j : 0;
+    voff_l[t] = kv_offset(p.V, b, g, jc);
+    if (recompute) koff_l[t] = kv_offset(p.K, b, g, jc);
   }
-  const bool recompute = !FUSED || grp;
   if (recompute) {
     for (int e = tid; e < nh * kHeadDim; e += kBlock) {
       const int64_t qo = ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim;
@@ -627,9 +667,12 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   __syncthreads();
 
   // Logits z[h][t] = scale * q_h . K_j (kept in e_l until the max is known).
+  // Per-head fused rows arrive with their softmax weights already formed
+  // (relative to the row's maximum, so all splits share one reference).
   if (!recompute) {
-    const float *srow = w.sigma + (int64_t)row * p.k_max + e0;
-    for (int t = tid; t < n; t += kBlock) e_l[t] = pos_l[t] >= 0 ? p.scale * srow[t] : -__builtin_inff();
+    const float *wrow = w.sigma + (int64_t)row * p.k_max + e0;
+    for (int t = tid; t < n; t += kBlock) e_l[t] = wrow[t];
+    if (tid == 0) mh[0] = 0.f;
   } else {
     for (int t = wv * 4 + sub; t < n; t += kWaves * 4) {
       const int32_t j = pos_l[t];
@@ -639,7 +682,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
         continue;
       }
       float kv[8];
-      load_row8<BF16>(p.K.base, kv_offset(p.K, b, g, j), col, kv);
+      load_row8<BF16>(p.K.base, koff_l[t], col, kv);
       for (int h = 0; h < nh; ++h) {
         float d = 0.f;
 #pragma unroll
@@ -653,20 +696,22 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     }
   }
   __syncthreads();
-  for (int h = 0; h < nh; ++h) {
-    float m = -__builtin_inff();
-    for (int t = tid; t < n; t += kBlock) m = fmaxf(m, e_l[h * split + t]);
-    m = block_max(m, ftmp);
-    if (tid == 0) mh[h] = m;
+  if (recompute) {
+    for (int h = 0; h < nh; ++h) {
+      float m = -__builtin_inff();
+      for (int t = tid; t < n; t += kBlock) m = fmaxf(m, e_l[h * split + t]);
+      m = block_max(m, ftmp);
+      if (tid == 0) mh[h] = m;
+    }
+    __syncthreads();
+    // Weights exp(z - m); skipped entries (z = -inf) give 0.
+    for (int e = tid; e < nh * n; e += kBlock) {
+      const int h = e / n, t = e % n;
+      const float z = e_l[h * split + t];
+      e_l[h * split + t] = z == -__builtin_inff() ? 0.f : expf(z - mh[h]);
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  // Weights exp(z - m); skipped entries (z = -inf) give 0.
-  for (int e = tid; e < nh * n; e += kBlock) {
-    const int h = e / n, t = e % n;
-    const float z = e_l[h * split + t];
-    e_l[h * split + t] = z == -__builtin_inff() ? 0.f : expf(z - mh[h]);
-  }
-  __syncthreads();
 
   for (int hb = 0; hb < nh; hb += kAttHeads) {
     const int nb = (nh - hb) < kAttHeads ? (nh - hb) : kAttHeads;
@@ -678,22 +723,23 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[h][c] = 0.f;
     }
+    // Branch-free gather: entries past the split or skipped (weight 0) read
+    // the sequence's position 0, so every step issues the same loads.
     for (int t0 = wv * 4 * kGatherUnroll; t0 < n; t0 += kWaves * 4 * kGatherUnroll) {
       float vv[kGatherUnroll][8];
       int tt[kGatherUnroll];
 #pragma unroll
       for (int u = 0; u < kGatherUnroll; ++u) {
         const int t = t0 + 4 * u + sub;
-        tt[u] = (t < n && pos_l[t] >= 0) ? t : -1;
-        if (tt[u] >= 0) load_row8<BF16>(p.V.base, kv_offset(p.V, b, g, pos_l[t]), col, vv[u]);
+        tt[u] = t < n ? t : -1;
+        load_row8<BF16>(p.V.base, voff_l[t < n ? t : 0], col, vv[u]);
       }
 #pragma unroll
       for (int u = 0; u < kGatherUnroll; ++u) {
-        if (tt[u] < 0) continue;
 #pragma unroll
         for (int h = 0; h < kAttHeads; ++h) {
           if (h < nb) {
-            const float e = e_l[(hb + h) * split + tt[u]];
+            const float e = tt[u] >= 0 ? e_l[(hb + h) * split + tt[u]] : 0.f;
             lsum[h] += e;
 #pragma unroll
             for (int c = 0; c < 8; ++c) acc[h][c] = fmaf(e, vv[u][c], acc[h][c]);
@@ -757,7 +803,7 @@ __global__ __launch_bounds__(kHeadDim) void k_merge(Params p, Work w, void *out,
   const int L = seq_len(p, b);
   const int n_list = attend_list_len(p, b, L, FUSED);
   const int nsp = (n_list + split - 1) / split;
-  if (nsp <= 1) return;
+  if (nsp <= 1 || L == 0) return;  // written directly by k_attend
   const int c = threadIdx.x;
   const float *pp = w.part + (int64_t)bh * w.nsplit * kPartStride;
   float M = -__builtin_inff();
@@ -819,6 +865,13 @@ hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream
   return hipGetLastError();
 }
 
+// Dynamic LDS per list entry of k_attend: value (and key) row offsets,
+// one weight per head served, and the position.
+static int64_t attend_bytes_per_entry(const Params &p) {
+  const int nh = p.group_shared ? p.G : 1;
+  return 8 + 8 + 4 * nh + 4;
+}
+
 int attend_split(const Params &p, int nsplit_max_positions) {
   // Positions per attend workgroup: enough workgroups to fill the chip
   // (about 2048), at least 64 positions each, LDS-bounded in group mode.
@@ -830,8 +883,7 @@ int attend_split(const Params &p, int nsplit_max_positions) {
   if (nsplit < 1) nsplit = 1;
   int64_t split = (k_max + nsplit - 1) / nsplit;
   split = (split + 63) / 64 * 64;
-  const int nh = p.group_shared ? p.G : 1;
-  const int64_t lds_limit = (48 * 1024 / 4) / (nh + 1) / 64 * 64;  // e[nh][split] + pos[split]
+  const int64_t lds_limit = (48 * 1024) / attend_bytes_per_entry(p) / 64 * 64;
   if (split > lds_limit) split = lds_limit;
   return (int)split;
 }
@@ -845,8 +897,7 @@ int attend_nsplit(const Params &p) {
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st) {
   const int split = attend_split(p, p.k_max);
-  const int nh = p.group_shared ? p.G : 1;
-  const size_t lds = (size_t)(nh + 1) * split * 4;
+  const size_t lds = (size_t)attend_bytes_per_entry(p) * split;
   const dim3 grid(w.nsplit, p.B * p.R);
   if (p.bf16) {
     if (fused) k_attend<true, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
