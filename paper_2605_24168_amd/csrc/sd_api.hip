@@ -17,10 +17,9 @@ using sd::kHeadDim;
 
 constexpr int kMaxDevices = 64;
 constexpr size_t kAlign = 256;
-constexpr int kLdsCapMax = 18000;  // candidate keys held in LDS by the selection
 constexpr int kRing = 64;          // profiled calls remembered per device
-// Longest cache (positions per sequence): the selection keeps one prefix
-// entry per 2048-key candidate list in LDS.
+// Longest cache (positions per sequence): the selection keeps two entries
+// per candidate chunk (at least 1024 keys) in LDS.
 constexpr int64_t kMaxCapacity = int64_t(1) << 24;
 constexpr size_t kSelectLdsBudget = 150 * 1024;  // dynamic LDS of the selection kernel
 
@@ -168,23 +167,35 @@ sd::Params make_params(const sd_tensor *q, const sd_kv *K, const sd_kv *V, const
   return p;
 }
 
-// Workspace layout.  Sizes depend only on the shapes, so the same layout is
-// recomputed on every call.
+// Keys per scoring wave.  A row expects about 2.5 k / L of a wave's keys to
+// pass its threshold; the wave must hold them in its staging area for the
+// row, kCandBuf / rows entries, with 2x headroom.  With a sparsity ratio
+// (k ~ L / ratio) the largest wave with 2 * 2.5 * wave / ratio <= area is
+// taken (256 at least: rows that still do not fit are sent to the exact
+// fallback by the pilot); with per-sequence k the 2048-key wave.
+int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared) {
+  if (sp->k_override) return sd::kWaveKeysMax;
+  const int rows = group_shared ? 1 : s.G;
+  const double area = (double)(sd::kCandBuf / rows);
+  int wk = sd::kWaveKeysMax;
+  while (wk > 256 && 5.0 * wk / sp->ratio > area) wk /= 2;
+  return wk;
+}
+
+// Workspace layout.  Sizes depend only on the shapes and the sparsity, so
+// the same layout is recomputed on every call.
 struct Layout {
-  size_t sample, theta, counts, cand, flags, dense, sigma, part, stats, total;
-  int nsub, capw, nsplit;
+  size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, total;
+  int nchunk, wave_keys, nsplit;
 };
 
-Layout layout_for(const Shape &s, int64_t k_max, bool fused, int group_shared) {
+Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp) {
   Layout L{};
+  const int group_shared = sp->group_shared ? 1 : 0;
   const int64_t rows = (int64_t)s.B * s.R;
-  L.nsub = (int)((s.ncap + sd::kWaveKeys - 1) / sd::kWaveKeys);
-  // Expected passes per list are about 2.5 k/L of its keys; keep 4x that plus slack.
-  const double expect = s.ncap > 0 ? 2.5 * (double)k_max / (double)s.ncap * sd::kWaveKeys : 0.0;
-  int capw = (int)std::ceil(4.0 * expect) + 64;
-  capw = (capw + 15) / 16 * 16;
-  if (capw > sd::kWaveKeys) capw = sd::kWaveKeys;
-  L.capw = capw;
+  L.wave_keys = wave_keys_for(s, sp, group_shared);
+  const int64_t ck = (int64_t)sd::kWaves * L.wave_keys;
+  L.nchunk = (int)((s.ncap + ck - 1) / ck);
   sd::Params shape_only{};
   shape_only.B = s.B;
   shape_only.R = s.R;
@@ -199,10 +210,12 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, int group_shared) {
     return o;
   };
   if (fused) {
+    const size_t blocks = (size_t)s.B * s.Hkv * L.nchunk * sd::kChunkCap;
     L.sample = take((size_t)rows * sd::kSampleMax * 4);
     L.theta = take((size_t)rows * 4);
-    L.counts = take((size_t)rows * L.nsub * 4);
-    L.cand = take((size_t)rows * L.nsub * L.capw * 8);
+    L.dir = take((size_t)rows * L.nchunk * 8);
+    L.ckey = take(blocks * 4);
+    L.cpos = take(blocks * 2);
     L.flags = take((size_t)rows * 4);
     L.dense = take((size_t)rows * s.ncap * 4);
     L.sigma = take((size_t)rows * k_max * 4);
@@ -242,16 +255,17 @@ sd::Work carve(char *base, const Layout &L, bool fused) {
   if (fused) {
     w.sample = (float *)(base + L.sample);
     w.theta = (float *)(base + L.theta);
-    w.counts = (int32_t *)(base + L.counts);
-    w.cand = (uint2 *)(base + L.cand);
+    w.dir = (int2 *)(base + L.dir);
+    w.ckey = (uint32_t *)(base + L.ckey);
+    w.cpos = (uint16_t *)(base + L.cpos);
     w.flags = (int32_t *)(base + L.flags);
     w.dense = (float *)(base + L.dense);
     w.sigma = (float *)(base + L.sigma);
   }
   w.part = (float *)(base + L.part);
   w.stats = (int32_t *)(base + L.stats);
-  w.nsub = L.nsub;
-  w.capw = L.capw;
+  w.nchunk = L.nchunk;
+  w.wave_keys = L.wave_keys;
   w.nsplit = L.nsplit;
   w.force_repair = (g_debug.load() & 1) ? 1 : 0;
   return w;
@@ -299,7 +313,7 @@ sd_status sparse_decode_workspace_size(const sd_tensor *q, const sd_kv *K, const
   int64_t k_max = 0;
   st = check_idx(idx, s, sp, k_max);
   if (st) return st;
-  *bytes = layout_for(s, k_max, true, sp->group_shared ? 1 : 0).total;
+  *bytes = layout_for(s, k_max, true, sp).total;
   return SD_OK;
 }
 
@@ -387,7 +401,7 @@ sd_status sparse_decode_attend(const sd_tensor *q, const sd_kv *K, const sd_kv *
   if (s.B == 0) return SD_OK;
   if (!seq_lens || (k_max > 0 && !idx->data)) return SD_ERR_INVALID_ARG;
   std::lock_guard<std::mutex> lk(g_mu);
-  const Layout L = layout_for(s, k_max, false, sp->group_shared ? 1 : 0);
+  const Layout L = layout_for(s, k_max, false, sp);
   DevState *ds = nullptr;
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
@@ -414,12 +428,14 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   if (!seq_lens) return SD_ERR_INVALID_ARG;
   const hipStream_t stream_h = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_mu);
-  const Layout L = layout_for(s, k_max, true, sp->group_shared ? 1 : 0);
+  const Layout L = layout_for(s, k_max, true, sp);
   DevState *ds = nullptr;
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
   if (st) return st;
-  const sd::Work w = carve(base, L, true);
+  sd::Work w = carve(base, L, true);
+  // float32 caches (small problems) take the full-score path for every row.
+  if (!s.bf16) w.force_repair = 1;
   const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   int32_t *idx_ptr = (int32_t *)idx->data;
 
@@ -434,15 +450,15 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   auto mark = [&](int i) -> hipError_t {
     return prof ? hipEventRecord(ev[i], stream_h) : hipSuccess;
   };
-  int lds_cap = (int)(4 * k_max + 1024);
-  if (lds_cap > kLdsCapMax) lds_cap = kLdsCapMax;
-  const size_t pre_bytes = sd::select_lds_bytes(p, 0);
-  const int lds_room = (int)((kSelectLdsBudget - pre_bytes) / 8);
-  if (lds_cap > lds_room) lds_cap = lds_room;
+  // Candidate keys the selection stages in LDS (about 2.5 k expected).
+  int64_t want = 4 * k_max + 1024;
+  const size_t pre_bytes = sd::select_lds_bytes(L.nchunk, 0);
+  const int64_t lds_room = (int64_t)((kSelectLdsBudget - pre_bytes) / 4);
+  const int lds_cap = (int)(want < lds_room ? want : lds_room);
   hipError_t e = mark(0);
   if (e == hipSuccess) e = sd::launch_pilot(p, w, stream_h);
   if (e == hipSuccess) e = mark(1);
-  if (e == hipSuccess && s.ncap > 0) e = sd::launch_score_filter(p, w, stream_h);
+  if (e == hipSuccess && s.ncap > 0) e = sd::launch_score_stream(p, w, stream_h);
   if (e == hipSuccess) e = mark(2);
   if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, stream_h);
   if (e == hipSuccess) e = mark(3);

@@ -15,8 +15,10 @@ constexpr int kTile = 16;          // keys per scoring tile (= KV page size)
 constexpr int kBlock = 256;        // threads per workgroup of every kernel
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxGroup = 16;      // query heads per KV head handled by one MFMA tile
-constexpr int kChunkKeys = 8192;   // keys one scoring workgroup streams
-constexpr int kWaveKeys = kChunkKeys / kWaves;
+constexpr int kWaveKeysMax = 2048; // keys one scoring wave streams (at most)
+constexpr int kCandBuf = 1024;     // candidates one scoring wave holds, over all its rows
+constexpr int kChunkCap = kWaves * kCandBuf;  // entries of one workgroup's packed block
+constexpr int kDenseChunk = 8192;  // keys per workgroup of the full-score kernels
 constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
 constexpr int kRepairParts = 16;   // workgroups per (sequence, KV head) in the repair stream
@@ -56,18 +58,20 @@ struct Params {
 struct Work {
   float *sample;     // [rows][kSampleMax] pilot sample scores
   float *theta;      // [rows] candidate threshold
-  int32_t *counts;   // [rows][nsub] candidates found by each scoring wave
-  uint2 *cand;       // [rows][nsub][capw] (order-preserving key, position)
+  int2 *dir;         // [rows][nchunk] (start, count) of the row's candidates in
+                     // its chunk's block; count -1 = a staging area overflowed
+  uint32_t *ckey;    // [B*Hkv][nchunk][kChunkCap] order-preserving score keys
+  uint16_t *cpos;    // [B*Hkv][nchunk][kChunkCap] positions within the chunk
   int32_t *flags;    // [rows] 1 = the row needs the exact fallback
   float *dense;      // [rows][ncap] fallback scores
   float *sigma;      // [rows][k_max] kept scores (group-shared mode) or softmax
                      // weights exp(scale*(s - max s)) (per-head mode), aligned with idx
   float *part;       // [B*Hq][nsplit][kPartStride] attend partials
   int32_t *stats;    // [4]: [0] rows repaired in the last call
-  int32_t nsub;
-  int32_t capw;
+  int32_t nchunk;      // chunks per sequence (of kWaves * wave_keys keys)
+  int32_t wave_keys;   // keys per scoring wave: 256, 512, 1024 or 2048
   int32_t nsplit;
-  int32_t force_repair;
+  int32_t force_repair;  // every row takes the exact fallback
 };
 
 // ---------------------------------------------------------------------------
@@ -396,9 +400,10 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
 
 // ---------------------------------------------------------------------------
 // Order-preserving compaction of the selection: walk items in order and keep
-// those with key > T plus the first need_eq with key == T.  emit(pos, item)
-// is called with the output slot of every kept item (slots 0..k-1 in item
-// order).  Each thread handles kIpt consecutive items per round.
+// those with key > T plus the first need_eq with key == T.  emit(slot, i, key)
+// is called for every kept item i with its output slot (0..k-1 in item
+// order).  Only keys are read here; the caller fetches whatever else a kept
+// item carries.  Each thread handles kIpt consecutive items per round.
 // ---------------------------------------------------------------------------
 constexpr int kIpt = 8;
 
@@ -410,13 +415,13 @@ __device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int n
 #pragma unroll 1
   for (int base = 0; base < n && sel_before < k; base += kBlock * kIpt) {
     const int p0 = base + tid * kIpt;
-    uint2 it[kIpt];
+    uint32_t key[kIpt];
     int n_eq = 0;
 #pragma unroll
     for (int u = 0; u < kIpt; ++u) {
       const int p = p0 + u;
-      it[u] = p < n ? src.get(p) : make_uint2(0u, 0u);
-      n_eq += (p < n && it[u].x == T) ? 1 : 0;
+      key[u] = p < n ? src.key(p) : 0u;
+      n_eq += (p < n && key[u] == T) ? 1 : 0;
     }
     int eq_tot;
     int eq_rank = block_excl_scan(n_eq, scan, &eq_tot) + eq_before;
@@ -427,9 +432,9 @@ __device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int n
       const int p = p0 + u;
       bool sel = false;
       if (p < n) {
-        if (it[u].x > T) {
+        if (key[u] > T) {
           sel = true;
-        } else if (it[u].x == T) {
+        } else if (key[u] == T) {
           sel = eq_rank < need_eq;
           ++eq_rank;
         }
@@ -438,10 +443,10 @@ __device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int n
       n_sel += sel ? 1 : 0;
     }
     int sel_tot;
-    int pos = block_excl_scan(n_sel, scan, &sel_tot) + sel_before;
+    int slot = block_excl_scan(n_sel, scan, &sel_tot) + sel_before;
 #pragma unroll
     for (int u = 0; u < kIpt; ++u)
-      if (sel_mask & (1u << u)) emit(pos++, it[u]);
+      if (sel_mask & (1u << u)) emit(slot++, p0 + u, key[u]);
     eq_before += eq_tot;
     sel_before += sel_tot;
   }

@@ -101,7 +101,11 @@ struct LdsKeys {
 
 // Per-row threshold = the r-th largest sample score, r = ceil(2.5 k m / L)
 // (so about 2.5 k of the L keys are expected to pass), or r = k when the
-// sample is the whole sequence.  Also clears the row's fallback flag.
+// sample is the whole sequence.  Also sets the row's fallback flag: rows
+// with k = 0 need nothing; the row takes the exact fallback (threshold +inf,
+// so it stages no candidates) when every row is forced to, or when its
+// expected candidates per wave, r * min(L, wave_keys) / m, exceed half of
+// its staging area (low sparsity).
 __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[2048];
@@ -109,23 +113,25 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   const int row = blockIdx.x, b = row / p.R;
   const int L = seq_len(p, b);
   const int k = row_budget(p, b, L);
-  if (threadIdx.x == 0) {
-    w.flags[row] = 0;
-    if (row == 0) w.stats[0] = 0;
-  }
-  if (k == 0 || w.force_repair) {
-    if (threadIdx.x == 0) w.theta[row] = __builtin_inff();
-    return;
-  }
+  if (threadIdx.x == 0 && row == 0) w.stats[0] = 0;
   const int m = L < kSampleMax ? L : kSampleMax;
-  int r;
-  if (m == L) {
-    r = k;
-  } else {
+  int r = k;
+  if (m < L) {
     const int64_t rr = (5LL * k * m + 2LL * L - 1) / (2LL * L);
     r = (int)(rr < m ? rr : m);
     if (r < 1) r = 1;
   }
+  const int cap = kCandBuf / (p.group_shared ? 1 : p.G);
+  const int64_t span = L < w.wave_keys ? L : w.wave_keys;
+  const bool dense = w.force_repair || 2LL * r * span > (int64_t)cap * m;
+  if (k == 0 || dense) {
+    if (threadIdx.x == 0) {
+      w.flags[row] = k > 0 ? 1 : 0;
+      w.theta[row] = __builtin_inff();
+    }
+    return;
+  }
+  if (threadIdx.x == 0) w.flags[row] = 0;
   for (int i = threadIdx.x; i < m; i += kBlock) keys[i] = f2key(w.sample[(int64_t)row * kSampleMax + i]);
   __syncthreads();
   uint32_t T;
@@ -137,254 +143,199 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
 }
 
 // ---------------------------------------------------------------------------
-// The scoring stream.  grid = (ceil(ncap / kChunkKeys), B*Hkv).  Wave v of
-// workgroup c streams keys [c*kChunkKeys + v*kWaveKeys, +kWaveKeys) of one
-// (sequence, KV head) in 16-key MFMA tiles, kDepth tiles in flight, and
-// writes its candidates of every row of the group to its own list
-// cand[row][c*4+v][0..capw) in position order; counts[row][c*4+v] gets the
-// number that passed (more than capw means the list overflowed).  Passing
-// keys are staged in LDS and written out in batches, so the streaming loop
-// issues no global stores and its load waits stay exact.
+// The scoring stream.  grid = (nchunk, B*Hkv); a chunk is kWaves * wk keys
+// (wk = w.wave_keys).  Wave v of workgroup c streams keys
+// [c*4wk + v*wk, +wk) of one (sequence, KV head) in 16-key MFMA tiles,
+// kDepth tiles in flight, and stages the keys at or above each row's
+// threshold in LDS, in position order, one area of kCandBuf / rows entries
+// per row of the group.  At the end the workgroup writes one packed block:
+// for every row its candidates (keys, then chunk-relative positions), in
+// position order, rows one after another; dir[row][c] gets the row's
+// (start, count) in the block, count -1 if one of its areas overflowed.
+// The streaming loop issues no global stores, so its load waits stay exact;
+// the block goes out in a few fully coalesced nontemporal stores.
 // ---------------------------------------------------------------------------
 constexpr int kDepth = 3;        // tiles in flight per wave
-constexpr int kCandBuf = 1024;   // candidates staged per wave, split evenly over its rows
-constexpr int kWavePages = kWaveKeys / kTile;
-static_assert(kCandBuf / kMaxGroup > kDepth * kTile, "a step must fit a row's staging area");
+constexpr int kWavePages = kWaveKeysMax / kTile;
+static_assert(kCandBuf / kMaxGroup >= kTile, "every row must hold a tile's keys");
+static_assert(kChunkCap % 4 == 0 && kWaves * kMaxGroup == 64, "block layout");
 
 struct WaveLds {
   u32x4 tile[256];
-  uint2 cand[kCandBuf + 64];   // per-row areas of (score bits, position), +64 discard slots
+  uint2 cand[kCandBuf + 64];   // per-row areas of (score bits, position in wave), +64 discard slots
   int32_t page[kWavePages];
 };
 
 // bfloat16 caches.  The loop body issues a fixed set of loads every step
-// (tile indices past the end are clamped to the last tile, whose rows the
-// filter masks), so the compiler's memory waits stay exact and kDepth tiles
-// stay in flight.  Each row served by the wave (a query head, or the KV head
-// in group-shared mode) owns an equal slice of an LDS staging buffer; a
-// passing key goes to its row's slice at the row's running count (lanes
-// whose key does not pass write a discard slot, so the append has no
-// branch).  A slice close to full is copied to the row's list in HBM with
-// coalesced stores; such a copy in mid-stream ends with a full wait on its
-// stores, which keeps the loop's load waits exact.
+// (tile indices past the end are clamped to the last tile, whose keys the
+// filter then masks), so the compiler's memory waits are exact.
 template <bool PAGED, bool GRP>
 __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   __shared__ WaveLds wlds[kWaves];
+  __shared__ int seg_n[kWaves * kMaxGroup];        // [row][wave] candidates found
+  __shared__ int seg_off[kWaves * kMaxGroup + 1];  // their offsets in the block
+  const int wk = w.wave_keys;
   const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
   const int L = seq_len(p, b);
-  const int64_t c0 = (int64_t)chunk * kChunkKeys;
-  if (c0 >= L) return;
+  const int64_t c0 = (int64_t)chunk * kWaves * wk;
+  if (c0 >= L) return;  // whole workgroup
   const int wv = wave_id();
-  const int64_t w0 = c0 + (int64_t)wv * kWaveKeys;
-  if (w0 >= L) return;
-  const int64_t w1 = (w0 + kWaveKeys < (int64_t)L) ? w0 + kWaveKeys : (int64_t)L;
-  const int nvalid = (int)(w1 - w0);
-  const int sub = chunk * kWaves + wv;
+  const int64_t w0 = c0 + (int64_t)wv * wk;
+  const int nvalid = w0 < L ? (int)((L - w0) < wk ? (L - w0) : wk) : 0;
   const int l = lane_id(), col = l & 15, s = l >> 4;
-  constexpr bool grp = GRP;
-  const int64_t row0 = grp ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
-  const int nrows = grp ? 1 : p.G;
+  const int64_t row0 = GRP ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
+  const int nrows = GRP ? 1 : p.G;
   const int cap = kCandBuf / nrows;  // staging slots per row
   WaveLds &wl = wlds[wv];
+  // Candidates found per row: lane group s counts rows 4s+r (wave-uniform
+  // within the group); counting continues past cap to detect overflow.
+  int cnt[4] = {0, 0, 0, 0};
 
-  QFrag qf;
-  load_q_bf16(p, b, g, qf);
-  // This lane serves rows 4s..4s+3 (heads of the group; heads beyond G never
-  // pass) or, in group-shared mode, lanes 0..15 serve the group's one row.
-  float th[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int h = 4 * s + r;
-    if (grp) th[r] = (s == 0 && r == 0) ? w.theta[row0] : __builtin_inff();
-    else th[r] = h < p.G ? w.theta[row0 + h] : __builtin_inff();
-  }
-  const int ntiles = (nvalid + kTile - 1) / kTile;
-  if (PAGED) {
-    const int32_t *bt = p.K.block_table + (int64_t)b * p.K.max_pages + (w0 >> 4);
-    for (int i = l; i < ntiles; i += 64) wl.page[i] = bt[i];
-    __builtin_amdgcn_wave_barrier();  // every lane reads every page id
-  }
-  const char *kbase = (const char *)p.K.base;
-  constexpr int64_t kRowBytes = kHeadDim * 2;
-  const char *slab = kbase + (((int64_t)b * p.K.hkv + g) * p.K.ncap + w0) * kRowBytes;
-  const int64_t page_bytes = (int64_t)kTile * p.K.hkv * kRowBytes;
-  const int a = l >> 4;
-  const int last = nvalid - 1;
-  int lane_row[4], lane_chunk[4];
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    lane_row[t] = 4 * t + a;
-    lane_chunk[t] = 16 * swz_chunk(t);
-  }
-  // Issue the four coalesced loads of tile ti (clamped to the last tile).
-  auto load = [&](int ti, u32x4 v[4]) {
-    ti = ti < ntiles ? ti : ntiles - 1;
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      int j = ti * kTile + lane_row[t];
-      j = j < last ? j : last;
-      const char *row;
-      if (PAGED) row = kbase + wl.page[ti] * page_bytes + ((int64_t)(j & 15) * p.K.hkv + g) * kRowBytes;
-      else row = slab + (int64_t)j * kRowBytes;
-      v[t] = __builtin_nontemporal_load((const u32x4 *)(row + lane_chunk[t]));
-    }
-  };
-
-  // Per-row counts: staged in LDS (cnt) and already written to HBM (done).
-  // Lane group s keeps those of its rows 4s+r (wave-uniform per group).
-  int cnt[4] = {0, 0, 0, 0}, done[4] = {0, 0, 0, 0};
-  // Copy every row's staged slice to its list (row h's counts live in lane
-  // group h >> 2).
-  auto flush = [&]() {
-    __builtin_amdgcn_wave_barrier();  // slices were written by other lanes
-    for (int h = 0; h < nrows; ++h) {
-      const int src_lane = 16 * (h >> 2);
-      int nh = 0, dh = 0;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int c_ = __shfl(cnt[r], src_lane), d_ = __shfl(done[r], src_lane);
-        if ((h & 3) == r) { nh = c_; dh = d_; }
-      }
-      uint2 *dst = w.cand + ((row0 + h) * w.nsub + sub) * (int64_t)w.capw;
-      const uint2 *srcp = wl.cand + h * cap;
-      for (int e = l; e < nh; e += 64) {
-        const int slot = dh + e;
-        const uint2 it = srcp[e];
-        if (slot < w.capw) dst[slot] = make_uint2(f2key(__uint_as_float(it.x)), (uint32_t)w0 + it.y);
-      }
-    }
+  if (nvalid > 0) {  // wave-uniform
+    QFrag qf;
+    load_q_bf16(p, b, g, qf);
+    // This lane filters rows 4s..4s+3 (heads of the group; heads beyond G
+    // never pass) or, in group-shared mode, lanes 0..15 the group's one row.
+    float th[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      done[r] += cnt[r];
-      cnt[r] = 0;
-    }
-  };
-
-  // Append the passing keys of one scored tile to their rows' slices.
-  auto filter = [&](f32x4 acc, int jl) {
-    const bool live = jl < nvalid;
-    if (grp) acc[0] = group_sum(acc);
-#pragma unroll
-    for (int r = 0; r < (grp ? 1 : 4); ++r) {
-      const bool pass = live && acc[r] >= th[r];
-      const uint32_t gm = (uint32_t)(__ballot(pass) >> (16 * s)) & 0xFFFFu;
-      const int e = pass ? (4 * s + r) * cap + cnt[r] + __popc(gm & ((1u << col) - 1u))
-                         : kCandBuf + l;
-      wl.cand[e] = make_uint2(__float_as_uint(acc[r]), (uint32_t)jl);
-      cnt[r] += __popc(gm);
-    }
-  };
-
-  const int nsteps = (ntiles + kDepth - 1) / kDepth * kDepth;
-  // A step filters kDepth tiles: at most 16 keys per row each.
-  const int flush_at = cap - kDepth * kTile;
-  u32x4 buf[kDepth][4];
-#pragma unroll
-  for (int d = 0; d < kDepth; ++d) {
-    load(d, buf[d]);
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  // The scores of a tile are filtered one step later, after the next tile's
-  // loads and matrix ops are issued, so the appends (which wait on the
-  // matrix results) never hold up the stream.
-  f32x4 prev = {0.f, 0.f, 0.f, 0.f};
-  int prev_jl = nvalid;  // nothing to filter before the first tile
-  for (int tb = 0; tb < nsteps; tb += kDepth) {
-    const int most = max(max(cnt[0], cnt[1]), max(cnt[2], cnt[3]));
-    if (__ballot(most > flush_at)) {
-      flush();
-      __builtin_amdgcn_s_waitcnt(0);
-    }
-#pragma unroll
-    for (int u = 0; u < kDepth; ++u) {
-      const int ti = tb + u;
-      stage_tile(wl.tile, buf[u]);
-      load(ti + kDepth, buf[u]);
-      __builtin_amdgcn_wave_barrier();  // the tile is read back by other lanes
-      KFrag kf;
-      read_kfrag(wl.tile, kf);
-      __builtin_amdgcn_wave_barrier();  // and overwritten by the next step
-      const f32x4 acc = mfma_scores(qf, kf);
-      filter(prev, prev_jl);
-      prev = acc;
-      prev_jl = ti * kTile + col;
-    }
-  }
-  filter(prev, prev_jl);
-  flush();
-  if (col == 0) {
-#pragma unroll
-    for (int r = 0; r < (grp ? 1 : 4); ++r) {
       const int h = 4 * s + r;
-      if (h < nrows) w.counts[(row0 + h) * w.nsub + sub] = done[r];
+      if (GRP) th[r] = (s == 0 && r == 0) ? w.theta[row0] : __builtin_inff();
+      else th[r] = h < p.G ? w.theta[row0 + h] : __builtin_inff();
     }
-  }
-}
-
-// float32 caches (small problems): vector-ALU scoring, direct list writes.
-__global__ __launch_bounds__(kBlock) void k_score_filter_f32(Params p, Work w) {
-  __shared__ float q_lds[kMaxGroup * kHeadDim];
-  const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
-  const int L = seq_len(p, b);
-  const int64_t c0 = (int64_t)chunk * kChunkKeys;
-  if (c0 >= L) return;  // whole workgroup: no barrier follows
-  Scorer<false> sc;
-  scorer_init<false>(p, b, g, sc, q_lds);
-  const int wv = wave_id();
-  const int64_t w0 = c0 + (int64_t)wv * kWaveKeys;
-  if (w0 >= L) return;
-  const int64_t w1 = (w0 + kWaveKeys < (int64_t)L) ? w0 + kWaveKeys : (int64_t)L;
-  const int sub = chunk * kWaves + wv;
-  const int l = lane_id(), col = l & 15, s = l >> 4;
-  const uint32_t below = (1u << col) - 1u;
-  const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
-  float th[4];
-  int cnt[4] = {0, 0, 0, 0};
-  uint2 *cl[4];
+    const int ntiles = (nvalid + kTile - 1) / kTile;
+    if (PAGED) {
+      const int32_t *bt = p.K.block_table + (int64_t)b * p.K.max_pages + (w0 >> 4);
+      for (int i = l; i < ntiles; i += 64) wl.page[i] = bt[i];
+      __builtin_amdgcn_wave_barrier();  // every lane reads every page id
+    }
+    const char *kbase = (const char *)p.K.base;
+    constexpr int64_t kRowBytes = kHeadDim * 2;
+    const char *slab = kbase + (((int64_t)b * p.K.hkv + g) * p.K.ncap + w0) * kRowBytes;
+    const int64_t page_bytes = (int64_t)kTile * p.K.hkv * kRowBytes;
+    const int a = l >> 4;
+    const int last = nvalid - 1;
+    int lane_row[4], lane_chunk[4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int h = 4 * s + r;
-    const int64_t row = p.group_shared ? row0 : row0 + (h < p.G ? h : 0);
-    th[r] = w.theta[row];
-    cl[r] = w.cand + (row * w.nsub + sub) * (int64_t)w.capw;
-  }
-  for (int64_t j0 = w0; j0 < w1; j0 += kTile) {
-    const int64_t jl = j0 + col < w1 ? j0 + col : w1 - 1;
-    const f32x4 acc = sc.score(p, b, g, jl);
-    const int64_t j = j0 + col;
-    const bool valid = j < w1;
-    if (!p.group_shared) {
+    for (int t = 0; t < 4; ++t) {
+      lane_row[t] = 4 * t + a;
+      lane_chunk[t] = 16 * swz_chunk(t);
+    }
+    // Issue the four coalesced loads of tile ti (clamped to the last tile).
+    auto load = [&](int ti, u32x4 v[4]) {
+      ti = ti < ntiles ? ti : ntiles - 1;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const bool pass = valid && (4 * s + r) < p.G && acc[r] >= th[r];
+      for (int t = 0; t < 4; ++t) {
+        int j = ti * kTile + lane_row[t];
+        j = j < last ? j : last;
+        const char *row;
+        if (PAGED) row = kbase + wl.page[ti] * page_bytes + ((int64_t)(j & 15) * p.K.hkv + g) * kRowBytes;
+        else row = slab + (int64_t)j * kRowBytes;
+        v[t] = __builtin_nontemporal_load((const u32x4 *)(row + lane_chunk[t]));
+      }
+    };
+    // Append the passing keys of one scored tile to their rows' areas;
+    // keys past an area's end go to this lane's discard slot.
+    auto filter = [&](f32x4 acc, int jl) {
+      const bool live = jl < nvalid;
+      if (GRP) acc[0] = group_sum(acc);
+#pragma unroll
+      for (int r = 0; r < (GRP ? 1 : 4); ++r) {
+        const bool pass = live && acc[r] >= th[r];
         const uint32_t gm = (uint32_t)(__ballot(pass) >> (16 * s)) & 0xFFFFu;
-        if (pass) {
-          const int slot = cnt[r] + __popc(gm & below);
-          if (slot < w.capw) cl[r][slot] = make_uint2(f2key(acc[r]), (uint32_t)j);
-        }
+        const int slot = cnt[r] + __popc(gm & ((1u << col) - 1u));
+        const int e = (pass && slot < cap) ? (4 * s + r) * cap + slot : kCandBuf + l;
+        wl.cand[e] = make_uint2(__float_as_uint(acc[r]), (uint32_t)jl);
         cnt[r] += __popc(gm);
       }
-    } else {
-      const float gs = group_sum(acc);
-      const bool pass = valid && s == 0 && gs >= th[0];
-      const uint32_t gm = (uint32_t)__ballot(pass) & 0xFFFFu;
-      if (pass) {
-        const int slot = cnt[0] + __popc(gm & below);
-        if (slot < w.capw) cl[0][slot] = make_uint2(f2key(gs), (uint32_t)j);
-      }
-      cnt[0] += __popc(gm);
+    };
+
+    const int nsteps = (ntiles + kDepth - 1) / kDepth * kDepth;
+    u32x4 buf[kDepth][4];
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+      load(d, buf[d]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    // The scores of a tile are filtered one step later, after the next
+    // tile's loads and matrix ops are issued, so the appends (which wait on
+    // the matrix results) never hold up the stream.
+    f32x4 prev = {0.f, 0.f, 0.f, 0.f};
+    int prev_jl = nvalid;  // nothing to filter before the first tile
+    for (int tb = 0; tb < nsteps; tb += kDepth) {
+#pragma unroll
+      for (int u = 0; u < kDepth; ++u) {
+        const int ti = tb + u;
+        stage_tile(wl.tile, buf[u]);
+        load(ti + kDepth, buf[u]);
+        __builtin_amdgcn_wave_barrier();  // the tile is read back by other lanes
+        KFrag kf;
+        read_kfrag(wl.tile, kf);
+        __builtin_amdgcn_wave_barrier();  // and overwritten by the next step
+        const f32x4 acc = mfma_scores(qf, kf);
+        filter(prev, prev_jl);
+        prev = acc;
+        prev_jl = ti * kTile + col;
+      }
+    }
+    filter(prev, prev_jl);
   }
   if (col == 0) {
-    if (!p.group_shared) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int h = 4 * s + r;
-        if (h < p.G) w.counts[(row0 + h) * w.nsub + sub] = cnt[r];
-      }
-    } else if (s == 0) {
-      w.counts[row0 * w.nsub + sub] = cnt[0];
+    for (int r = 0; r < 4; ++r) {
+      const int h = 4 * s + r;
+      if (h < nrows) seg_n[h * kWaves + wv] = cnt[r];
     }
+  }
+  __syncthreads();
+
+  // Block layout: segment t = (row t/4, wave t%4), rows in order.
+  const int tid = threadIdx.x;
+  if (tid < 64) {
+    const int h = tid / kWaves;
+    const int n = h < nrows ? seg_n[tid] : 0;
+    const int nc = n < cap ? n : cap;
+    const int inc = wave_incl_scan(nc);
+    const int row_end = __shfl(inc, (tid | (kWaves - 1)));
+    const uint64_t over = __ballot(n > cap);
+    seg_off[tid] = inc - nc;
+    if (tid == 63) seg_off[64] = inc;
+    if (tid % kWaves == 0 && h < nrows) {
+      const int start = inc - nc;
+      const bool ovf = ((over >> tid) & ((1ull << kWaves) - 1ull)) != 0;
+      w.dir[(row0 + h) * w.nchunk + chunk] = make_int2(start, ovf ? -1 : row_end - start);
+    }
+  }
+  __syncthreads();
+  const int ntot = seg_off[64];
+  const int64_t blk = ((int64_t)bg * w.nchunk + chunk) * kChunkCap;
+  uint32_t *kdst = w.ckey + blk;
+  uint16_t *pdst = w.cpos + blk;
+  for (int i0 = 4 * tid; i0 < ntot; i0 += 4 * kBlock) {
+    // Segment of item i0: the last t with seg_off[t] <= i0.
+    int t = 0;
+#pragma unroll
+    for (int step = 32; step > 0; step >>= 1)
+      if (seg_off[t + step] <= i0) t += step;
+    u32x4 kv;
+    uint32_t pv[2] = {0u, 0u};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u;
+      uint32_t key = 0u, pos = 0u;
+      if (i < ntot) {
+        while (seg_off[t + 1] <= i) ++t;  // stops at t = 63: seg_off[64] = ntot > i
+        const int h = t / kWaves, v = t % kWaves;
+        const uint2 it = wlds[v].cand[h * cap + (i - seg_off[t])];
+        key = f2key(__uint_as_float(it.x));
+        pos = (uint32_t)(v * wk) + it.y;
+      }
+      kv[u] = key;
+      pv[u >> 1] |= pos << (16 * (u & 1));
+    }
+    __builtin_nontemporal_store(kv, (u32x4 *)(kdst + i0));
+    __builtin_nontemporal_store((unsigned long long)pv[0] | ((unsigned long long)pv[1] << 32),
+                                (unsigned long long *)(pdst + i0));
   }
 }
 
@@ -442,32 +393,41 @@ __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, Work w, float 
 struct DenseSrc {
   const float *row;
   __device__ __forceinline__ uint32_t key(int i) const { return f2key(row[i]); }
-  __device__ __forceinline__ uint2 get(int i) const { return make_uint2(f2key(row[i]), (uint32_t)i); }
+  __device__ __forceinline__ uint32_t pos(int i) const { return (uint32_t)i; }
 };
 
-struct LdsCands {
-  const uint32_t *keys;
-  const uint32_t *pos;
-  __device__ __forceinline__ uint32_t key(int i) const { return keys[i]; }
-  __device__ __forceinline__ uint2 get(int i) const { return make_uint2(keys[i], pos[i]); }
-};
-
-// Candidate lists read in place: item i lives in the last list s with
-// pre[s] <= i (empty lists share their successor's prefix value).
-struct GlobalCands {
-  const uint2 *lists;  // this row's lists, capw entries apart
-  const int *pre;      // LDS prefix sums, n_lists + 1 entries
-  int n_lists;
-  int capw;
-  __device__ __forceinline__ uint2 get(int i) const {
-    int lo = 0, hi = n_lists - 1;
+// The candidates of one row, chunk by chunk: chunk c contributes
+// pre[c+1] - pre[c] items stored from offset start[c] of its block.  Keys
+// are read from LDS when they were staged there (lkey), else from the blocks.
+struct ChunkCands {
+  const uint32_t *lkey;
+  const int *pre;        // nch + 1 prefix sums (LDS)
+  const int *start;      // nch block offsets (LDS)
+  int nch;
+  const uint32_t *gkey;  // the group's blocks, kChunkCap entries apart
+  const uint16_t *gpos;
+  int ck;                // keys per chunk
+  // Chunk holding item i: the last c with pre[c] <= i (empty chunks share
+  // their successor's prefix value, so this is the owner).
+  __device__ __forceinline__ int chunk_of(int i) const {
+    int lo = 0, hi = nch - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
       if (pre[mid] <= i) lo = mid; else hi = mid - 1;
     }
-    return lists[(int64_t)lo * capw + (i - pre[lo])];
+    return lo;
   }
-  __device__ __forceinline__ uint32_t key(int i) const { return get(i).x; }
+  __device__ __forceinline__ int64_t slot(int c, int i) const {
+    return (int64_t)c * kChunkCap + start[c] + (i - pre[c]);
+  }
+  __device__ __forceinline__ uint32_t key(int i) const {
+    if (lkey) return lkey[i];
+    return gkey[slot(chunk_of(i), i)];
+  }
+  __device__ __forceinline__ uint32_t pos(int i) const {
+    const int c = chunk_of(i);
+    return (uint32_t)c * (uint32_t)ck + gpos[slot(c, i)];
+  }
 };
 
 template <class Src>
@@ -476,9 +436,9 @@ __device__ __forceinline__ void select_and_write(const Src &src, int n, int k, u
   uint32_t T;
   int need_eq;
   radix_select(src, n, k, hist, sh, T, need_eq);
-  compact_selected(src, n, k, T, need_eq, sh->scan, [&](int pos, uint2 it) {
-    irow[pos] = (int32_t)it.y;
-    if (vrow) vrow[pos] = key2f(it.x);
+  compact_selected(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
+    irow[slot] = (int32_t)src.pos(i);
+    if (vrow) vrow[slot] = key2f(key);
   });
 }
 
@@ -512,24 +472,34 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   const int tid = threadIdx.x;
   if (k > 0) {
     if (MODE == 0) {
-      const int n_lists = (L + kWaveKeys - 1) / kWaveKeys;
-      int *pre = (int *)dyn;  // n_lists + 1
-      uint32_t *ckey = dyn + (n_lists + 1);
-      uint32_t *cpos = ckey + lds_cap;
-      const int32_t *counts = w.counts + (int64_t)row * w.nsub;
+      if (w.flags[row]) {  // routed to the fallback by the pilot
+        if (tid == 0) atomicAdd(&w.stats[0], 1);
+        return;
+      }
+      const int ck = kWaves * w.wave_keys;
+      const int nch = (L + ck - 1) / ck;
+      const int rr = row % p.R;
+      const int g = p.group_shared ? rr : rr / p.G;
+      int *pre = (int *)dyn;          // nch + 1
+      int *start = pre + (nch + 1);   // nch
+      uint32_t *lkey = (uint32_t *)(start + nch);
+      const int2 *drow = w.dir + (int64_t)row * w.nchunk;
       if (tid == 0) status = 0;
       __syncthreads();
       int carry = 0;
-      for (int base = 0; base < n_lists; base += kBlock) {
-        const int s = base + tid;
-        const int c = s < n_lists ? counts[s] : 0;
-        if (c > w.capw) status = 1;  // a list overflowed
+      for (int base = 0; base < nch; base += kBlock) {
+        const int c = base + tid;
+        const int2 d = c < nch ? drow[c] : make_int2(0, 0);
+        if (d.y < 0) status = 1;  // a staging area overflowed
         int tot;
-        const int e = block_excl_scan(c, sh.scan, &tot);
-        if (s < n_lists) pre[s] = carry + e;
+        const int e = block_excl_scan(d.y > 0 ? d.y : 0, sh.scan, &tot);
+        if (c < nch) {
+          pre[c] = carry + e;
+          start[c] = d.x;
+        }
         carry += tot;
       }
-      if (tid == 0) pre[n_lists] = carry;
+      if (tid == 0) pre[nch] = carry;
       __syncthreads();
       const int total = carry;
       if (status || total < k) {
@@ -539,24 +509,27 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
         }
         return;
       }
-      const uint2 *lists = w.cand + (int64_t)row * w.nsub * w.capw;
-      GlobalCands gsrc{lists, pre, n_lists, w.capw};
+      const int64_t gblk = ((int64_t)b * p.Hkv + g) * w.nchunk * kChunkCap;
+      ChunkCands src{nullptr, pre, start, nch, w.ckey + gblk, w.cpos + gblk, ck};
       if (total <= lds_cap) {
-        // One wave per list: the list's entries are contiguous in memory.
-        for (int sl = wave_id(); sl < n_lists; sl += kWaves) {
-          const int c0 = pre[sl], cnt = pre[sl + 1] - c0;
-          const uint2 *src = lists + (int64_t)sl * w.capw;
-          for (int e = lane_id(); e < cnt; e += 64) {
-            const uint2 it = src[e];
-            ckey[c0 + e] = it.x;
-            cpos[c0 + e] = it.y;
+        constexpr int kU = 4;  // loads in flight per thread
+        for (int i0 = tid; i0 < total; i0 += kBlock * kU) {
+          uint32_t v[kU];
+#pragma unroll
+          for (int u = 0; u < kU; ++u) {
+            const int i = i0 + u * kBlock;
+            v[u] = i < total ? src.key(i) : 0u;
+          }
+#pragma unroll
+          for (int u = 0; u < kU; ++u) {
+            const int i = i0 + u * kBlock;
+            if (i < total) lkey[i] = v[u];
           }
         }
         __syncthreads();
-        select_and_write(LdsCands{ckey, cpos}, total, k, hist, &sh, irow, vrow);
-      } else {
-        select_and_write(gsrc, total, k, hist, &sh, irow, vrow);
+        src.lkey = lkey;
       }
+      select_and_write(src, total, k, hist, &sh, irow, vrow);
     } else {
       select_and_write(DenseSrc{dense + (int64_t)row * ld}, L, k, hist, &sh, irow, vrow);
     }
@@ -825,17 +798,18 @@ __global__ __launch_bounds__(kHeadDim) void k_merge(Params p, Work w, void *out,
 static inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
 
 hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
-  const dim3 g1(8, p.B * p.Hkv);
-  if (p.bf16) k_pilot_score<true><<<g1, kBlock, 0, st>>>(p, w);
-  else k_pilot_score<false><<<g1, kBlock, 0, st>>>(p, w);
+  if (!w.force_repair) {
+    const dim3 g1(8, p.B * p.Hkv);
+    k_pilot_score<true><<<g1, kBlock, 0, st>>>(p, w);
+  }
   k_pilot_select<<<p.B * p.R, kBlock, 0, st>>>(p, w);
   return hipGetLastError();
 }
 
-hipError_t launch_score_filter(const Params &p, const Work &w, hipStream_t st) {
-  const dim3 grid(cdiv(p.ncap, kChunkKeys), p.B * p.Hkv);
-  if (!p.bf16) k_score_filter_f32<<<grid, kBlock, 0, st>>>(p, w);
-  else if (p.K.paged) {
+hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st) {
+  if (w.force_repair) return hipSuccess;  // every row takes the fallback
+  const dim3 grid(w.nchunk, p.B * p.Hkv);
+  if (p.K.paged) {
     if (p.group_shared) k_score_stream<true, true><<<grid, kBlock, 0, st>>>(p, w);
     else k_score_stream<true, false><<<grid, kBlock, 0, st>>>(p, w);
   } else {
@@ -845,14 +819,13 @@ hipError_t launch_score_filter(const Params &p, const Work &w, hipStream_t st) {
   return hipGetLastError();
 }
 
-size_t select_lds_bytes(const Params &p, int lds_cap) {
-  const int n_lists = (int)cdiv(p.ncap, kWaveKeys);
-  return (size_t)(n_lists + 1) * 4 + (size_t)lds_cap * 8;
+size_t select_lds_bytes(int nchunk, int lds_cap) {
+  return (size_t)(2 * nchunk + 1) * 4 + (size_t)lds_cap * 4;
 }
 
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
                                     hipStream_t st) {
-  const size_t lds = select_lds_bytes(p, lds_cap);
+  const size_t lds = select_lds_bytes(w.nchunk, lds_cap);
   k_select<0><<<p.B * p.R, kBlock, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
   return hipGetLastError();
 }
@@ -920,7 +893,7 @@ hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, voi
 }
 
 hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st) {
-  const dim3 grid(cdiv(p.ncap, kChunkKeys), p.B * p.Hkv);
+  const dim3 grid(cdiv(p.ncap, kDenseChunk), p.B * p.Hkv);
   Work none{};
   if (p.bf16) k_score_dense<true, false, true><<<grid, kBlock, 0, st>>>(p, none, scores, p.ncap);
   else k_score_dense<false, false, true><<<grid, kBlock, 0, st>>>(p, none, scores, p.ncap);

@@ -265,13 +265,35 @@ def test_group_shared_mode_group_sizes(sd, G):
 
 @pytest.mark.parametrize("name,ratio", [("w3", 4.0), ("w2", 6.0), ("w5", 5.0), ("w4", 8.0)])
 def test_long_candidate_lists(sd, name, ratio):
-    # Low sparsity: each scoring wave stages hundreds of candidates per row,
-    # so its lists span several 64-entry batches and the staging buffer is
-    # written out in mid-stream (regression test for both).
+    # Low sparsity: hundreds of candidates per row and wave, so the scoring
+    # waves shrink, and rows too dense for the staging areas are sent to the
+    # exact fallback by the pilot.
     kw = {"w4": dict(B=2, lmin=6000, lmax=9000, N=9000)}.get(name, dict(B=1, N=12000))
     inp = make(name, seed=14, ratio=ratio, **kw)
     out, idx, _ = gpu_fused(sd, inp)
     check_fused(inp, out, idx, label=f"{name} ratio {ratio}")
+
+
+def test_clustered_candidates_overflow_to_the_exact_fallback(sd):
+    # 400 consecutive keys close to head 0's query direction: all of them
+    # pass head 0's threshold inside one scoring wave, more than its staging
+    # area holds, so the row must take the exact fallback.
+    inp = make("w2", seed=15, B=1, N=12000, ratio=50.0)
+    rng = np.random.default_rng(15)
+    q0 = synth.bf16_to_f32(inp.q[0, 0]).astype(np.float64)
+    base = 3.0 * q0 / np.linalg.norm(q0) * np.sqrt(inp.d)
+    clus = base[None, :] + 0.3 * rng.standard_normal((400, inp.d))
+    k = inp.k.copy()
+    k[0, 0, 100:500] = synth.bf16_bits(clus.astype(np.float32))
+    inp = dataclasses.replace(inp, k=k)
+    sd.set_profiling(True)
+    out, idx, _ = gpu_fused(sd, inp)
+    prof = sd.last_profile()
+    sd.set_profiling(False)
+    assert prof["repaired_rows"] >= 1
+    check_fused(inp, out, idx, label="clustered overflow")
+    k0 = int(P.budgets(inp)[0])
+    assert set(idx[0, 0, :k0]) <= set(range(100, 500))
 
 
 def test_float32_gqa_and_paged(sd):
