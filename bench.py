@@ -25,8 +25,9 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
 METRIC = "sparse decode attention: queries/sec + achieved HBM GB/s vs peak at N=128K"
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "score_filter_counters.json")
-KERNEL_SRC = os.path.join(ROOT, "paper_2605_24168_amd", "csrc", "sd_kernels.hip")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "score_stream_w3_counters.json")
+KERNEL_SRC = [os.path.join(ROOT, "paper_2605_24168_amd", "csrc", f)
+              for f in ("sd_kernels.hip", "sd_internal.hpp")]
 
 
 def log(msg):
@@ -34,8 +35,12 @@ def log(msg):
 
 
 def kernel_hash() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of the kernel sources (counters taken on other sources are stale)."""
+    h = hashlib.sha256()
+    for path in KERNEL_SRC:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def path_bytes(inp, ks):
@@ -100,6 +105,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=4,
                     help="sequences of the workload the CPU oracle is timed on (0: skip)")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, copy this many MiB device to device once (a plain "
+                         "copy of known size that scales hardware traffic counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -176,7 +184,7 @@ def main():
                    "layout": inp.layout, "group_shared": inp.group_shared},
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_score_filter",
+            "kernel": "k_score_stream",
             "achieved": score_gbps,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
@@ -200,6 +208,15 @@ def main():
         },
     }
     del q, cache, lens, out, idx, ws
+    if args.copy_mib > 0:
+        n = args.copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        rec["copy_calibration_bytes"] = n
+        del src, dst
     if args.cpu_sample > 0:
         log(f"timing the CPU oracle on {args.cpu_sample} sequences")
         rec["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample)

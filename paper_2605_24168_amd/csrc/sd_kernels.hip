@@ -442,6 +442,125 @@ __device__ __forceinline__ void select_and_write(const Src &src, int n, int k, u
   });
 }
 
+// Candidates whose keys are staged in LDS (src.lkey), kmin..kmax their key
+// range.  The k-th largest key is found with one histogram over 2048 value
+// buckets, bucket(v) = min(2047, floor((v - vmin) * 2048 / (vmax - vmin))),
+// which is monotone in v (rounded subtraction and scaling by a positive
+// constant preserve order), so a higher bucket holds only larger scores;
+// inside the bucket that holds the k-th largest, an exact rank count over
+// its few items gives the key T and the number need_eq of items equal to T
+// that are kept.  (Radix passes over the key bits are the fallback: equal
+// extremes, non-finite ranges, or a crowded bucket.)  The compaction then
+// records each kept item's index in place of the consumed keys (slot <= item
+// index, and a round reads all its keys before its scans) and writes the
+// softmax weights exp(scale * (s - vmax)) (or, group-shared mode, the kept
+// scores), and every thread fetches the positions of its kept items with
+// the loads in flight together.
+constexpr int kBuckets = 2048;
+constexpr int kBucketItems = kBlock;  // items of the k-th bucket ranked exactly
+
+__device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, int n, int k,
+                                                        uint32_t kmin, uint32_t kmax,
+                                                        uint32_t *hist, SelShared *sh,
+                                                        uint32_t *bitems, int *nbitems,
+                                                        int32_t *irow, float *vrow,
+                                                        bool weights, float scale) {
+  const int tid = threadIdx.x;
+  const float vmin = key2f(kmin), vmax = key2f(kmax);
+  const float inv = (float)kBuckets / (vmax - vmin);
+  uint32_t T = kmin;
+  int need_eq = k;
+  bool found = kmin == kmax;  // all candidates equal: the first k are kept
+  if (!found && __builtin_isfinite(vmin) && __builtin_isfinite(inv) && inv > 0.f) {
+    auto bucket = [&](uint32_t key) {
+      const int bk = (int)((key2f(key) - vmin) * inv);
+      return bk < kBuckets - 1 ? bk : kBuckets - 1;
+    };
+    for (int i = tid; i < kBuckets; i += kBlock) hist[i] = 0;
+    __syncthreads();
+    for (int base = 0; base < n; base += kBlock) {
+      const int i = base + tid;
+      const uint32_t key = i < n ? src.lkey[i] : kmin;
+      hist_add(hist, (uint32_t)bucket(key), i < n);
+    }
+    __syncthreads();
+    // Thread t owns buckets [nb - (t+1)*bpt, nb - t*bpt), counted from the top.
+    constexpr int bpt = kBuckets / kBlock;
+    const int hi = kBuckets - tid * bpt;
+    int mine = 0;
+    for (int j = 1; j <= bpt; ++j) mine += (int)hist[hi - j];
+    int tot;
+    const int before = block_excl_scan(mine, sh->scan, &tot);
+    if (tid == 0) *nbitems = 0;
+    if (before < k && k <= before + mine) {
+      int cum = before;
+      for (int j = 1; j <= bpt; ++j) {
+        const int c = (int)hist[hi - j];
+        if (cum + c >= k) {
+          sh->digit = (uint32_t)(hi - j);
+          sh->above = cum;
+          break;
+        }
+        cum += c;
+      }
+    }
+    __syncthreads();
+    const int bstar = (int)sh->digit;
+    const int krem = k - sh->above;
+    const int m = (int)hist[bstar];
+    if (m <= kBucketItems) {  // uniform
+      for (int base = 0; base < n; base += kBlock) {
+        const int i = base + tid;
+        if (i < n) {
+          const uint32_t key = src.lkey[i];
+          if (bucket(key) == bstar) bitems[atomicAdd(nbitems, 1)] = key;
+        }
+      }
+      __syncthreads();
+      if (tid < m) {
+        const uint32_t x = bitems[tid];
+        int gt = 0, ge = 0;
+        for (int y = 0; y < m; ++y) {
+          const uint32_t v = bitems[y];
+          gt += v > x ? 1 : 0;
+          ge += v >= x ? 1 : 0;
+        }
+        if (gt < krem && krem <= ge) {  // x is the krem-th largest (equal items agree)
+          sh->digit = x;
+          sh->above = gt;
+        }
+      }
+      __syncthreads();
+      T = sh->digit;
+      need_eq = krem - sh->above;
+      found = true;
+    }
+    __syncthreads();  // sh is reused below
+  }
+  if (!found) radix_select(src, n, k, hist, sh, T, need_eq);
+  uint32_t *stage = const_cast<uint32_t *>(src.lkey);
+  compact_selected(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
+    stage[slot] = (uint32_t)i;
+    const float v = key2f(key);
+    vrow[slot] = weights ? expf(scale * (v - vmax)) : v;
+  });
+  __syncthreads();
+  constexpr int kP = 4;
+  for (int s0 = tid; s0 < k; s0 += kBlock * kP) {
+    uint32_t pos[kP];
+#pragma unroll
+    for (int u = 0; u < kP; ++u) {
+      const int s = s0 + u * kBlock;
+      pos[u] = s < k ? src.pos((int)stage[s]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kP; ++u) {
+      const int s = s0 + u * kBlock;
+      if (s < k) irow[s] = (int32_t)pos[u];
+    }
+  }
+}
+
 // Per-head rows of the fused path: turn the kept scores (vrow[0..k), written
 // by this workgroup) into softmax weights exp(scale*(s - max s)) in place, so
 // that the attention is a plain weighted gather whose splits all share one
@@ -462,6 +581,10 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   __shared__ SelShared sh;
   __shared__ int status;
   __shared__ float ftmp[kWaves];
+  __shared__ uint32_t range[kWaves][2];
+  __shared__ uint32_t bitems[kBucketItems];
+  __shared__ int nbitems;
+  bool weights_done = false;
   const int row = blockIdx.x, b = row / p.R;
   if (MODE == 2 && w.flags[row] == 0) return;
   const bool weights = MODE != 1 && !p.group_shared;
@@ -512,7 +635,8 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
       const int64_t gblk = ((int64_t)b * p.Hkv + g) * w.nchunk * kChunkCap;
       ChunkCands src{nullptr, pre, start, nch, w.ckey + gblk, w.cpos + gblk, ck};
       if (total <= lds_cap) {
-        constexpr int kU = 4;  // loads in flight per thread
+        constexpr int kU = 16;  // loads in flight per thread
+        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
         for (int i0 = tid; i0 < total; i0 += kBlock * kU) {
           uint32_t v[kU];
 #pragma unroll
@@ -523,17 +647,41 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
 #pragma unroll
           for (int u = 0; u < kU; ++u) {
             const int i = i0 + u * kBlock;
-            if (i < total) lkey[i] = v[u];
+            if (i < total) {
+              lkey[i] = v[u];
+              mn = v[u] < mn ? v[u] : mn;
+              mx = v[u] > mx ? v[u] : mx;
+            }
           }
         }
+        // Block-wide key range (the sync also publishes lkey).
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+          const uint32_t a = __shfl_xor(mn, o), c = __shfl_xor(mx, o);
+          mn = a < mn ? a : mn;
+          mx = c > mx ? c : mx;
+        }
+        if (lane_id() == 0) {
+          range[wave_id()][0] = mn;
+          range[wave_id()][1] = mx;
+        }
         __syncthreads();
+#pragma unroll
+        for (int v = 0; v < kWaves; ++v) {
+          mn = range[v][0] < mn ? range[v][0] : mn;
+          mx = range[v][1] > mx ? range[v][1] : mx;
+        }
         src.lkey = lkey;
+        select_and_write_staged(src, total, k, mn, mx, hist, &sh, bitems, &nbitems, irow, vrow,
+                                weights, p.scale);
+        weights_done = true;
+      } else {
+        select_and_write(src, total, k, hist, &sh, irow, vrow);
       }
-      select_and_write(src, total, k, hist, &sh, irow, vrow);
     } else {
       select_and_write(DenseSrc{dense + (int64_t)row * ld}, L, k, hist, &sh, irow, vrow);
     }
-    if (weights) kept_scores_to_weights(vrow, k, p.scale, ftmp);
+    if (weights && !weights_done) kept_scores_to_weights(vrow, k, p.scale, ftmp);
   }
   for (int i = k + tid; i < p.k_max; i += kBlock) {
     irow[i] = -1;
