@@ -696,29 +696,55 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
 // FUSED: the list holds exactly k_b valid positions and sigma their scores;
 // otherwise entries outside [0, L_b) are skipped and the logits recomputed
 // from the key rows.  The softmax weights exp(z - max) are formed once per
-// position in LDS; each wave then walks sixteen positions per step (four
-// per 16-lane group, loads issued together), 16 lanes x 16 bytes covering one
-// 256-byte bf16 value row.  A row split over several workgroups leaves
-// (max, sum, unnormalised output) partials that k_merge combines.
+// position in LDS.  Each wave then walks 4 * kGatherU positions per step
+// (kGatherU per 16-lane group, 16 lanes x 16 bytes covering one 256-byte
+// bf16 value row), with the next step's loads issued before the current
+// step is consumed.  A row split over several workgroups leaves (max, sum,
+// unnormalised output) partials that k_merge combines.
+// Dynamic LDS: voff[split] i64, koff[split] i64 (recompute only),
+// e[nh][split] f32, pos[split] i32, q[nh][128] f32 (recompute only),
+// red[kWaves][nhb][128] f32, lred[kWaves][nhb] f32, nhb = min(nh, kAttHeads).
 // ---------------------------------------------------------------------------
 constexpr int kAttHeads = 8;  // heads accumulated per pass over the value rows
-constexpr int kGatherUnroll = 8;
+
+template <bool BF16>
+struct RowRaw {
+  u32x4 v[BF16 ? 1 : 2];  // this lane's 8 channels of one value row
+};
+
+template <bool BF16>
+__device__ __forceinline__ void load_raw(const void *base, int64_t off, int col, RowRaw<BF16> &r) {
+  if constexpr (BF16) {
+    r.v[0] = *(const u32x4 *)((const uint16_t *)base + off + 8 * col);
+  } else {
+    const u32x4 *q = (const u32x4 *)((const float *)base + off + 8 * col);
+    r.v[0] = q[0];
+    r.v[1] = q[1];
+  }
+}
+
+template <bool BF16>
+__device__ __forceinline__ void unpack_raw(const RowRaw<BF16> &r, float v[8]) {
+  if constexpr (BF16) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[2 * e] = bf16_to_f32(r.v[0][e] & 0xFFFFu);
+      v[2 * e + 1] = bf16_to_f32(r.v[0][e] >> 16);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v[e] = __uint_as_float(r.v[0][e]);
+      v[4 + e] = __uint_as_float(r.v[1][e]);
+    }
+  }
+}
 
 template <bool BF16>
 __device__ __forceinline__ void load_row8(const void *base, int64_t off, int col, float v[8]) {
-  if constexpr (BF16) {
-    const u32x4 raw = *(const u32x4 *)((const uint16_t *)base + off + 8 * col);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      v[2 * e] = bf16_to_f32(raw[e] & 0xFFFFu);
-      v[2 * e + 1] = bf16_to_f32(raw[e] >> 16);
-    }
-  } else {
-    const float4 a = *(const float4 *)((const float *)base + off + 8 * col);
-    const float4 c = *(const float4 *)((const float *)base + off + 8 * col + 4);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = c.x; v[5] = c.y; v[6] = c.z; v[7] = c.w;
-  }
+  RowRaw<BF16> r;
+  load_raw<BF16>(base, off, col, r);
+  unpack_raw<BF16>(r, v);
 }
 
 template <bool BF16>
@@ -731,31 +757,57 @@ __device__ __forceinline__ int attend_list_len(const Params &p, int b, int L, bo
   return fused ? row_budget(p, b, L) : p.k_max;
 }
 
-template <bool BF16, bool FUSED>
+__host__ __device__ inline bool attend_recompute(bool fused, int group_shared) {
+  return !fused || group_shared;
+}
+
+// Byte offsets of the dynamic LDS areas of k_attend (host and device agree).
+struct AttLds {
+  int voff, koff, e, pos, q, red, lred, total;
+  __host__ __device__ AttLds(int split, int nh, bool recompute) {
+    const int nhb = nh < kAttHeads ? nh : kAttHeads;
+    int o = 0;
+    voff = o; o += 8 * split;
+    koff = o; o += recompute ? 8 * split : 0;
+    e = o; o += 4 * nh * split;
+    pos = o; o += 4 * split;
+    q = o; o += recompute ? 4 * nh * kHeadDim : 0;
+    red = o; o += 4 * kWaves * nhb * kHeadDim;
+    lred = o; o += 4 * kWaves * nhb;
+    total = o;
+  }
+};
+
+template <bool BF16, bool FUSED, bool GRP>
 __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32_t *idx, void *out,
                                                    int split) {
-  extern __shared__ int64_t att_dyn[];  // voff[split], koff[split], e[nh][split], pos[split]
-  __shared__ float q_l[kMaxGroup][kHeadDim];
-  __shared__ float red[kWaves][kAttHeads][kHeadDim];
-  __shared__ float lred[kWaves][kAttHeads];
+  extern __shared__ int64_t att_dyn[];
   __shared__ float mh[kMaxGroup];
   __shared__ float ftmp[kWaves];
+  constexpr int U = (BF16 && !GRP) ? 8 : 4;  // positions per 16-lane group per step
+  constexpr int HB = GRP ? kAttHeads : 1;  // heads accumulated per pass
 
   const int s = blockIdx.x, row = blockIdx.y;
   const int b = row / p.R, r = row % p.R;
-  const bool grp = p.group_shared;
+  constexpr bool grp = GRP;
   const int nh = grp ? p.G : 1;
+  const int nhb = nh < kAttHeads ? nh : kAttHeads;
   const int h0 = grp ? r * p.G : r;
   const int g = grp ? r : r / p.G;
   const int L = seq_len(p, b);
   const int n_list = attend_list_len(p, b, L, FUSED);
   const int nsp = (n_list + split - 1) / split;
   const int tid = threadIdx.x, l = lane_id(), col = l & 15, sub = l >> 4, wv = wave_id();
-  const bool recompute = !FUSED || grp;
-  int64_t *voff_l = att_dyn;                       // element offsets of the value rows
-  int64_t *koff_l = att_dyn + split;               // and of the key rows (recompute only)
-  float *e_l = (float *)(att_dyn + (recompute ? 2 : 1) * split);
-  int32_t *pos_l = (int32_t *)(e_l + nh * split);
+  const bool recompute = attend_recompute(FUSED, grp);
+  const AttLds lay(split, nh, recompute);
+  char *dyn = (char *)att_dyn;
+  int64_t *voff_l = (int64_t *)(dyn + lay.voff);
+  int64_t *koff_l = (int64_t *)(dyn + lay.koff);
+  float *e_l = (float *)(dyn + lay.e);
+  int32_t *pos_l = (int32_t *)(dyn + lay.pos);
+  float *q_l = (float *)(dyn + lay.q);        // [nh][128]
+  float *red = (float *)(dyn + lay.red);      // [kWaves][nhb][128]
+  float *lred = (float *)(dyn + lay.lred);    // [kWaves][nhb]
 
   if (n_list == 0 || L == 0) {  // nothing kept: zero output
     if (s == 0)
@@ -781,8 +833,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   if (recompute) {
     for (int e = tid; e < nh * kHeadDim; e += kBlock) {
       const int64_t qo = ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim;
-      q_l[e / kHeadDim][e % kHeadDim] =
-          BF16 ? bf16_to_f32(((const uint16_t *)p.q)[qo]) : ((const float *)p.q)[qo];
+      q_l[e] = BF16 ? bf16_to_f32(((const uint16_t *)p.q)[qo]) : ((const float *)p.q)[qo];
     }
   }
   __syncthreads();
@@ -807,7 +858,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
       for (int h = 0; h < nh; ++h) {
         float d = 0.f;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) d = fmaf(q_l[h][8 * col + e], kv[e], d);
+        for (int e = 0; e < 8; ++e) d = fmaf(q_l[h * kHeadDim + 8 * col + e], kv[e], d);
         d += __shfl_xor(d, 1);
         d += __shfl_xor(d, 2);
         d += __shfl_xor(d, 4);
@@ -834,43 +885,60 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     __syncthreads();
   }
 
-  for (int hb = 0; hb < nh; hb += kAttHeads) {
-    const int nb = (nh - hb) < kAttHeads ? (nh - hb) : kAttHeads;
-    float acc[kAttHeads][8];
-    float lsum[kAttHeads];
+  const int stride = kWaves * 4 * U;  // positions per workgroup step
+  for (int hb = 0; hb < nh; hb += HB) {
+    const int nb = (nh - hb) < HB ? (nh - hb) : HB;
+    float acc[HB][8];
+    float lsum[HB];
 #pragma unroll
-    for (int h = 0; h < kAttHeads; ++h) {
+    for (int h = 0; h < HB; ++h) {
       lsum[h] = 0.f;
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[h][c] = 0.f;
     }
-    // Branch-free gather: entries past the split or skipped (weight 0) read
-    // the sequence's position 0, so every step issues the same loads.
-    for (int t0 = wv * 4 * kGatherUnroll; t0 < n; t0 += kWaves * 4 * kGatherUnroll) {
-      float vv[kGatherUnroll][8];
-      int tt[kGatherUnroll];
+    // Branch-free gather: entries past the slice read entry 0's row (weight
+    // 0), so every step issues the same loads, and the next step's loads are
+    // in flight while this step's rows are accumulated.
+    auto issue = [&](int tb, RowRaw<BF16> buf[U]) {
 #pragma unroll
-      for (int u = 0; u < kGatherUnroll; ++u) {
-        const int t = t0 + 4 * u + sub;
-        tt[u] = t < n ? t : -1;
-        load_row8<BF16>(p.V.base, voff_l[t < n ? t : 0], col, vv[u]);
+      for (int u = 0; u < U; ++u) {
+        const int t = tb + 4 * u + sub;
+        load_raw<BF16>(p.V.base, voff_l[t < n ? t : 0], col, buf[u]);
       }
+    };
+    auto consume = [&](int tb, const RowRaw<BF16> buf[U]) {
 #pragma unroll
-      for (int u = 0; u < kGatherUnroll; ++u) {
+      for (int u = 0; u < U; ++u) {
+        const int t = tb + 4 * u + sub;
+        float vv[8];
+        unpack_raw<BF16>(buf[u], vv);
 #pragma unroll
-        for (int h = 0; h < kAttHeads; ++h) {
+        for (int h = 0; h < HB; ++h) {
           if (h < nb) {
-            const float e = tt[u] >= 0 ? e_l[(hb + h) * split + tt[u]] : 0.f;
+            const float e = t < n ? e_l[(hb + h) * split + t] : 0.f;
             lsum[h] += e;
 #pragma unroll
-            for (int c = 0; c < 8; ++c) acc[h][c] = fmaf(e, vv[u][c], acc[h][c]);
+            for (int c = 0; c < 8; ++c) acc[h][c] = fmaf(e, vv[c], acc[h][c]);
           }
         }
+      }
+    };
+    RowRaw<BF16> b0[U], b1[U];
+    int t0 = wv * 4 * U;
+    if (t0 < n) {  // wave-uniform
+      issue(t0, b0);
+      for (;; t0 += 2 * stride) {
+        issue(t0 + stride, b1);
+        consume(t0, b0);
+        if (t0 + stride >= n) break;
+        issue(t0 + 2 * stride, b0);
+        consume(t0 + stride, b1);
+        if (t0 + 2 * stride >= n) break;
       }
     }
     // Reduce over the four position groups of a wave, then over waves.
 #pragma unroll
-    for (int h = 0; h < kAttHeads; ++h) {
+    for (int h = 0; h < HB; ++h) {
       if (h < nb) {
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
@@ -884,8 +952,8 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
         ls += __shfl_xor(ls, 32);
         if (sub == 0) {
 #pragma unroll
-          for (int c = 0; c < 8; ++c) red[wv][h][8 * col + c] = acc[h][c];
-          if (col == 0) lred[wv][h] = ls;
+          for (int c = 0; c < 8; ++c) red[(wv * nhb + h) * kHeadDim + 8 * col + c] = acc[h][c];
+          if (col == 0) lred[wv * nhb + h] = ls;
         }
       }
     }
@@ -895,8 +963,8 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
       float o = 0.f, ls = 0.f;
 #pragma unroll
       for (int v = 0; v < kWaves; ++v) {
-        o += red[v][h][c];
-        ls += lred[v][h];
+        o += red[(v * nhb + h) * kHeadDim + c];
+        ls += lred[v * nhb + h];
       }
       const int hq = h0 + hb + h;
       if (nsp == 1) {
@@ -986,48 +1054,66 @@ hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream
   return hipGetLastError();
 }
 
-// Dynamic LDS per list entry of k_attend: value (and key) row offsets,
-// one weight per head served, and the position.
-static int64_t attend_bytes_per_entry(const Params &p) {
-  const int nh = p.group_shared ? p.G : 1;
-  return 8 + 8 + 4 * nh + 4;
-}
+constexpr int kAttendWorkgroups = 1024;   // enough to fill the chip
+constexpr int kAttendLdsMax = 60 * 1024;  // dynamic LDS of one attend workgroup
 
-int attend_split(const Params &p, int nsplit_max_positions) {
-  // Positions per attend workgroup: enough workgroups to fill the chip
-  // (about 2048), at least 64 positions each, LDS-bounded in group mode.
+// Positions per attend workgroup: about kAttendWorkgroups workgroups over
+// all rows, at least 64 positions each, within the LDS budget.
+int attend_split(const Params &p, int k_max_positions, bool fused) {
   const int64_t rows = (int64_t)p.B * p.R;
-  const int64_t k_max = nsplit_max_positions > 0 ? nsplit_max_positions : 1;
-  int64_t nsplit = (2048 + rows - 1) / rows;
+  const int64_t k_max = k_max_positions > 0 ? k_max_positions : 1;
+  const int nh = p.group_shared ? p.G : 1;
+  const bool rc = attend_recompute(fused, p.group_shared);
+  int64_t nsplit = (kAttendWorkgroups + rows - 1) / rows;
   const int64_t most = (k_max + 63) / 64;
   if (nsplit > most) nsplit = most;
   if (nsplit < 1) nsplit = 1;
   int64_t split = (k_max + nsplit - 1) / nsplit;
   split = (split + 63) / 64 * 64;
-  const int64_t lds_limit = (48 * 1024) / attend_bytes_per_entry(p) / 64 * 64;
-  if (split > lds_limit) split = lds_limit;
+  while (split > 64 && AttLds((int)split, nh, rc).total > kAttendLdsMax) split -= 64;
   return (int)split;
 }
 
 int attend_nsplit(const Params &p) {
-  const int split = attend_split(p, p.k_max);
-  const int64_t k_max = p.k_max > 0 ? p.k_max : 1;
-  return (int)((k_max + split - 1) / split);
+  // The larger of the fused and unfused split counts (the unfused layout
+  // needs more LDS per entry, hence smaller splits).
+  int most = 1;
+  for (int fused = 0; fused < 2; ++fused) {
+    const int split = attend_split(p, p.k_max, fused != 0);
+    const int64_t k_max = p.k_max > 0 ? p.k_max : 1;
+    const int ns = (int)((k_max + split - 1) / split);
+    most = ns > most ? ns : most;
+  }
+  return most;
 }
 
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st) {
-  const int split = attend_split(p, p.k_max);
-  const size_t lds = (size_t)attend_bytes_per_entry(p) * split;
-  const dim3 grid(w.nsplit, p.B * p.R);
+  const int split = attend_split(p, p.k_max, fused);
+  const size_t lds = (size_t)AttLds(split, p.group_shared ? p.G : 1,
+                                    attend_recompute(fused, p.group_shared)).total;
+  const int64_t kk = p.k_max > 0 ? p.k_max : 1;
+  const int nsplit = (int)((kk + split - 1) / split);
+  const dim3 grid(nsplit, p.B * p.R);
+  const bool g = p.group_shared != 0;
   if (p.bf16) {
-    if (fused) k_attend<true, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
-    else k_attend<true, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    if (fused) {
+      if (g) k_attend<true, true, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+      else k_attend<true, true, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    } else {
+      if (g) k_attend<true, false, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+      else k_attend<true, false, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    }
   } else {
-    if (fused) k_attend<false, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
-    else k_attend<false, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    if (fused) {
+      if (g) k_attend<false, true, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+      else k_attend<false, true, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    } else {
+      if (g) k_attend<false, false, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+      else k_attend<false, false, false><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    }
   }
-  if (w.nsplit > 1) {
+  if (nsplit > 1) {
     const unsigned rows = (unsigned)(p.B * p.Hq);
     if (p.bf16) {
       if (fused) k_merge<true, true><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
