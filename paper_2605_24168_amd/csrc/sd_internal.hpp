@@ -21,7 +21,8 @@ constexpr int kChunkCap = kWaves * kCandBuf;  // entries of one workgroup's pack
 constexpr int kDenseChunk = 8192;  // keys per workgroup of the full-score kernels
 constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
-constexpr int kRepairParts = 16;   // workgroups per (sequence, KV head) in the repair stream
+constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the fallback scoring
+constexpr int kRepairGrid = 512;   // workgroups of each fallback kernel
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));

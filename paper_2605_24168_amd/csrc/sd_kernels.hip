@@ -4,24 +4,24 @@
 // sparsity under GQA).
 //
 // Fused pipeline for one decode step, all on the caller's stream:
-//   k_pilot_score   scores a strided sample of <= 4096 keys per row
+//   k_pilot_score   scores a strided sample of <= 2048 keys per row
 //   k_pilot_select  picks a per-row threshold from the sample (aimed at about
-//                   2.5 k candidates) and clears the per-row state
+//                   2.5 k candidates) and flags rows for the fallback
 //   k_score_stream  streams every key once (MFMA scoring, one K tile shared
-//                   by all query heads of the group) and appends the keys at
-//                   or above the threshold to per-wave candidate lists, in
-//                   position order, with ballots instead of atomics
+//                   by all query heads of the group), stages the keys at or
+//                   above the threshold in LDS in position order (ballots,
+//                   no atomics) and writes one packed block per workgroup
 //   k_select        exact top-k over the candidates; a row whose candidates
 //                   cannot prove exactness is flagged for the fallback
-//   k_score_dense   (fallback) full scores of the flagged rows' groups
-//   k_select        (fallback) exact top-k over those full scores
+//   k_repair_score  (fallback) full scores of the flagged rows' groups
+//   k_repair_select (fallback) exact top-k over those full scores
 //   k_attend        gathers the kept value rows, split over workgroups
 //   k_merge         combines the splits' (max, sum, output) partials by
-//                   log-sum-exp
+//                   log-sum-exp (only when a row is split)
 // The threshold is only a filter: the selection is exact whenever every
 // kept position passed it, which holds iff at least k candidates passed
 // (then the k-th largest candidate is >= the threshold, so nothing above
-// the true k-th largest score was filtered out) and no candidate list
+// the true k-th largest score was filtered out) and no staging area
 // overflowed.  Otherwise the row takes the exact fallback.
 #include "sd_internal.hpp"
 #include "sd_launch.hpp"
@@ -94,6 +94,128 @@ __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// k-th largest of n order-preserving keys staged in LDS, kmin..kmax their
+// range (1 <= k <= n).  One histogram over kBuckets value buckets,
+// bucket(v) = min(kBuckets-1, floor((v - vmin) * kBuckets / (vmax - vmin))),
+// which is monotone in v (rounded subtraction and scaling by a positive
+// constant preserve order), so a higher bucket holds only larger values;
+// inside the bucket holding the k-th largest, an exact rank count over its
+// items gives T (the k-th largest key) and need_eq (how many items equal to
+// T belong to the top k).  Returns false, with T and need_eq unset, when the
+// range is not finite or that bucket holds more than kBucketItems items.
+// Every thread of the block must call it.
+// ---------------------------------------------------------------------------
+constexpr int kBuckets = 2048;
+constexpr int kBucketItems = kBlock;
+
+struct BucketShared {
+  uint32_t items[kBucketItems];
+  int n;
+};
+
+__device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, uint32_t kmax,
+                           uint32_t *hist, SelShared *sh, BucketShared *bs, uint32_t &T,
+                           int &need_eq) {
+  if (kmin == kmax) {  // all equal: the first k
+    T = kmin;
+    need_eq = k;
+    return true;
+  }
+  const int tid = threadIdx.x;
+  const float vmin = key2f(kmin), vmax = key2f(kmax);
+  const float inv = (float)kBuckets / (vmax - vmin);
+  if (!(__builtin_isfinite(vmin) && __builtin_isfinite(inv) && inv > 0.f)) return false;
+  auto bucket = [&](uint32_t key) {
+    const int bk = (int)((key2f(key) - vmin) * inv);
+    return bk < kBuckets - 1 ? bk : kBuckets - 1;
+  };
+  for (int i = tid; i < kBuckets; i += kBlock) hist[i] = 0;
+  __syncthreads();
+  for (int base = 0; base < n; base += kBlock) {
+    const int i = base + tid;
+    const uint32_t key = i < n ? keys[i] : kmin;
+    hist_add(hist, (uint32_t)bucket(key), i < n);
+  }
+  __syncthreads();
+  // Thread t owns buckets [nb - (t+1)*bpt, nb - t*bpt), counted from the top.
+  constexpr int bpt = kBuckets / kBlock;
+  const int hi = kBuckets - tid * bpt;
+  int mine = 0;
+  for (int j = 1; j <= bpt; ++j) mine += (int)hist[hi - j];
+  int tot;
+  const int before = block_excl_scan(mine, sh->scan, &tot);
+  if (tid == 0) bs->n = 0;
+  if (before < k && k <= before + mine) {
+    int cum = before;
+    for (int j = 1; j <= bpt; ++j) {
+      const int c = (int)hist[hi - j];
+      if (cum + c >= k) {
+        sh->digit = (uint32_t)(hi - j);
+        sh->above = cum;
+        break;
+      }
+      cum += c;
+    }
+  }
+  __syncthreads();
+  const int bstar = (int)sh->digit;
+  const int krem = k - sh->above;
+  const int m = (int)hist[bstar];
+  bool found = false;
+  if (m <= kBucketItems) {  // uniform
+    for (int base = 0; base < n; base += kBlock) {
+      const int i = base + tid;
+      if (i < n) {
+        const uint32_t key = keys[i];
+        if (bucket(key) == bstar) bs->items[atomicAdd(&bs->n, 1)] = key;
+      }
+    }
+    __syncthreads();
+    if (tid < m) {
+      const uint32_t x = bs->items[tid];
+      int gt = 0, ge = 0;
+      for (int y = 0; y < m; ++y) {
+        const uint32_t v = bs->items[y];
+        gt += v > x ? 1 : 0;
+        ge += v >= x ? 1 : 0;
+      }
+      if (gt < krem && krem <= ge) {  // x is the krem-th largest (equal items agree)
+        sh->digit = x;
+        sh->above = gt;
+      }
+    }
+    __syncthreads();
+    T = sh->digit;
+    need_eq = krem - sh->above;
+    found = true;
+  }
+  __syncthreads();  // sh and hist are reused by the caller
+  return found;
+}
+
+// Block-wide (min, max) of per-thread key ranges; tmp: LDS uint32[kWaves][2].
+// Ends with a barrier (so LDS written before the call is visible after it).
+__device__ __forceinline__ void block_key_range(uint32_t &mn, uint32_t &mx, uint32_t (*tmp)[2]) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t a = __shfl_xor(mn, o), c = __shfl_xor(mx, o);
+    mn = a < mn ? a : mn;
+    mx = c > mx ? c : mx;
+  }
+  if (lane_id() == 0) {
+    tmp[wave_id()][0] = mn;
+    tmp[wave_id()][1] = mx;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < kWaves; ++v) {
+    mn = tmp[v][0] < mn ? tmp[v][0] : mn;
+    mx = tmp[v][1] > mx ? tmp[v][1] : mx;
+  }
+  __syncthreads();
+}
+
 struct LdsKeys {
   const uint32_t *keys;
   __device__ __forceinline__ uint32_t key(int i) const { return keys[i]; }
@@ -110,6 +232,8 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[2048];
   __shared__ SelShared sh;
+  __shared__ BucketShared bs;
+  __shared__ uint32_t range[kWaves][2];
   const int row = blockIdx.x, b = row / p.R;
   const int L = seq_len(p, b);
   const int k = row_budget(p, b, L);
@@ -132,13 +256,20 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
     return;
   }
   if (threadIdx.x == 0) w.flags[row] = 0;
-  for (int i = threadIdx.x; i < m; i += kBlock) keys[i] = f2key(w.sample[(int64_t)row * kSampleMax + i]);
-  __syncthreads();
+  uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+  for (int i = threadIdx.x; i < m; i += kBlock) {
+    const uint32_t key = f2key(w.sample[(int64_t)row * kSampleMax + i]);
+    keys[i] = key;
+    mn = key < mn ? key : mn;
+    mx = key > mx ? key : mx;
+  }
+  block_key_range(mn, mx, range);  // also publishes keys
   uint32_t T;
   int need_eq;
-  // Two histogram passes fix the top 22 key bits of the r-th largest sample;
-  // the threshold is the lowest key with those bits (at or below it).
-  radix_select(LdsKeys{keys}, m, r, hist, &sh, T, need_eq, 2);
+  // The r-th largest sample exactly; else (rare) two radix passes fix its
+  // top 22 key bits and the threshold is the lowest key with those bits.
+  if (!bucket_kth(keys, m, r, mn, mx, hist, &sh, &bs, T, need_eq))
+    radix_select(LdsKeys{keys}, m, r, hist, &sh, T, need_eq, 2);
   if (threadIdx.x == 0) w.theta[row] = key2f(T);
 }
 
@@ -340,29 +471,22 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
 }
 
 // ---------------------------------------------------------------------------
-// Full scores.  grid = (parts, B*Hkv).  dst[row][j] for j < L_b; with
-// FILL_TAIL, -inf for L_b <= j < ncap.  With ONLY_FLAGGED the workgroup does
-// nothing unless a row of its group is flagged (the exact fallback).
+// Full scores of one (sequence b, KV head g): part `part` of `parts` takes
+// tiles part*4 + wave, stepping by parts*4.  dst[row][j] for j < L_b; with
+// fill_tail, -inf for L_b <= j < ncap.  Every thread of the block must call
+// it (the f32 scorer stages the queries in LDS behind a barrier).
 // ---------------------------------------------------------------------------
-template <bool BF16, bool ONLY_FLAGGED, bool FILL_TAIL>
-__global__ __launch_bounds__(kBlock) void k_score_dense(Params p, Work w, float *dst, int64_t ld) {
-  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
-  const int bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
+template <bool BF16>
+__device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_t ld, int b, int g,
+                                             int part, int parts, bool fill_tail, float *q_lds) {
   const int L = seq_len(p, b);
   const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
-  const int nrows = p.group_shared ? 1 : p.G;
-  if constexpr (ONLY_FLAGGED) {
-    int any = 0;
-    for (int r = 0; r < nrows; ++r) any |= w.flags[row0 + r];
-    if (!any) return;  // uniform over the workgroup
-  }
   Scorer<BF16> sc;
   scorer_init<BF16>(p, b, g, sc, q_lds);
-  const int64_t end = FILL_TAIL ? p.ncap : (int64_t)L;
+  const int64_t end = fill_tail ? p.ncap : (int64_t)L;
   const int64_t ntiles = (end + kTile - 1) / kTile;
   const int l = lane_id(), col = l & 15, s = l >> 4;
-  for (int64_t t = (int64_t)blockIdx.x * kWaves + wave_id(); t < ntiles;
-       t += (int64_t)gridDim.x * kWaves) {
+  for (int64_t t = (int64_t)part * kWaves + wave_id(); t < ntiles; t += (int64_t)parts * kWaves) {
     const int64_t j = t * kTile + col;
     const bool in_seq = j < L;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -381,12 +505,43 @@ __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, Work w, float 
   }
 }
 
+// sparse_decode_score: grid = (parts, B*Hkv).
+template <bool BF16>
+__global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, int64_t ld) {
+  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
+  const int bg = blockIdx.y;
+  dense_scores<BF16>(p, dst, ld, bg / p.Hkv, bg % p.Hkv, blockIdx.x, gridDim.x, true, q_lds);
+}
+
+// Exact fallback, scoring: a small grid walks the (group, part) items and
+// scores the groups holding a flagged row into w.dense.  stats[0] counts the
+// flagged rows (the selection adds every flagged row before this runs), so
+// a call with none costs one read per workgroup.
+template <bool BF16>
+__global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
+  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
+  if (__hip_atomic_load(&w.stats[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
+    return;  // no row was flagged
+  const int nrows = p.group_shared ? 1 : p.G;
+  const int64_t items = (int64_t)p.B * p.Hkv * kRepairParts;
+  for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+    const int bg = (int)(it / kRepairParts), part = (int)(it % kRepairParts);
+    const int b = bg / p.Hkv, g = bg % p.Hkv;
+    const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
+    int any = 0;
+    for (int r = 0; r < nrows; ++r) any |= w.flags[row0 + r];
+    if (!any) continue;  // uniform over the workgroup
+    dense_scores<BF16>(p, w.dense, p.ncap, b, g, part, kRepairParts, false, q_lds);
+    if (!BF16) __syncthreads();  // q_lds is rewritten for the next item
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Exact top-k of one row per workgroup.
 //   MODE 0: over the row's candidate lists (fused path); flags the row when
 //           the candidates do not prove exactness.
 //   MODE 1: over a full score row (sparse_decode_topk).
-//   MODE 2: over a full fallback score row, flagged rows only.
+// (k_repair_select below does the flagged rows of the fallback.)
 // Output: idx[row][0..k) ascending positions, then -1; vals[row][...] the
 // kept scores (or -inf), when vals is not null.
 // ---------------------------------------------------------------------------
@@ -443,101 +598,23 @@ __device__ __forceinline__ void select_and_write(const Src &src, int n, int k, u
 }
 
 // Candidates whose keys are staged in LDS (src.lkey), kmin..kmax their key
-// range.  The k-th largest key is found with one histogram over 2048 value
-// buckets, bucket(v) = min(2047, floor((v - vmin) * 2048 / (vmax - vmin))),
-// which is monotone in v (rounded subtraction and scaling by a positive
-// constant preserve order), so a higher bucket holds only larger scores;
-// inside the bucket that holds the k-th largest, an exact rank count over
-// its few items gives the key T and the number need_eq of items equal to T
-// that are kept.  (Radix passes over the key bits are the fallback: equal
-// extremes, non-finite ranges, or a crowded bucket.)  The compaction then
-// records each kept item's index in place of the consumed keys (slot <= item
-// index, and a round reads all its keys before its scans) and writes the
-// softmax weights exp(scale * (s - vmax)) (or, group-shared mode, the kept
-// scores), and every thread fetches the positions of its kept items with
-// the loads in flight together.
-constexpr int kBuckets = 2048;
-constexpr int kBucketItems = kBlock;  // items of the k-th bucket ranked exactly
-
+// range: the k-th largest by bucket_kth (radix passes over the key bits
+// when it declines).  The compaction then records each kept item's index in
+// place of the consumed keys (slot <= item index, and a round reads all its
+// keys before its scans) and writes the softmax weights exp(scale * (s -
+// vmax)) (or, group-shared mode, the kept scores); finally every thread
+// fetches the positions of its kept items with the loads in flight together.
 __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, int n, int k,
                                                         uint32_t kmin, uint32_t kmax,
                                                         uint32_t *hist, SelShared *sh,
-                                                        uint32_t *bitems, int *nbitems,
-                                                        int32_t *irow, float *vrow,
-                                                        bool weights, float scale) {
+                                                        BucketShared *bs, int32_t *irow,
+                                                        float *vrow, bool weights, float scale) {
   const int tid = threadIdx.x;
-  const float vmin = key2f(kmin), vmax = key2f(kmax);
-  const float inv = (float)kBuckets / (vmax - vmin);
-  uint32_t T = kmin;
-  int need_eq = k;
-  bool found = kmin == kmax;  // all candidates equal: the first k are kept
-  if (!found && __builtin_isfinite(vmin) && __builtin_isfinite(inv) && inv > 0.f) {
-    auto bucket = [&](uint32_t key) {
-      const int bk = (int)((key2f(key) - vmin) * inv);
-      return bk < kBuckets - 1 ? bk : kBuckets - 1;
-    };
-    for (int i = tid; i < kBuckets; i += kBlock) hist[i] = 0;
-    __syncthreads();
-    for (int base = 0; base < n; base += kBlock) {
-      const int i = base + tid;
-      const uint32_t key = i < n ? src.lkey[i] : kmin;
-      hist_add(hist, (uint32_t)bucket(key), i < n);
-    }
-    __syncthreads();
-    // Thread t owns buckets [nb - (t+1)*bpt, nb - t*bpt), counted from the top.
-    constexpr int bpt = kBuckets / kBlock;
-    const int hi = kBuckets - tid * bpt;
-    int mine = 0;
-    for (int j = 1; j <= bpt; ++j) mine += (int)hist[hi - j];
-    int tot;
-    const int before = block_excl_scan(mine, sh->scan, &tot);
-    if (tid == 0) *nbitems = 0;
-    if (before < k && k <= before + mine) {
-      int cum = before;
-      for (int j = 1; j <= bpt; ++j) {
-        const int c = (int)hist[hi - j];
-        if (cum + c >= k) {
-          sh->digit = (uint32_t)(hi - j);
-          sh->above = cum;
-          break;
-        }
-        cum += c;
-      }
-    }
-    __syncthreads();
-    const int bstar = (int)sh->digit;
-    const int krem = k - sh->above;
-    const int m = (int)hist[bstar];
-    if (m <= kBucketItems) {  // uniform
-      for (int base = 0; base < n; base += kBlock) {
-        const int i = base + tid;
-        if (i < n) {
-          const uint32_t key = src.lkey[i];
-          if (bucket(key) == bstar) bitems[atomicAdd(nbitems, 1)] = key;
-        }
-      }
-      __syncthreads();
-      if (tid < m) {
-        const uint32_t x = bitems[tid];
-        int gt = 0, ge = 0;
-        for (int y = 0; y < m; ++y) {
-          const uint32_t v = bitems[y];
-          gt += v > x ? 1 : 0;
-          ge += v >= x ? 1 : 0;
-        }
-        if (gt < krem && krem <= ge) {  // x is the krem-th largest (equal items agree)
-          sh->digit = x;
-          sh->above = gt;
-        }
-      }
-      __syncthreads();
-      T = sh->digit;
-      need_eq = krem - sh->above;
-      found = true;
-    }
-    __syncthreads();  // sh is reused below
-  }
-  if (!found) radix_select(src, n, k, hist, sh, T, need_eq);
+  const float vmax = key2f(kmax);
+  uint32_t T;
+  int need_eq;
+  if (!bucket_kth(src.lkey, n, k, kmin, kmax, hist, sh, bs, T, need_eq))
+    radix_select(src, n, k, hist, sh, T, need_eq);
   uint32_t *stage = const_cast<uint32_t *>(src.lkey);
   compact_selected(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
     stage[slot] = (uint32_t)i;
@@ -582,11 +659,9 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   __shared__ int status;
   __shared__ float ftmp[kWaves];
   __shared__ uint32_t range[kWaves][2];
-  __shared__ uint32_t bitems[kBucketItems];
-  __shared__ int nbitems;
+  __shared__ BucketShared bs;
   bool weights_done = false;
   const int row = blockIdx.x, b = row / p.R;
-  if (MODE == 2 && w.flags[row] == 0) return;
   const bool weights = MODE != 1 && !p.group_shared;
   const int L = seq_len(p, b);
   const int k = row_budget(p, b, L);
@@ -654,26 +729,10 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
             }
           }
         }
-        // Block-wide key range (the sync also publishes lkey).
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const uint32_t a = __shfl_xor(mn, o), c = __shfl_xor(mx, o);
-          mn = a < mn ? a : mn;
-          mx = c > mx ? c : mx;
-        }
-        if (lane_id() == 0) {
-          range[wave_id()][0] = mn;
-          range[wave_id()][1] = mx;
-        }
-        __syncthreads();
-#pragma unroll
-        for (int v = 0; v < kWaves; ++v) {
-          mn = range[v][0] < mn ? range[v][0] : mn;
-          mx = range[v][1] > mx ? range[v][1] : mx;
-        }
+        block_key_range(mn, mx, range);  // also publishes lkey
         src.lkey = lkey;
-        select_and_write_staged(src, total, k, mn, mx, hist, &sh, bitems, &nbitems, irow, vrow,
-                                weights, p.scale);
+        select_and_write_staged(src, total, k, mn, mx, hist, &sh, &bs, irow, vrow, weights,
+                                p.scale);
         weights_done = true;
       } else {
         select_and_write(src, total, k, hist, &sh, irow, vrow);
@@ -686,6 +745,35 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   for (int i = k + tid; i < p.k_max; i += kBlock) {
     irow[i] = -1;
     if (vrow) vrow[i] = -__builtin_inff();
+  }
+}
+
+// Exact fallback, selection: a small grid walks the rows; each flagged row
+// is selected from its full scores in w.dense and gets its softmax weights
+// (per-head mode) or kept scores (group-shared mode) in w.sigma.
+__global__ __launch_bounds__(kBlock) void k_repair_select(Params p, Work w, int32_t *idx) {
+  __shared__ uint32_t hist[2048];
+  __shared__ SelShared sh;
+  __shared__ float ftmp[kWaves];
+  if (__hip_atomic_load(&w.stats[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
+    return;  // no row was flagged
+  const int rows = p.B * p.R;
+  for (int row = blockIdx.x; row < rows; row += gridDim.x) {
+    if (w.flags[row] == 0) continue;  // uniform over the workgroup
+    const int b = row / p.R;
+    const int L = seq_len(p, b);
+    const int k = row_budget(p, b, L);
+    int32_t *irow = idx + (int64_t)row * p.k_max;
+    float *vrow = w.sigma + (int64_t)row * p.k_max;
+    if (k > 0) {
+      select_and_write(DenseSrc{w.dense + (int64_t)row * p.ncap}, L, k, hist, &sh, irow, vrow);
+      if (!p.group_shared) kept_scores_to_weights(vrow, k, p.scale, ftmp);
+    }
+    for (int i = k + threadIdx.x; i < p.k_max; i += kBlock) {
+      irow[i] = -1;
+      vrow[i] = -__builtin_inff();
+    }
+    __syncthreads();  // LDS is reused by the next row
   }
 }
 
@@ -1015,7 +1103,8 @@ static inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1
 
 hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
   if (!w.force_repair) {
-    const dim3 g1(8, p.B * p.Hkv);
+    // Four 16-key sample tiles per wave.
+    const dim3 g1(kSampleMax / (4 * kTile * kWaves), p.B * p.Hkv);
     k_pilot_score<true><<<g1, kBlock, 0, st>>>(p, w);
   }
   k_pilot_select<<<p.B * p.R, kBlock, 0, st>>>(p, w);
@@ -1047,10 +1136,9 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
 }
 
 hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream_t st) {
-  const dim3 grid(kRepairParts, p.B * p.Hkv);
-  if (p.bf16) k_score_dense<true, true, false><<<grid, kBlock, 0, st>>>(p, w, w.dense, p.ncap);
-  else k_score_dense<false, true, false><<<grid, kBlock, 0, st>>>(p, w, w.dense, p.ncap);
-  k_select<2><<<p.B * p.R, kBlock, 0, st>>>(p, w, w.dense, p.ncap, idx, w.sigma, 0);
+  if (p.bf16) k_repair_score<true><<<kRepairGrid, kBlock, 0, st>>>(p, w);
+  else k_repair_score<false><<<kRepairGrid, kBlock, 0, st>>>(p, w);
+  k_repair_select<<<kRepairGrid, kBlock, 0, st>>>(p, w, idx);
   return hipGetLastError();
 }
 
@@ -1128,9 +1216,8 @@ hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, voi
 
 hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st) {
   const dim3 grid(cdiv(p.ncap, kDenseChunk), p.B * p.Hkv);
-  Work none{};
-  if (p.bf16) k_score_dense<true, false, true><<<grid, kBlock, 0, st>>>(p, none, scores, p.ncap);
-  else k_score_dense<false, false, true><<<grid, kBlock, 0, st>>>(p, none, scores, p.ncap);
+  if (p.bf16) k_score_dense<true><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  else k_score_dense<false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
   return hipGetLastError();
 }
 
