@@ -429,6 +429,8 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   const hipStream_t stream_h = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_mu);
   const Layout L = layout_for(s, k_max, true, sp);
+  // One scoring workgroup per (chunk, sequence, KV head) on a 1-D grid.
+  if ((int64_t)L.nchunk * s.B * s.Hkv > INT32_MAX) return SD_ERR_UNSUPPORTED;
   DevState *ds = nullptr;
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);

@@ -274,8 +274,9 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
 }
 
 // ---------------------------------------------------------------------------
-// The scoring stream.  grid = (nchunk, B*Hkv); a chunk is kWaves * wk keys
-// (wk = w.wave_keys).  Wave v of workgroup c streams keys
+// The scoring stream.  grid = nchunk * B * Hkv workgroups, one per (chunk,
+// sequence, KV head); a chunk is kWaves * wk keys (wk = w.wave_keys).  Wave
+// v of the workgroup of chunk c streams keys
 // [c*4wk + v*wk, +wk) of one (sequence, KV head) in 16-key MFMA tiles,
 // kDepth tiles in flight, and stages the keys at or above each row's
 // threshold in LDS, in position order, one area of kCandBuf / rows entries
@@ -306,7 +307,21 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   __shared__ int seg_n[kWaves * kMaxGroup];        // [row][wave] candidates found
   __shared__ int seg_off[kWaves * kMaxGroup + 1];  // their offsets in the block
   const int wk = w.wave_keys;
-  const int chunk = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
+  // Dispatch order (consecutive workgroups run together): in the paged
+  // layout the KV heads of a page block are adjacent in memory, so heads go
+  // fastest; in the contiguous layout a head's slab is swept chunk by chunk.
+  const int wid = (int)blockIdx.x;
+  int chunk, g, b;
+  if (PAGED) {
+    g = wid % p.Hkv;
+    chunk = (wid / p.Hkv) % w.nchunk;
+    b = wid / (p.Hkv * w.nchunk);
+  } else {
+    chunk = wid % w.nchunk;
+    g = (wid / w.nchunk) % p.Hkv;
+    b = wid / (w.nchunk * p.Hkv);
+  }
+  const int bg = b * p.Hkv + g;
   const int L = seq_len(p, b);
   const int64_t c0 = (int64_t)chunk * kWaves * wk;
   if (c0 >= L) return;  // whole workgroup
@@ -1113,7 +1128,7 @@ hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
 
 hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st) {
   if (w.force_repair) return hipSuccess;  // every row takes the fallback
-  const dim3 grid(w.nchunk, p.B * p.Hkv);
+  const dim3 grid((unsigned)((int64_t)w.nchunk * p.B * p.Hkv));
   if (p.K.paged) {
     if (p.group_shared) k_score_stream<true, true><<<grid, kBlock, 0, st>>>(p, w);
     else k_score_stream<true, false><<<grid, kBlock, 0, st>>>(p, w);
