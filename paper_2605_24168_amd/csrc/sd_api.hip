@@ -462,9 +462,9 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   if (e == hipSuccess) e = mark(1);
   if (e == hipSuccess && s.ncap > 0) e = sd::launch_score_stream(p, w, stream_h);
   if (e == hipSuccess) e = mark(2);
-  if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, stream_h);
+  if (e == hipSuccess && s.ncap > 0) e = sd::launch_repair(p, w, stream_h);
   if (e == hipSuccess) e = mark(3);
-  if (e == hipSuccess && s.ncap > 0) e = sd::launch_repair(p, w, idx_ptr, stream_h);
+  if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, stream_h);
   if (e == hipSuccess) e = mark(4);
   if (e == hipSuccess) e = sd::launch_attend(p, w, idx_ptr, out->data, true, stream_h);
   if (e == hipSuccess) e = mark(5);
@@ -507,8 +507,8 @@ sd_status summarize(sd_profile *out, int32_t *n_out, bool mean) {
   }
   out->pilot_ms = (float)(acc[0] / n);
   out->score_ms = (float)(acc[1] / n);
-  out->select_ms = (float)(acc[2] / n);
-  out->repair_ms = (float)(acc[3] / n);
+  out->repair_ms = (float)(acc[2] / n);  // stages run: pilot, score, repair, select, attend
+  out->select_ms = (float)(acc[3] / n);
   out->attend_ms = (float)(acc[4] / n);
   out->total_ms = (float)(acc[5] / n);
   int32_t repaired = 0;

@@ -11,10 +11,10 @@
 //                   by all query heads of the group), stages the keys at or
 //                   above the threshold in LDS in position order (ballots,
 //                   no atomics) and writes one packed block per workgroup
-//   k_select        exact top-k over the candidates; a row whose candidates
-//                   cannot prove exactness is flagged for the fallback
-//   k_repair_score  (fallback) full scores of the flagged rows' groups
-//   k_repair_select (fallback) exact top-k over those full scores
+//   k_repair_score  flags the rows whose candidates cannot prove exactness
+//                   and scores their groups in full (the exact fallback)
+//   k_select        exact top-k: over the candidates, or over the full
+//                   scores for a flagged row
 //   k_attend        gathers the kept value rows, split over workgroups
 //   k_merge         combines the splits' (max, sum, output) partials by
 //                   log-sum-exp (only when a row is split)
@@ -61,25 +61,40 @@ __device__ __forceinline__ void scorer_init(const Params &p, int b, int g, Score
 }
 
 // ---------------------------------------------------------------------------
-// Pilot: scores of a strided sample of each sequence.
-// grid = (parts, B*Hkv).  Sample i of a sequence of length L is position
-// floor(i*L/m), m = min(L, kSampleMax), so m = L samples every position.
+// Pilot: scores of a strided sample of each sequence (bfloat16 caches).
+// grid = (kSampleMax / (kPilotTiles * kTile * kWaves), B*Hkv).  Sample i of a
+// sequence of length L is position floor(i*L/m), m = min(L, kSampleMax), so
+// m = L samples every position.  Each wave scores up to kPilotTiles sample
+// tiles, all of their (scattered) key loads issued before the matrix ops.
 // ---------------------------------------------------------------------------
-template <bool BF16>
+constexpr int kPilotTiles = 4;
+
 __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
-  __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
   const int bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
   const int L = seq_len(p, b);
-  Scorer<BF16> sc;
-  scorer_init<BF16>(p, b, g, sc, q_lds);
   const int m = L < kSampleMax ? L : kSampleMax;
   const int ntiles = (m + kTile - 1) / kTile;
   const int l = lane_id(), col = l & 15, s = l >> 4;
-  for (int t = blockIdx.x * kWaves + wave_id(); t < ntiles; t += gridDim.x * kWaves) {
+  const int t0 = blockIdx.x * kWaves + wave_id();
+  const int stride = gridDim.x * kWaves;
+  if (t0 >= ntiles) return;  // wave-uniform; no barriers in this kernel
+  QFrag qf;
+  load_q_bf16(p, b, g, qf);
+  KFrag kf[kPilotTiles];
+#pragma unroll
+  for (int u = 0; u < kPilotTiles; ++u) {
+    const int t = t0 + u * stride;
+    const int si = t * kTile + col;
+    const int64_t pos = (t < ntiles && si < m) ? ((int64_t)si * L) / m : 0;
+    load_k_bf16(p.K, kv_offset(p.K, b, g, pos), kf[u]);
+  }
+#pragma unroll
+  for (int u = 0; u < kPilotTiles; ++u) {
+    const int t = t0 + u * stride;
+    if (t >= ntiles) break;  // wave-uniform
     const int si = t * kTile + col;
     const bool valid = si < m;
-    const int64_t pos = valid ? ((int64_t)si * L) / m : 0;
-    const f32x4 acc = sc.score(p, b, g, pos);
+    const f32x4 acc = mfma_scores(qf, kf[u]);
     if (!p.group_shared) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -528,35 +543,56 @@ __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, in
   dense_scores<BF16>(p, dst, ld, bg / p.Hkv, bg % p.Hkv, blockIdx.x, gridDim.x, true, q_lds);
 }
 
-// Exact fallback, scoring: a small grid walks the (group, part) items and
-// scores the groups holding a flagged row into w.dense.  stats[0] counts the
-// flagged rows (the selection adds every flagged row before this runs), so
-// a call with none costs one read per workgroup.
+// Exact fallback, scoring.  grid = (kRepairParts, B*Hkv).  A row takes the
+// fallback when every row is forced to, or when its candidates cannot prove
+// exactness: fewer than k passed, or a staging area overflowed (a per-chunk
+// count of -1).  Each workgroup derives its group's flags from the rows'
+// per-chunk counts (part 0 records them in w.flags for the selection) and,
+// when a row of the group is flagged, scores its part of the group into
+// w.dense.
 template <bool BF16>
 __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
-  if (__hip_atomic_load(&w.stats[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
-    return;  // no row was flagged
+  __shared__ int cnt[kMaxGroup], bad[kMaxGroup];
+  __shared__ int any;
+  const int part = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
   const int nrows = p.group_shared ? 1 : p.G;
-  const int64_t items = (int64_t)p.B * p.Hkv * kRepairParts;
-  for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
-    const int bg = (int)(it / kRepairParts), part = (int)(it % kRepairParts);
-    const int b = bg / p.Hkv, g = bg % p.Hkv;
-    const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
-    int any = 0;
-    for (int r = 0; r < nrows; ++r) any |= w.flags[row0 + r];
-    if (!any) continue;  // uniform over the workgroup
-    dense_scores<BF16>(p, w.dense, p.ncap, b, g, part, kRepairParts, false, q_lds);
-    if (!BF16) __syncthreads();  // q_lds is rewritten for the next item
+  const int L = seq_len(p, b);
+  const int k = row_budget(p, b, L);
+  const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
+  const int tid = threadIdx.x;
+  if (tid < kMaxGroup) {
+    cnt[tid] = 0;
+    bad[tid] = 0;
   }
+  if (tid == 0) any = 0;
+  __syncthreads();
+  if (k > 0 && !w.force_repair) {
+    const int ck = kWaves * w.wave_keys;
+    const int nch = (L + ck - 1) / ck;
+    for (int e = tid; e < nrows * nch; e += kBlock) {
+      const int r = e / nch;
+      const int2 d = w.dir[(row0 + r) * w.nchunk + (e % nch)];
+      if (d.y < 0) bad[r] = 1;
+      else if (d.y > 0) atomicAdd(&cnt[r], d.y);
+    }
+  }
+  __syncthreads();
+  if (tid < nrows) {
+    const bool flag = k > 0 && (w.force_repair || bad[tid] || cnt[tid] < k);
+    if (flag) any = 1;
+    if (part == 0) w.flags[row0 + tid] = flag ? 1 : 0;
+  }
+  __syncthreads();
+  if (any) dense_scores<BF16>(p, w.dense, p.ncap, b, g, part, kRepairParts, false, q_lds);
 }
 
 // ---------------------------------------------------------------------------
 // Exact top-k of one row per workgroup.
-//   MODE 0: over the row's candidate lists (fused path); flags the row when
-//           the candidates do not prove exactness.
+//   MODE 0: the fused path.  A row flagged for the exact fallback (by
+//           k_repair_score) is selected from its full scores in w.dense, any
+//           other row from its candidates.
 //   MODE 1: over a full score row (sparse_decode_topk).
-// (k_repair_select below does the flagged rows of the fallback.)
 // Output: idx[row][0..k) ascending positions, then -1; vals[row][...] the
 // kept scores (or -inf), when vals is not null.
 // ---------------------------------------------------------------------------
@@ -671,7 +707,6 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   extern __shared__ uint32_t dyn[];
   __shared__ uint32_t hist[2048];
   __shared__ SelShared sh;
-  __shared__ int status;
   __shared__ float ftmp[kWaves];
   __shared__ uint32_t range[kWaves][2];
   __shared__ BucketShared bs;
@@ -684,11 +719,11 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   float *vrow = vals ? vals + (int64_t)row * p.k_max : nullptr;
   const int tid = threadIdx.x;
   if (k > 0) {
-    if (MODE == 0) {
-      if (w.flags[row]) {  // routed to the fallback by the pilot
-        if (tid == 0) atomicAdd(&w.stats[0], 1);
-        return;
-      }
+    if (MODE == 0 && w.flags[row]) {  // the exact fallback: full scores
+      if (tid == 0) atomicAdd(&w.stats[0], 1);
+      select_and_write(DenseSrc{w.dense + (int64_t)row * p.ncap}, L, k, hist, &sh, irow, vrow);
+    } else if (MODE == 0) {
+      // Candidates: at least k of them and no overflow (else flagged).
       const int ck = kWaves * w.wave_keys;
       const int nch = (L + ck - 1) / ck;
       const int rr = row % p.R;
@@ -697,13 +732,10 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
       int *start = pre + (nch + 1);   // nch
       uint32_t *lkey = (uint32_t *)(start + nch);
       const int2 *drow = w.dir + (int64_t)row * w.nchunk;
-      if (tid == 0) status = 0;
-      __syncthreads();
       int carry = 0;
       for (int base = 0; base < nch; base += kBlock) {
         const int c = base + tid;
         const int2 d = c < nch ? drow[c] : make_int2(0, 0);
-        if (d.y < 0) status = 1;  // a staging area overflowed
         int tot;
         const int e = block_excl_scan(d.y > 0 ? d.y : 0, sh.scan, &tot);
         if (c < nch) {
@@ -715,13 +747,6 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
       if (tid == 0) pre[nch] = carry;
       __syncthreads();
       const int total = carry;
-      if (status || total < k) {
-        if (tid == 0) {
-          w.flags[row] = 1;
-          atomicAdd(&w.stats[0], 1);
-        }
-        return;
-      }
       const int64_t gblk = ((int64_t)b * p.Hkv + g) * w.nchunk * kChunkCap;
       ChunkCands src{nullptr, pre, start, nch, w.ckey + gblk, w.cpos + gblk, ck};
       if (total <= lds_cap) {
@@ -760,35 +785,6 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   for (int i = k + tid; i < p.k_max; i += kBlock) {
     irow[i] = -1;
     if (vrow) vrow[i] = -__builtin_inff();
-  }
-}
-
-// Exact fallback, selection: a small grid walks the rows; each flagged row
-// is selected from its full scores in w.dense and gets its softmax weights
-// (per-head mode) or kept scores (group-shared mode) in w.sigma.
-__global__ __launch_bounds__(kBlock) void k_repair_select(Params p, Work w, int32_t *idx) {
-  __shared__ uint32_t hist[2048];
-  __shared__ SelShared sh;
-  __shared__ float ftmp[kWaves];
-  if (__hip_atomic_load(&w.stats[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
-    return;  // no row was flagged
-  const int rows = p.B * p.R;
-  for (int row = blockIdx.x; row < rows; row += gridDim.x) {
-    if (w.flags[row] == 0) continue;  // uniform over the workgroup
-    const int b = row / p.R;
-    const int L = seq_len(p, b);
-    const int k = row_budget(p, b, L);
-    int32_t *irow = idx + (int64_t)row * p.k_max;
-    float *vrow = w.sigma + (int64_t)row * p.k_max;
-    if (k > 0) {
-      select_and_write(DenseSrc{w.dense + (int64_t)row * p.ncap}, L, k, hist, &sh, irow, vrow);
-      if (!p.group_shared) kept_scores_to_weights(vrow, k, p.scale, ftmp);
-    }
-    for (int i = k + threadIdx.x; i < p.k_max; i += kBlock) {
-      irow[i] = -1;
-      vrow[i] = -__builtin_inff();
-    }
-    __syncthreads();  // LDS is reused by the next row
   }
 }
 
@@ -1118,9 +1114,8 @@ static inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1
 
 hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
   if (!w.force_repair) {
-    // Four 16-key sample tiles per wave.
-    const dim3 g1(kSampleMax / (4 * kTile * kWaves), p.B * p.Hkv);
-    k_pilot_score<true><<<g1, kBlock, 0, st>>>(p, w);
+    const dim3 g1(kSampleMax / (kPilotTiles * kTile * kWaves), p.B * p.Hkv);
+    k_pilot_score<<<g1, kBlock, 0, st>>>(p, w);
   }
   k_pilot_select<<<p.B * p.R, kBlock, 0, st>>>(p, w);
   return hipGetLastError();
@@ -1150,10 +1145,10 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
   return hipGetLastError();
 }
 
-hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream_t st) {
-  if (p.bf16) k_repair_score<true><<<kRepairGrid, kBlock, 0, st>>>(p, w);
-  else k_repair_score<false><<<kRepairGrid, kBlock, 0, st>>>(p, w);
-  k_repair_select<<<kRepairGrid, kBlock, 0, st>>>(p, w, idx);
+hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st) {
+  const dim3 grid(kRepairParts, p.B * p.Hkv);
+  if (p.bf16) k_repair_score<true><<<grid, kBlock, 0, st>>>(p, w);
+  else k_repair_score<false><<<grid, kBlock, 0, st>>>(p, w);
   return hipGetLastError();
 }
 

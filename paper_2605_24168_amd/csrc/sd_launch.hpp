@@ -12,7 +12,7 @@ hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st);
 size_t select_lds_bytes(int nchunk, int lds_cap);
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
                                     hipStream_t st);
-hipError_t launch_repair(const Params &p, const Work &w, int32_t *idx, hipStream_t st);
+hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st);
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st);
 int attend_nsplit(const Params &p);
