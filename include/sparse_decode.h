@@ -174,7 +174,10 @@ int64_t sparse_decode_budget(int64_t L, const sd_sparsity *sparsity);
 
 /* Profiling: while enabled, sparse_decode_attention records HIP events
  * between its stages on the call's stream (a ring of 64 calls per device;
- * enabling again starts a new series).  sparse_decode_last_profile waits for
+ * enabling again starts a new series).  enable = 1 records every stage;
+ * enable = 2 times only the scoring kernel, with events attached to its own
+ * dispatch (the profile then holds score_ms alone; nothing is added to the
+ * stream between kernels).  sparse_decode_last_profile waits for
  * the most recent call's events and fills `out`; sparse_decode_profile_mean
  * averages the stage times of the series' last min(n, 64) calls and stores
  * that count in *n_calls (repaired_rows is the last call's). */

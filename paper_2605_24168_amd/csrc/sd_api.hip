@@ -29,6 +29,7 @@ struct DevState {
   bool user_ws = false;
   bool events = false;
   hipEvent_t ev[kRing][6];
+  int level[kRing] = {};  // profiling level each ring slot was recorded with
   int64_t n_calls = 0;  // profiled calls in the current series
   int32_t *stats = nullptr;
 };
@@ -293,7 +294,7 @@ int64_t sparse_decode_budget(int64_t L, const sd_sparsity *sp) {
 
 sd_status sparse_decode_set_profiling(int32_t enable) {
   std::lock_guard<std::mutex> lk(g_mu);
-  g_profiling.store(enable ? 1 : 0);
+  g_profiling.store(enable == 2 ? 2 : (enable ? 1 : 0));
   if (enable)
     for (auto &d : g_dev) d.n_calls = 0;
   return SD_OK;
@@ -441,7 +442,8 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   int32_t *idx_ptr = (int32_t *)idx->data;
 
-  const bool prof = g_profiling.load() != 0;
+  const int prof_level = g_profiling.load();
+  const bool prof = prof_level != 0;
   if (prof && !ds->events) {
     for (auto &set : ds->ev)
       for (auto &e : set)
@@ -450,7 +452,7 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   }
   hipEvent_t *ev = ds->ev[ds->n_calls % kRing];
   auto mark = [&](int i) -> hipError_t {
-    return prof ? hipEventRecord(ev[i], stream_h) : hipSuccess;
+    return prof_level == 1 ? hipEventRecord(ev[i], stream_h) : hipSuccess;
   };
   // Candidate keys the selection stages in LDS (about 2.5 k expected).
   int64_t want = 4 * k_max + 1024;
@@ -460,7 +462,14 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   hipError_t e = mark(0);
   if (e == hipSuccess) e = sd::launch_pilot(p, w, stream_h);
   if (e == hipSuccess) e = mark(1);
-  if (e == hipSuccess && s.ncap > 0) e = sd::launch_score_stream(p, w, stream_h);
+  // Level 2 times the scoring kernel alone, with events attached to its
+  // dispatch (recorded back to back when the kernel does not run).
+  const bool streams = s.ncap > 0 && !w.force_repair;
+  if (e == hipSuccess && prof_level == 2 && !streams) e = hipEventRecord(ev[1], stream_h);
+  if (e == hipSuccess && prof_level == 2 && !streams) e = hipEventRecord(ev[2], stream_h);
+  if (e == hipSuccess && streams)
+    e = prof_level == 2 ? sd::launch_score_stream(p, w, stream_h, ev[1], ev[2])
+                        : sd::launch_score_stream(p, w, stream_h);
   if (e == hipSuccess) e = mark(2);
   if (e == hipSuccess && s.ncap > 0) e = sd::launch_repair(p, w, stream_h);
   if (e == hipSuccess) e = mark(3);
@@ -468,7 +477,10 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   if (e == hipSuccess) e = mark(4);
   if (e == hipSuccess) e = sd::launch_attend(p, w, idx_ptr, out->data, true, stream_h);
   if (e == hipSuccess) e = mark(5);
-  if (prof && e == hipSuccess) ds->n_calls++;
+  if (prof && e == hipSuccess) {
+    ds->level[ds->n_calls % kRing] = prof_level;
+    ds->n_calls++;
+  }
   ds->stats = w.stats;
   return hip_status(e);
 }
@@ -477,9 +489,17 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
 
 namespace {
 
-// Stage times of ring slot `slot` (its events must be complete).
+// Stage times of ring slot `slot` (its events must be complete).  A slot
+// recorded at level 2 has only the scoring-stream time (t[1]); the other
+// entries are 0.
 sd_status read_slot(DevState &ds, int slot, float t[6]) {
   hipEvent_t *ev = ds.ev[slot];
+  for (int i = 0; i < 6; ++i) t[i] = 0.f;
+  if (ds.level[slot] == 2) {
+    if (hipEventSynchronize(ev[2]) != hipSuccess) return SD_ERR_HIP;
+    if (hipEventElapsedTime(&t[1], ev[1], ev[2]) != hipSuccess) return SD_ERR_HIP;
+    return SD_OK;
+  }
   if (hipEventSynchronize(ev[5]) != hipSuccess) return SD_ERR_HIP;
   for (int i = 0; i < 5; ++i)
     if (hipEventElapsedTime(&t[i], ev[i], ev[i + 1]) != hipSuccess) return SD_ERR_HIP;

@@ -23,6 +23,8 @@
 // (then the k-th largest candidate is >= the threshold, so nothing above
 // the true k-th largest score was filtered out) and no staging area
 // overflowed.  Otherwise the row takes the exact fallback.
+#include <hip/hip_ext.h>
+
 #include "sd_internal.hpp"
 #include "sd_launch.hpp"
 
@@ -1121,17 +1123,29 @@ hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st) {
+// Launch with start/stop events attached to the kernel's own dispatch (no
+// extra packets on the stream), or a plain launch when they are null.
+static hipError_t launch_with_events(void (*kern)(Params, Work), dim3 grid, const Params &p,
+                                     const Work &w, hipStream_t st, hipEvent_t t0,
+                                     hipEvent_t t1) {
+  if (!t0) {
+    kern<<<grid, kBlock, 0, st>>>(p, w);
+    return hipGetLastError();
+  }
+  Params pa = p;
+  Work wa = w;
+  void *args[] = {&pa, &wa};
+  return hipExtLaunchKernel((const void *)kern, grid, dim3(kBlock), args, 0, st, t0, t1, 0);
+}
+
+hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st, hipEvent_t t0,
+                               hipEvent_t t1) {
   if (w.force_repair) return hipSuccess;  // every row takes the fallback
   const dim3 grid((unsigned)((int64_t)w.nchunk * p.B * p.Hkv));
-  if (p.K.paged) {
-    if (p.group_shared) k_score_stream<true, true><<<grid, kBlock, 0, st>>>(p, w);
-    else k_score_stream<true, false><<<grid, kBlock, 0, st>>>(p, w);
-  } else {
-    if (p.group_shared) k_score_stream<false, true><<<grid, kBlock, 0, st>>>(p, w);
-    else k_score_stream<false, false><<<grid, kBlock, 0, st>>>(p, w);
-  }
-  return hipGetLastError();
+  void (*kern)(Params, Work);
+  if (p.K.paged) kern = p.group_shared ? k_score_stream<true, true> : k_score_stream<true, false>;
+  else kern = p.group_shared ? k_score_stream<false, true> : k_score_stream<false, false>;
+  return launch_with_events(kern, grid, p, w, st, t0, t1);
 }
 
 size_t select_lds_bytes(int nchunk, int lds_cap) {

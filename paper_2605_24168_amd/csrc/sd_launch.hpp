@@ -8,7 +8,10 @@
 namespace sd {
 
 hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st);
-hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st);
+// t0/t1 (both or neither): events recorded at the scoring kernel's start and
+// end, attached to its dispatch.
+hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st,
+                               hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 size_t select_lds_bytes(int nchunk, int lds_cap);
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
                                     hipStream_t st);

@@ -295,8 +295,10 @@ def set_workspace(buf: Optional[torch.Tensor]) -> None:
     _workspace_ref = buf
 
 
-def set_profiling(enable: bool) -> None:
-    _check(lib.sparse_decode_set_profiling(int(bool(enable))), "sparse_decode_set_profiling")
+def set_profiling(enable) -> None:
+    """True/1: events between every stage; 2: only around the scoring stream."""
+    level = 2 if enable == 2 else int(bool(enable))
+    _check(lib.sparse_decode_set_profiling(level), "sparse_decode_set_profiling")
 
 
 def last_profile() -> dict:

@@ -296,6 +296,40 @@ def test_clustered_candidates_overflow_to_the_exact_fallback(sd):
     assert set(idx[0, 0, :k0]) <= set(range(100, 500))
 
 
+def test_profiling_levels(sd):
+    # Level 1 times every stage; level 2 only the scoring kernel (events
+    # attached to its dispatch).  Both leave the results unchanged, and level
+    # 2 still works when no scoring kernel runs (every row forced to the
+    # exact fallback).
+    inp = make("w3", seed=16)
+    q, cache, lens = sd.cache_from_inputs(inp)
+    sp = sd.sparsity_from_inputs(inp)
+    k_max = O.k_max_for(inp)
+    out0, idx0 = sd.sparse_decode_attention(q, cache, lens, sp, k_max=k_max)
+    profs = {}
+    for level in (1, 2):
+        sd.set_profiling(level)
+        for _ in range(3):
+            out, idx = sd.sparse_decode_attention(q, cache, lens, sp, k_max=k_max)
+        torch.cuda.synchronize()
+        sd.set_profiling(False)
+        profs[level] = sd.profile_mean()
+        assert torch.equal(out, out0) and torch.equal(idx, idx0)
+    assert profs[1]["valid"] == 1 and profs[1]["calls"] == 3 and profs[1]["total_ms"] > 0
+    assert profs[2]["valid"] == 1 and profs[2]["score_ms"] > 0 and profs[2]["total_ms"] == 0
+    sd.set_debug(1)
+    try:
+        sd.set_profiling(2)
+        out, idx = sd.sparse_decode_attention(q, cache, lens, sp, k_max=k_max)
+        torch.cuda.synchronize()
+        sd.set_profiling(False)
+        prof = sd.profile_mean()
+    finally:
+        sd.set_debug(0)
+    assert prof["valid"] == 1 and prof["score_ms"] >= 0
+    assert torch.equal(out, out0) and torch.equal(idx, idx0)
+
+
 def test_float32_gqa_and_paged(sd):
     inp = make("w4", seed=10, B=3, lmin=3000, lmax=9000, N=9000, dtype="f32")
     out, idx, _ = gpu_fused(sd, inp)
