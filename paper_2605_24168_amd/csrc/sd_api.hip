@@ -21,7 +21,6 @@ constexpr int kRing = 64;          // profiled calls remembered per device
 // Longest cache (positions per sequence): the selection keeps two entries
 // per candidate chunk (at least 1024 keys) in LDS.
 constexpr int64_t kMaxCapacity = int64_t(1) << 24;
-constexpr size_t kSelectLdsBudget = 150 * 1024;  // dynamic LDS of the selection kernel
 
 struct DevState {
   void *ws = nullptr;
@@ -457,7 +456,9 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   // Candidate keys the selection stages in LDS (about 2.5 k expected).
   int64_t want = 4 * k_max + 1024;
   const size_t pre_bytes = sd::select_lds_bytes(L.nchunk, 0);
-  const int64_t lds_room = (int64_t)((kSelectLdsBudget - pre_bytes) / 4);
+  const size_t budget = sd::select_lds_budget(p);
+  if (pre_bytes >= budget) return SD_ERR_UNSUPPORTED;
+  const int64_t lds_room = (int64_t)((budget - pre_bytes) / 4);
   const int lds_cap = (int)(want < lds_room ? want : lds_room);
   hipError_t e = mark(0);
   if (e == hipSuccess) e = sd::launch_pilot(p, w, stream_h);

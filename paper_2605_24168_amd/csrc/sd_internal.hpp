@@ -22,7 +22,7 @@ constexpr int kDenseChunk = 8192;  // keys per workgroup of the full-score kerne
 constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
 constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the fallback scoring
-constexpr int kRepairGrid = 512;   // workgroups of each fallback kernel
+constexpr int kSelectWideRows = 256; // fewer rows: 1024-thread selection workgroups
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -271,7 +271,9 @@ __device__ __forceinline__ float group_sum(f32x4 acc) {
 }
 
 // ---------------------------------------------------------------------------
-// Block-wide primitives (blockDim.x == kBlock).
+// Block-wide primitives for blocks of NT threads (NT / 64 waves, default
+// kBlock; the selection also runs 1024-thread blocks when rows are few).
+constexpr int kMaxBlockWaves = 16;
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int wave_incl_scan(int v) {
   const int l = lane_id();
@@ -284,14 +286,16 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 }
 
 // Exclusive prefix sum over the block in thread order; *total gets the sum.
-// tmp: LDS int[kWaves].  Must be reached by every thread of the block.
+// tmp: LDS int[NT / 64].  Must be reached by every thread of the block.
+template <int NT = kBlock>
 __device__ __forceinline__ int block_excl_scan(int v, int *tmp, int *total) {
+  constexpr int NW = NT / 64;
   const int inc = wave_incl_scan(v);
   if (lane_id() == 63) tmp[wave_id()] = inc;
   __syncthreads();
   int before = 0, tot = 0;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  for (int w = 0; w < NW; ++w) {
     const int t = tmp[w];
     before += (w < wave_id()) ? t : 0;
     tot += t;
@@ -307,13 +311,15 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+template <int NT = kBlock>
 __device__ __forceinline__ float block_max(float v, float *tmp) {
+  constexpr int NW = NT / 64;
   v = wave_max(v);
   if (lane_id() == 0) tmp[wave_id()] = v;
   __syncthreads();
   float m = tmp[0];
 #pragma unroll
-  for (int w = 1; w < kWaves; ++w) m = fmaxf(m, tmp[w]);
+  for (int w = 1; w < NW; ++w) m = fmaxf(m, tmp[w]);
   __syncthreads();
   return m;
 }
@@ -341,12 +347,12 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t dig, bool act)
 // bound of the k-th largest key.
 // ---------------------------------------------------------------------------
 struct SelShared {
-  int scan[kWaves];
+  int scan[kMaxBlockWaves];
   uint32_t digit;
   int above;
 };
 
-template <class Src>
+template <int NT = kBlock, class Src>
 __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelShared *sh,
                              uint32_t &T, int &need_eq, int passes = 3) {
   uint32_t prefix = 0, mask = 0;
@@ -357,9 +363,9 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
     const int shift = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
     const int nb = pass == 2 ? 1024 : 2048;
     const uint32_t dmask = (uint32_t)nb - 1u;
-    for (int i = tid; i < nb; i += kBlock) hist[i] = 0;
+    for (int i = tid; i < nb; i += NT) hist[i] = 0;
     __syncthreads();
-    for (int base = 0; base < n; base += kBlock) {
+    for (int base = 0; base < n; base += NT) {
       const int p = base + tid;
       uint32_t key = 0;
       bool act = false;
@@ -371,12 +377,12 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
     }
     __syncthreads();
     // Thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top.
-    const int bpt = nb / kBlock;
+    const int bpt = nb / NT;
     const int hi = nb - tid * bpt;
     int mine = 0;
     for (int i = 1; i <= bpt; ++i) mine += (int)hist[hi - i];
     int tot;
-    const int before = block_excl_scan(mine, sh->scan, &tot);
+    const int before = block_excl_scan<NT>(mine, sh->scan, &tot);
     if (before < krem && krem <= before + mine) {
       int cum = before;
       for (int i = 1; i <= bpt; ++i) {
@@ -408,13 +414,13 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
 // ---------------------------------------------------------------------------
 constexpr int kIpt = 8;
 
-template <class Src, class Emit>
+template <int NT = kBlock, class Src, class Emit>
 __device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int need_eq, int *scan,
                                  Emit emit) {
   int eq_before = 0, sel_before = 0;
   const int tid = threadIdx.x;
 #pragma unroll 1
-  for (int base = 0; base < n && sel_before < k; base += kBlock * kIpt) {
+  for (int base = 0; base < n && sel_before < k; base += NT * kIpt) {
     const int p0 = base + tid * kIpt;
     uint32_t key[kIpt];
     int n_eq = 0;
@@ -425,7 +431,7 @@ __device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int n
       n_eq += (p < n && key[u] == T) ? 1 : 0;
     }
     int eq_tot;
-    int eq_rank = block_excl_scan(n_eq, scan, &eq_tot) + eq_before;
+    int eq_rank = block_excl_scan<NT>(n_eq, scan, &eq_tot) + eq_before;
     unsigned sel_mask = 0;
     int n_sel = 0;
 #pragma unroll
@@ -444,7 +450,7 @@ __device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int n
       n_sel += sel ? 1 : 0;
     }
     int sel_tot;
-    int slot = block_excl_scan(n_sel, scan, &sel_tot) + sel_before;
+    int slot = block_excl_scan<NT>(n_sel, scan, &sel_tot) + sel_before;
 #pragma unroll
     for (int u = 0; u < kIpt; ++u)
       if (sel_mask & (1u << u)) emit(slot++, p0 + u, key[u]);

@@ -120,19 +120,21 @@ __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
 // inside the bucket holding the k-th largest, an exact rank count over its
 // items gives T (the k-th largest key) and need_eq (how many items equal to
 // T belong to the top k).  Returns false, with T and need_eq unset, when the
-// range is not finite or that bucket holds more than kBucketItems items.
+// range is not finite or that bucket holds more items than the block has
+// threads.
 // Every thread of the block must call it.
 // ---------------------------------------------------------------------------
 constexpr int kBuckets = 2048;
-constexpr int kBucketItems = kBlock;
 
+template <int NT = kBlock>
 struct BucketShared {
-  uint32_t items[kBucketItems];
+  uint32_t items[NT];  // the k-th bucket's items, at most one per thread
   int n;
 };
 
+template <int NT = kBlock>
 __device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, uint32_t kmax,
-                           uint32_t *hist, SelShared *sh, BucketShared *bs, uint32_t &T,
+                           uint32_t *hist, SelShared *sh, BucketShared<NT> *bs, uint32_t &T,
                            int &need_eq) {
   if (kmin == kmax) {  // all equal: the first k
     T = kmin;
@@ -147,21 +149,21 @@ __device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, ui
     const int bk = (int)((key2f(key) - vmin) * inv);
     return bk < kBuckets - 1 ? bk : kBuckets - 1;
   };
-  for (int i = tid; i < kBuckets; i += kBlock) hist[i] = 0;
+  for (int i = tid; i < kBuckets; i += NT) hist[i] = 0;
   __syncthreads();
-  for (int base = 0; base < n; base += kBlock) {
+  for (int base = 0; base < n; base += NT) {
     const int i = base + tid;
     const uint32_t key = i < n ? keys[i] : kmin;
     hist_add(hist, (uint32_t)bucket(key), i < n);
   }
   __syncthreads();
   // Thread t owns buckets [nb - (t+1)*bpt, nb - t*bpt), counted from the top.
-  constexpr int bpt = kBuckets / kBlock;
+  constexpr int bpt = kBuckets / NT;
   const int hi = kBuckets - tid * bpt;
   int mine = 0;
   for (int j = 1; j <= bpt; ++j) mine += (int)hist[hi - j];
   int tot;
-  const int before = block_excl_scan(mine, sh->scan, &tot);
+  const int before = block_excl_scan<NT>(mine, sh->scan, &tot);
   if (tid == 0) bs->n = 0;
   if (before < k && k <= before + mine) {
     int cum = before;
@@ -180,8 +182,8 @@ __device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, ui
   const int krem = k - sh->above;
   const int m = (int)hist[bstar];
   bool found = false;
-  if (m <= kBucketItems) {  // uniform
-    for (int base = 0; base < n; base += kBlock) {
+  if (m <= NT) {  // uniform
+    for (int base = 0; base < n; base += NT) {
       const int i = base + tid;
       if (i < n) {
         const uint32_t key = keys[i];
@@ -211,8 +213,9 @@ __device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, ui
   return found;
 }
 
-// Block-wide (min, max) of per-thread key ranges; tmp: LDS uint32[kWaves][2].
+// Block-wide (min, max) of per-thread key ranges; tmp: LDS uint32[NT/64][2].
 // Ends with a barrier (so LDS written before the call is visible after it).
+template <int NT = kBlock>
 __device__ __forceinline__ void block_key_range(uint32_t &mn, uint32_t &mx, uint32_t (*tmp)[2]) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -226,7 +229,7 @@ __device__ __forceinline__ void block_key_range(uint32_t &mn, uint32_t &mx, uint
   }
   __syncthreads();
 #pragma unroll
-  for (int v = 0; v < kWaves; ++v) {
+  for (int v = 0; v < NT / 64; ++v) {
     mn = tmp[v][0] < mn ? tmp[v][0] : mn;
     mx = tmp[v][1] > mx ? tmp[v][1] : mx;
   }
@@ -249,7 +252,7 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[2048];
   __shared__ SelShared sh;
-  __shared__ BucketShared bs;
+  __shared__ BucketShared<> bs;
   __shared__ uint32_t range[kWaves][2];
   const int row = blockIdx.x, b = row / p.R;
   const int L = seq_len(p, b);
@@ -638,13 +641,13 @@ struct ChunkCands {
   }
 };
 
-template <class Src>
+template <int NT = kBlock, class Src>
 __device__ __forceinline__ void select_and_write(const Src &src, int n, int k, uint32_t *hist,
                                                  SelShared *sh, int32_t *irow, float *vrow) {
   uint32_t T;
   int need_eq;
-  radix_select(src, n, k, hist, sh, T, need_eq);
-  compact_selected(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
+  radix_select<NT>(src, n, k, hist, sh, T, need_eq);
+  compact_selected<NT>(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
     irow[slot] = (int32_t)src.pos(i);
     if (vrow) vrow[slot] = key2f(key);
   });
@@ -657,35 +660,36 @@ __device__ __forceinline__ void select_and_write(const Src &src, int n, int k, u
 // keys before its scans) and writes the softmax weights exp(scale * (s -
 // vmax)) (or, group-shared mode, the kept scores); finally every thread
 // fetches the positions of its kept items with the loads in flight together.
+template <int NT>
 __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, int n, int k,
                                                         uint32_t kmin, uint32_t kmax,
                                                         uint32_t *hist, SelShared *sh,
-                                                        BucketShared *bs, int32_t *irow,
+                                                        BucketShared<NT> *bs, int32_t *irow,
                                                         float *vrow, bool weights, float scale) {
   const int tid = threadIdx.x;
   const float vmax = key2f(kmax);
   uint32_t T;
   int need_eq;
-  if (!bucket_kth(src.lkey, n, k, kmin, kmax, hist, sh, bs, T, need_eq))
-    radix_select(src, n, k, hist, sh, T, need_eq);
+  if (!bucket_kth<NT>(src.lkey, n, k, kmin, kmax, hist, sh, bs, T, need_eq))
+    radix_select<NT>(src, n, k, hist, sh, T, need_eq);
   uint32_t *stage = const_cast<uint32_t *>(src.lkey);
-  compact_selected(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
+  compact_selected<NT>(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
     stage[slot] = (uint32_t)i;
     const float v = key2f(key);
     vrow[slot] = weights ? expf(scale * (v - vmax)) : v;
   });
   __syncthreads();
-  constexpr int kP = 4;
-  for (int s0 = tid; s0 < k; s0 += kBlock * kP) {
+  constexpr int kP = 8;  // position loads in flight per thread
+  for (int s0 = tid; s0 < k; s0 += NT * kP) {
     uint32_t pos[kP];
 #pragma unroll
     for (int u = 0; u < kP; ++u) {
-      const int s = s0 + u * kBlock;
+      const int s = s0 + u * NT;
       pos[u] = s < k ? src.pos((int)stage[s]) : 0u;
     }
 #pragma unroll
     for (int u = 0; u < kP; ++u) {
-      const int s = s0 + u * kBlock;
+      const int s = s0 + u * NT;
       if (s < k) irow[s] = (int32_t)pos[u];
     }
   }
@@ -695,23 +699,26 @@ __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, i
 // by this workgroup) into softmax weights exp(scale*(s - max s)) in place, so
 // that the attention is a plain weighted gather whose splits all share one
 // reference maximum.
+template <int NT = kBlock>
 __device__ __forceinline__ void kept_scores_to_weights(float *vrow, int k, float scale, float *ftmp) {
   __syncthreads();  // vrow was written by other threads of the block
   float m = -__builtin_inff();
-  for (int i = threadIdx.x; i < k; i += kBlock) m = fmaxf(m, vrow[i]);
-  m = block_max(m, ftmp);
-  for (int i = threadIdx.x; i < k; i += kBlock) vrow[i] = expf(scale * (vrow[i] - m));
+  for (int i = threadIdx.x; i < k; i += NT) m = fmaxf(m, vrow[i]);
+  m = block_max<NT>(m, ftmp);
+  for (int i = threadIdx.x; i < k; i += NT) vrow[i] = expf(scale * (vrow[i] - m));
 }
 
-template <int MODE>
-__global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float *dense, int64_t ld,
-                                                   int32_t *idx, float *vals, int lds_cap) {
+// NT threads per workgroup: 256, or 1024 when the rows are too few to fill
+// the GPU one workgroup each (every per-thread loop is then 4x shorter).
+template <int MODE, int NT>
+__global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *dense, int64_t ld,
+                                               int32_t *idx, float *vals, int lds_cap) {
   extern __shared__ uint32_t dyn[];
   __shared__ uint32_t hist[2048];
   __shared__ SelShared sh;
-  __shared__ float ftmp[kWaves];
-  __shared__ uint32_t range[kWaves][2];
-  __shared__ BucketShared bs;
+  __shared__ float ftmp[NT / 64];
+  __shared__ uint32_t range[NT / 64][2];
+  __shared__ BucketShared<NT> bs;
   bool weights_done = false;
   const int row = blockIdx.x, b = row / p.R;
   const bool weights = MODE != 1 && !p.group_shared;
@@ -723,7 +730,7 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
   if (k > 0) {
     if (MODE == 0 && w.flags[row]) {  // the exact fallback: full scores
       if (tid == 0) atomicAdd(&w.stats[0], 1);
-      select_and_write(DenseSrc{w.dense + (int64_t)row * p.ncap}, L, k, hist, &sh, irow, vrow);
+      select_and_write<NT>(DenseSrc{w.dense + (int64_t)row * p.ncap}, L, k, hist, &sh, irow, vrow);
     } else if (MODE == 0) {
       // Candidates: at least k of them and no overflow (else flagged).
       const int ck = kWaves * w.wave_keys;
@@ -735,11 +742,11 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
       uint32_t *lkey = (uint32_t *)(start + nch);
       const int2 *drow = w.dir + (int64_t)row * w.nchunk;
       int carry = 0;
-      for (int base = 0; base < nch; base += kBlock) {
+      for (int base = 0; base < nch; base += NT) {
         const int c = base + tid;
         const int2 d = c < nch ? drow[c] : make_int2(0, 0);
         int tot;
-        const int e = block_excl_scan(d.y > 0 ? d.y : 0, sh.scan, &tot);
+        const int e = block_excl_scan<NT>(d.y > 0 ? d.y : 0, sh.scan, &tot);
         if (c < nch) {
           pre[c] = carry + e;
           start[c] = d.x;
@@ -754,16 +761,16 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
       if (total <= lds_cap) {
         constexpr int kU = 16;  // loads in flight per thread
         uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-        for (int i0 = tid; i0 < total; i0 += kBlock * kU) {
+        for (int i0 = tid; i0 < total; i0 += NT * kU) {
           uint32_t v[kU];
 #pragma unroll
           for (int u = 0; u < kU; ++u) {
-            const int i = i0 + u * kBlock;
+            const int i = i0 + u * NT;
             v[u] = i < total ? src.key(i) : 0u;
           }
 #pragma unroll
           for (int u = 0; u < kU; ++u) {
-            const int i = i0 + u * kBlock;
+            const int i = i0 + u * NT;
             if (i < total) {
               lkey[i] = v[u];
               mn = v[u] < mn ? v[u] : mn;
@@ -771,20 +778,20 @@ __global__ __launch_bounds__(kBlock) void k_select(Params p, Work w, const float
             }
           }
         }
-        block_key_range(mn, mx, range);  // also publishes lkey
+        block_key_range<NT>(mn, mx, range);  // also publishes lkey
         src.lkey = lkey;
-        select_and_write_staged(src, total, k, mn, mx, hist, &sh, &bs, irow, vrow, weights,
+        select_and_write_staged<NT>(src, total, k, mn, mx, hist, &sh, &bs, irow, vrow, weights,
                                 p.scale);
         weights_done = true;
       } else {
-        select_and_write(src, total, k, hist, &sh, irow, vrow);
+        select_and_write<NT>(src, total, k, hist, &sh, irow, vrow);
       }
     } else {
-      select_and_write(DenseSrc{dense + (int64_t)row * ld}, L, k, hist, &sh, irow, vrow);
+      select_and_write<NT>(DenseSrc{dense + (int64_t)row * ld}, L, k, hist, &sh, irow, vrow);
     }
-    if (weights && !weights_done) kept_scores_to_weights(vrow, k, p.scale, ftmp);
+    if (weights && !weights_done) kept_scores_to_weights<NT>(vrow, k, p.scale, ftmp);
   }
-  for (int i = k + tid; i < p.k_max; i += kBlock) {
+  for (int i = k + tid; i < p.k_max; i += NT) {
     irow[i] = -1;
     if (vrow) vrow[i] = -__builtin_inff();
   }
@@ -1152,10 +1159,21 @@ size_t select_lds_bytes(int nchunk, int lds_cap) {
   return (size_t)(2 * nchunk + 1) * 4 + (size_t)lds_cap * 4;
 }
 
+size_t select_lds_budget(const Params &p) {
+  // Dynamic LDS left by the selection kernel's static LDS (hist, scan and
+  // bucket scratch: about 9.4 KB at 256 threads, 12.6 KB at 1024) under the
+  // 160 KB of a workgroup.
+  return (size_t)(p.B * p.R) < (size_t)kSelectWideRows ? 144 * 1024 : 150 * 1024;
+}
+
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
                                     hipStream_t st) {
   const size_t lds = select_lds_bytes(w.nchunk, lds_cap);
-  k_select<0><<<p.B * p.R, kBlock, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
+  const unsigned rows = (unsigned)(p.B * p.R);
+  if (rows < kSelectWideRows)
+    k_select<0, 1024><<<rows, 1024, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
+  else
+    k_select<0, kBlock><<<rows, kBlock, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
   return hipGetLastError();
 }
 
@@ -1248,7 +1266,7 @@ hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st) {
 hipError_t launch_topk(const Params &p, const float *scores, int32_t *idx, float *vals,
                        hipStream_t st) {
   Work none{};
-  k_select<1><<<p.B * p.R, kBlock, 0, st>>>(p, none, scores, p.ncap, idx, vals, 0);
+  k_select<1, kBlock><<<p.B * p.R, kBlock, 0, st>>>(p, none, scores, p.ncap, idx, vals, 0);
   return hipGetLastError();
 }
 

@@ -13,6 +13,8 @@ hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st);
 hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st,
                                hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 size_t select_lds_bytes(int nchunk, int lds_cap);
+// Dynamic LDS available to the candidate selection for these shapes.
+size_t select_lds_budget(const Params &p);
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
                                     hipStream_t st);
 hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st);
