@@ -155,18 +155,25 @@ struct QFrag {
   u32x4 v[4];
 };
 
-__device__ __forceinline__ void load_q_bf16(const Params &p, int b, int g, QFrag &qf) {
+// Query operand of nh (<= 16) consecutive query heads from `first`; rows
+// beyond nh are zero.
+__device__ __forceinline__ void load_q_heads(const Params &p, int b, int first, int nh,
+                                             QFrag &qf) {
   const int l = lane_id();
   const int h = l & 15, s = l >> 4;
-  if (h < p.G) {
-    const uint16_t *qp =
-        (const uint16_t *)p.q + ((int64_t)b * p.Hq + (int64_t)g * p.G + h) * kHeadDim + 8 * s;
+  if (h < nh) {
+    const uint16_t *qp = (const uint16_t *)p.q + ((int64_t)b * p.Hq + first + h) * kHeadDim + 8 * s;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) qf.v[kk] = *(const u32x4 *)(qp + 32 * kk);
   } else {
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) qf.v[kk] = u32x4{0u, 0u, 0u, 0u};
   }
+}
+
+// The G query heads of KV head g.
+__device__ __forceinline__ void load_q_bf16(const Params &p, int b, int g, QFrag &qf) {
+  load_q_heads(p, b, g * p.G, p.G, qf);
 }
 
 struct KFrag {

@@ -891,7 +891,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
                                                    int split) {
   extern __shared__ int64_t att_dyn[];
   __shared__ float mh[kMaxGroup];
-  __shared__ float ftmp[kWaves];
+  __shared__ float hmax[kWaves][kMaxGroup];
   constexpr int U = (BF16 && !GRP) ? 8 : 4;  // positions per 16-lane group per step
   constexpr int HB = GRP ? kAttHeads : 1;  // heads accumulated per pass
 
@@ -938,10 +938,10 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     voff_l[t] = kv_offset(p.V, b, g, jc);
     if (recompute) koff_l[t] = kv_offset(p.K, b, g, jc);
   }
-  if (recompute) {
+  if (recompute && !BF16) {  // float32 queries for the vector-ALU logits
     for (int e = tid; e < nh * kHeadDim; e += kBlock) {
       const int64_t qo = ((int64_t)b * p.Hq + h0 + e / kHeadDim) * kHeadDim + e % kHeadDim;
-      q_l[e] = BF16 ? bf16_to_f32(((const uint16_t *)p.q)[qo]) : ((const float *)p.q)[qo];
+      q_l[e] = ((const float *)p.q)[qo];
     }
   }
   __syncthreads();
@@ -953,6 +953,40 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     const float *wrow = w.sigma + (int64_t)row * p.k_max + e0;
     for (int t = tid; t < n; t += kBlock) e_l[t] = wrow[t];
     if (tid == 0) mh[0] = 0.f;
+  } else if constexpr (BF16) {
+    // Logits by MFMA: a wave scores 16 kept positions per tile, each lane
+    // loading its position's key slices straight into the operand layout;
+    // the query operand's rows are the nh heads served.  Two tiles' loads
+    // are in flight before their matrix ops.
+    QFrag qf;
+    load_q_heads(p, b, h0, nh, qf);
+    const int ntile = (n + kTile - 1) / kTile;
+    const int kcol = l & 15, quad = l >> 4;
+    auto tile_off = [&](int ti) {
+      const int t = ti * kTile + kcol;
+      return koff_l[t < n ? t : 0];
+    };
+    for (int ti = wv; ti < ntile; ti += 2 * kWaves) {
+      const int ti1 = ti + kWaves;
+      KFrag kf[2];
+      load_k_bf16(p.K, tile_off(ti), kf[0]);
+      load_k_bf16(p.K, tile_off(ti1 < ntile ? ti1 : ti), kf[1]);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int tt = u == 0 ? ti : ti1;
+        if (tt >= ntile) break;  // wave-uniform
+        const f32x4 acc = mfma_scores(qf, kf[u]);
+        const int t = tt * kTile + kcol;
+        if (t < n) {
+          const bool skip = pos_l[t] < 0;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int h = 4 * quad + r;
+            if (h < nh) e_l[h * split + t] = skip ? -__builtin_inff() : p.scale * acc[r];
+          }
+        }
+      }
+    }
   } else {
     for (int t = wv * 4 + sub; t < n; t += kWaves * 4) {
       const int32_t j = pos_l[t];
@@ -977,11 +1011,20 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   }
   __syncthreads();
   if (recompute) {
+    // Per-head maxima: every wave reduces its share, one barrier, then
+    // thread h combines the waves.
     for (int h = 0; h < nh; ++h) {
       float m = -__builtin_inff();
       for (int t = tid; t < n; t += kBlock) m = fmaxf(m, e_l[h * split + t]);
-      m = block_max(m, ftmp);
-      if (tid == 0) mh[h] = m;
+      m = wave_max(m);
+      if (l == 0) hmax[wv][h] = m;
+    }
+    __syncthreads();
+    if (tid < nh) {
+      float m = hmax[0][tid];
+#pragma unroll
+      for (int v = 1; v < kWaves; ++v) m = fmaxf(m, hmax[v][tid]);
+      mh[tid] = m;
     }
     __syncthreads();
     // Weights exp(z - m); skipped entries (z = -inf) give 0.
