@@ -801,11 +801,12 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
 // Gather-attend.  grid = (splits, rows).  Workgroup s of row (b, r) takes
 // list entries [s*split, +split) of idx[b][r]; in per-head mode the row is
 // query head r, in group-shared mode it serves the G heads of KV head r.
-// FUSED: the list holds exactly k_b valid positions and sigma their scores;
-// otherwise entries outside [0, L_b) are skipped and the logits recomputed
-// from the key rows.  The softmax weights exp(z - max) are formed once per
-// position in LDS.  Each wave then walks 4 * kGatherU positions per step
-// (kGatherU per 16-lane group, 16 lanes x 16 bytes covering one 256-byte
+// FUSED: the list holds exactly k_b valid positions, and per-head rows take
+// their softmax weights from sigma (formed by the selection); group-shared
+// rows, and every row of the unfused call, recompute each head's logits
+// from the kept key rows (MFMA tiles for bf16), skipping entries outside
+// [0, L_b), and form the weights exp(z - max) once per position in LDS.  Each wave then walks 4 * U positions per step
+// (U per 16-lane group, 16 lanes x 16 bytes covering one 256-byte
 // bf16 value row), with the next step's loads issued before the current
 // step is consumed.  A row split over several workgroups leaves (max, sum,
 // unnormalised output) partials that k_merge combines.
