@@ -103,7 +103,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", type=int, default=3, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-sample", type=int, default=4,
+    ap.add_argument("--cpu-sample", type=int, default=8,
                     help="sequences of the workload the CPU oracle is timed on (0: skip)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device to device once (a plain "

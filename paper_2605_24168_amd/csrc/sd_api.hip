@@ -42,6 +42,7 @@ struct Shape {
   int B, Hq, Hkv, G, R;
   int64_t ncap;
   int bf16;
+  int paged;
   int64_t k_max;
 };
 
@@ -104,6 +105,7 @@ sd_status check_problem(const sd_tensor *q, const sd_kv *K, const sd_kv *V, cons
   }
   if (s.Hq % hkv) return SD_ERR_INVALID_ARG;
   s.Hkv = hkv;
+  s.paged = K->layout == SD_KV_PAGED_NHD;
   s.G = s.Hq / hkv;
   if (s.G > sd::kMaxGroup) return SD_ERR_UNSUPPORTED;
   s.ncap = ncap;
@@ -186,7 +188,7 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared) {
 // the same layout is recomputed on every call.
 struct Layout {
   size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, total;
-  int nchunk, wave_keys, nsplit;
+  int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
 };
 
 Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp) {
@@ -194,8 +196,15 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
   const int group_shared = sp->group_shared ? 1 : 0;
   const int64_t rows = (int64_t)s.B * s.R;
   L.wave_keys = wave_keys_for(s, sp, group_shared);
-  const int64_t ck = (int64_t)sd::kWaves * L.wave_keys;
-  L.nchunk = (int)((s.ncap + ck - 1) / ck);
+  // Paged caches with a multiple of 4 KV heads are scored one head per wave
+  // over shared chunks of wave_keys keys (the workgroup reads four heads of
+  // each page block together), unless that makes too many chunks for the
+  // selection's per-chunk tables.
+  const int64_t qchunks = (s.ncap + L.wave_keys - 1) / L.wave_keys;
+  const bool quad = s.paged && s.Hkv % sd::kWaves == 0 && qchunks <= 8192;
+  L.chunk_keys = quad ? L.wave_keys : sd::kWaves * L.wave_keys;
+  L.blk_cap = quad ? sd::kCandBuf : sd::kChunkCap;
+  L.nchunk = (int)((s.ncap + L.chunk_keys - 1) / L.chunk_keys);
   sd::Params shape_only{};
   shape_only.B = s.B;
   shape_only.R = s.R;
@@ -210,7 +219,7 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
     return o;
   };
   if (fused) {
-    const size_t blocks = (size_t)s.B * s.Hkv * L.nchunk * sd::kChunkCap;
+    const size_t blocks = (size_t)s.B * s.Hkv * L.nchunk * L.blk_cap;
     L.sample = take((size_t)rows * sd::kSampleMax * 4);
     L.theta = take((size_t)rows * 4);
     L.dir = take((size_t)rows * L.nchunk * 8);
@@ -266,6 +275,8 @@ sd::Work carve(char *base, const Layout &L, bool fused) {
   w.stats = (int32_t *)(base + L.stats);
   w.nchunk = L.nchunk;
   w.wave_keys = L.wave_keys;
+  w.chunk_keys = L.chunk_keys;
+  w.blk_cap = L.blk_cap;
   w.nsplit = L.nsplit;
   w.force_repair = (g_debug.load() & 1) ? 1 : 0;
   return w;

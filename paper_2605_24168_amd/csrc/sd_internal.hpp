@@ -61,16 +61,19 @@ struct Work {
   float *theta;      // [rows] candidate threshold
   int2 *dir;         // [rows][nchunk] (start, count) of the row's candidates in
                      // its chunk's block; count -1 = a staging area overflowed
-  uint32_t *ckey;    // [B*Hkv][nchunk][kChunkCap] order-preserving score keys
-  uint16_t *cpos;    // [B*Hkv][nchunk][kChunkCap] positions within the chunk
+  uint32_t *ckey;    // [B*Hkv][nchunk][blk_cap] order-preserving score keys
+  uint16_t *cpos;    // [B*Hkv][nchunk][blk_cap] positions within the chunk
   int32_t *flags;    // [rows] 1 = the row needs the exact fallback
   float *dense;      // [rows][ncap] fallback scores
   float *sigma;      // [rows][k_max] kept scores (group-shared mode) or softmax
                      // weights exp(scale*(s - max s)) (per-head mode), aligned with idx
   float *part;       // [B*Hq][nsplit][kPartStride] attend partials
   int32_t *stats;    // [4]: [0] rows repaired in the last call
-  int32_t nchunk;      // chunks per sequence (of kWaves * wave_keys keys)
+  int32_t nchunk;      // chunks per sequence (of chunk_keys keys)
   int32_t wave_keys;   // keys per scoring wave: 256, 512, 1024 or 2048
+  int32_t chunk_keys;  // keys per chunk: kWaves * wave_keys, or wave_keys when
+                       // each wave of a workgroup scores its own KV head
+  int32_t blk_cap;     // entries per packed block: kChunkCap, or kCandBuf
   int32_t nsplit;
   int32_t force_repair;  // every row takes the exact fallback
 };

@@ -321,18 +321,29 @@ struct WaveLds {
 // bfloat16 caches.  The loop body issues a fixed set of loads every step
 // (tile indices past the end are clamped to the last tile, whose keys the
 // filter then masks), so the compiler's memory waits are exact.
-template <bool PAGED, bool GRP>
+// QUAD (paged layout, Hkv a multiple of 4): a chunk is wk keys, and wave v
+// of the workgroup of (quad q, chunk) scores KV head 4q + v over the whole
+// chunk, so the workgroup reads four of the heads of every page block
+// together; each wave then packs its own head's block.
+template <bool PAGED, bool GRP, bool QUAD>
 __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
+  static_assert(PAGED || !QUAD, "head quads are for the paged layout");
   __shared__ WaveLds wlds[kWaves];
-  __shared__ int seg_n[kWaves * kMaxGroup];        // [row][wave] candidates found
-  __shared__ int seg_off[kWaves * kMaxGroup + 1];  // their offsets in the block
+  __shared__ int seg_n[kWaves * kMaxGroup];            // [row][wave] candidates found
+  __shared__ int seg_off[kWaves * (kMaxGroup + 1)];    // their offsets in the block(s)
   const int wk = w.wave_keys;
+  const int wv = wave_id();
   // Dispatch order (consecutive workgroups run together): in the paged
   // layout the KV heads of a page block are adjacent in memory, so heads go
   // fastest; in the contiguous layout a head's slab is swept chunk by chunk.
   const int wid = (int)blockIdx.x;
   int chunk, g, b;
-  if (PAGED) {
+  if (QUAD) {
+    const int nq = p.Hkv / kWaves;
+    chunk = (wid / nq) % w.nchunk;
+    b = wid / (nq * w.nchunk);
+    g = kWaves * (wid % nq) + wv;
+  } else if (PAGED) {
     g = wid % p.Hkv;
     chunk = (wid / p.Hkv) % w.nchunk;
     b = wid / (p.Hkv * w.nchunk);
@@ -343,10 +354,9 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   }
   const int bg = b * p.Hkv + g;
   const int L = seq_len(p, b);
-  const int64_t c0 = (int64_t)chunk * kWaves * wk;
-  if (c0 >= L) return;  // whole workgroup
-  const int wv = wave_id();
-  const int64_t w0 = c0 + (int64_t)wv * wk;
+  const int64_t c0 = (int64_t)chunk * w.chunk_keys;
+  if (c0 >= L) return;  // whole workgroup (every wave has the same chunk)
+  const int64_t w0 = QUAD ? c0 : c0 + (int64_t)wv * wk;
   const int nvalid = w0 < L ? (int)((L - w0) < wk ? (L - w0) : wk) : 0;
   const int l = lane_id(), col = l & 15, s = l >> 4;
   const int64_t row0 = GRP ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
@@ -446,6 +456,55 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
     }
     filter(prev, prev_jl);
   }
+  if constexpr (QUAD) {
+    // This wave's block: its rows one after another, each in position order.
+    int *off = seg_off + wv * (kMaxGroup + 1);
+    if (col == 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int h = 4 * s + r;
+        if (h < nrows) seg_n[wv * kMaxGroup + h] = cnt[r];
+      }
+    }
+    __builtin_amdgcn_wave_barrier();  // counts were written by other lanes
+    const int n = l < nrows ? seg_n[wv * kMaxGroup + l] : 0;
+    const int nc = n < cap ? n : cap;
+    const int inc = wave_incl_scan(nc);
+    if (l < nrows)
+      w.dir[(row0 + l) * w.nchunk + chunk] = make_int2(inc - nc, n > cap ? -1 : nc);
+    if (l <= kMaxGroup) off[l] = inc - nc;  // rows >= nrows: the total
+    const int ntot = __shfl(inc, 63);
+    __builtin_amdgcn_wave_barrier();  // offsets are read by every lane
+    const int64_t blk = ((int64_t)bg * w.nchunk + chunk) * w.blk_cap;
+    uint32_t *kdst = w.ckey + blk;
+    uint16_t *pdst = w.cpos + blk;
+    for (int i0 = 4 * l; i0 < ntot; i0 += 4 * 64) {
+      // Row of item i0: the last t with off[t] <= i0.
+      int t = 0;
+#pragma unroll
+      for (int step = 8; step > 0; step >>= 1)
+        if (off[t + step] <= i0) t += step;
+      u32x4 kv;
+      uint32_t pv[2] = {0u, 0u};
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u;
+        uint32_t key = 0u, pos = 0u;
+        if (i < ntot) {
+          while (off[t + 1] <= i) ++t;  // stops at t = 15: off[16] = ntot > i
+          const uint2 it = wl.cand[t * cap + (i - off[t])];
+          key = f2key(__uint_as_float(it.x));
+          pos = it.y;
+        }
+        kv[u] = key;
+        pv[u >> 1] |= pos << (16 * (u & 1));
+      }
+      __builtin_nontemporal_store(kv, (u32x4 *)(kdst + i0));
+      __builtin_nontemporal_store((unsigned long long)pv[0] | ((unsigned long long)pv[1] << 32),
+                                  (unsigned long long *)(pdst + i0));
+    }
+    return;
+  }
   if (col == 0) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -474,7 +533,7 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   }
   __syncthreads();
   const int ntot = seg_off[64];
-  const int64_t blk = ((int64_t)bg * w.nchunk + chunk) * kChunkCap;
+  const int64_t blk = ((int64_t)bg * w.nchunk + chunk) * w.blk_cap;
   uint32_t *kdst = w.ckey + blk;
   uint16_t *pdst = w.cpos + blk;
   for (int i0 = 4 * tid; i0 < ntot; i0 += 4 * kBlock) {
@@ -573,7 +632,7 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   if (tid == 0) any = 0;
   __syncthreads();
   if (k > 0 && !w.force_repair) {
-    const int ck = kWaves * w.wave_keys;
+    const int ck = w.chunk_keys;
     const int nch = (L + ck - 1) / ck;
     for (int e = tid; e < nrows * nch; e += kBlock) {
       const int r = e / nch;
@@ -615,9 +674,10 @@ struct ChunkCands {
   const int *pre;        // nch + 1 prefix sums (LDS)
   const int *start;      // nch block offsets (LDS)
   int nch;
-  const uint32_t *gkey;  // the group's blocks, kChunkCap entries apart
+  const uint32_t *gkey;  // the group's blocks, cap entries apart
   const uint16_t *gpos;
   int ck;                // keys per chunk
+  int cap;               // entries per block
   // Chunk holding item i: the last c with pre[c] <= i (empty chunks share
   // their successor's prefix value, so this is the owner).
   __device__ __forceinline__ int chunk_of(int i) const {
@@ -629,7 +689,7 @@ struct ChunkCands {
     return lo;
   }
   __device__ __forceinline__ int64_t slot(int c, int i) const {
-    return (int64_t)c * kChunkCap + start[c] + (i - pre[c]);
+    return (int64_t)c * cap + start[c] + (i - pre[c]);
   }
   __device__ __forceinline__ uint32_t key(int i) const {
     if (lkey) return lkey[i];
@@ -733,7 +793,7 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
       select_and_write<NT>(DenseSrc{w.dense + (int64_t)row * p.ncap}, L, k, hist, &sh, irow, vrow);
     } else if (MODE == 0) {
       // Candidates: at least k of them and no overflow (else flagged).
-      const int ck = kWaves * w.wave_keys;
+      const int ck = w.chunk_keys;
       const int nch = (L + ck - 1) / ck;
       const int rr = row % p.R;
       const int g = p.group_shared ? rr : rr / p.G;
@@ -756,8 +816,8 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
       if (tid == 0) pre[nch] = carry;
       __syncthreads();
       const int total = carry;
-      const int64_t gblk = ((int64_t)b * p.Hkv + g) * w.nchunk * kChunkCap;
-      ChunkCands src{nullptr, pre, start, nch, w.ckey + gblk, w.cpos + gblk, ck};
+      const int64_t gblk = ((int64_t)b * p.Hkv + g) * w.nchunk * w.blk_cap;
+      ChunkCands src{nullptr, pre, start, nch, w.ckey + gblk, w.cpos + gblk, ck, w.blk_cap};
       if (total <= lds_cap) {
         constexpr int kU = 16;  // loads in flight per thread
         uint32_t mn = 0xFFFFFFFFu, mx = 0u;
@@ -1189,14 +1249,24 @@ static hipError_t launch_with_events(void (*kern)(Params, Work), dim3 grid, cons
   return hipExtLaunchKernel((const void *)kern, grid, dim3(kBlock), args, 0, st, t0, t1, 0);
 }
 
+bool stream_by_head_quads(const Work &w) { return w.chunk_keys == w.wave_keys; }
+
 hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st, hipEvent_t t0,
                                hipEvent_t t1) {
   if (w.force_repair) return hipSuccess;  // every row takes the fallback
-  const dim3 grid((unsigned)((int64_t)w.nchunk * p.B * p.Hkv));
   void (*kern)(Params, Work);
-  if (p.K.paged) kern = p.group_shared ? k_score_stream<true, true> : k_score_stream<true, false>;
-  else kern = p.group_shared ? k_score_stream<false, true> : k_score_stream<false, false>;
-  return launch_with_events(kern, grid, p, w, st, t0, t1);
+  int64_t wgs;
+  if (stream_by_head_quads(w)) {
+    kern = p.group_shared ? k_score_stream<true, true, true> : k_score_stream<true, false, true>;
+    wgs = (int64_t)w.nchunk * p.B * (p.Hkv / kWaves);
+  } else if (p.K.paged) {
+    kern = p.group_shared ? k_score_stream<true, true, false> : k_score_stream<true, false, false>;
+    wgs = (int64_t)w.nchunk * p.B * p.Hkv;
+  } else {
+    kern = p.group_shared ? k_score_stream<false, true, false> : k_score_stream<false, false, false>;
+    wgs = (int64_t)w.nchunk * p.B * p.Hkv;
+  }
+  return launch_with_events(kern, dim3((unsigned)wgs), p, w, st, t0, t1);
 }
 
 size_t select_lds_bytes(int nchunk, int lds_cap) {

@@ -8,6 +8,10 @@
 namespace sd {
 
 hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st);
+// True when the workspace was laid out for the scoring stream to run one KV
+// head per wave over shared chunks of wave_keys keys (paged layout with a
+// multiple of 4 KV heads); blocks are then kCandBuf entries.
+bool stream_by_head_quads(const Work &w);
 // t0/t1 (both or neither): events recorded at the scoring kernel's start and
 // end, attached to its dispatch.
 hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st,

@@ -256,6 +256,17 @@ def test_head_groupings(sd, Hq, Hkv):
     check_fused(inp, out, idx, label=f"{Hq}q/{Hkv}kv")
 
 
+@pytest.mark.parametrize("Hq,Hkv,shared", [(8, 1, False), (8, 2, False), (16, 4, False),
+                                            (24, 12, False), (8, 2, True), (16, 4, True)])
+def test_paged_head_counts(sd, Hq, Hkv, shared):
+    # Paged caches are scored one KV head per wave, four heads per workgroup,
+    # when Hkv is a multiple of 4, else one head per workgroup; both paths.
+    inp = make("w4", seed=17, B=3, lmin=2000, lmax=20000, N=20000, Hq=Hq, Hkv=Hkv,
+               group_shared=shared)
+    out, idx, _ = gpu_fused(sd, inp)
+    check_fused(inp, out, idx, label=f"paged {Hq}q/{Hkv}kv shared={shared}")
+
+
 @pytest.mark.parametrize("G", [1, 4, 16])
 def test_group_shared_mode_group_sizes(sd, G):
     inp = make("w5", seed=9, N=20000, Hq=2 * G, Hkv=2)
