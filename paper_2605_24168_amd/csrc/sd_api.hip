@@ -464,8 +464,11 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   auto mark = [&](int i) -> hipError_t {
     return prof_level == 1 ? hipEventRecord(ev[i], stream_h) : hipSuccess;
   };
-  // Candidate keys the selection stages in LDS (about 2.5 k expected).
-  int64_t want = 4 * k_max + 1024;
+  // Candidate keys the selection stages in LDS.  About 2.5 k are expected
+  // and the count varies by about 1/sqrt(r) (r >= 2.5 k m / L sample ranks,
+  // at least 50 at the budgets this serves), so 3.5 k + 1024 is more than
+  // five deviations of room; rows beyond it select from global memory.
+  const int64_t want = 7 * k_max / 2 + 1024;
   const size_t pre_bytes = sd::select_lds_bytes(L.nchunk, 0);
   const size_t budget = sd::select_lds_budget(p);
   if (pre_bytes >= budget) return SD_ERR_UNSUPPORTED;

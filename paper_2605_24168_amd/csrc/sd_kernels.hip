@@ -154,7 +154,7 @@ __device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, ui
   for (int base = 0; base < n; base += NT) {
     const int i = base + tid;
     const uint32_t key = i < n ? keys[i] : kmin;
-    hist_add(hist, (uint32_t)bucket(key), i < n);
+    if (i < n) atomicAdd(&hist[bucket(key)], 1u);  // buckets spread the items
   }
   __syncthreads();
   // Thread t owns buckets [nb - (t+1)*bpt, nb - t*bpt), counted from the top.
