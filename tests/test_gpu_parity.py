@@ -234,9 +234,12 @@ def test_contiguous_and_paged_layouts_agree(sd):
 # ---------------------------------------------------------------------------
 
 def test_ragged_contiguous_batch_with_empty_and_tiny_sequences(sd):
-    # Lengths 0, 1, 15, 17, a full tile multiple, and ones crossing a
-    # scoring-workgroup boundary; positions beyond each length hold poison.
-    inp = synth.make_inputs(2, seq_lens=[0, 1, 15, 17, 4096, 8193, 12000], ncap=12011)
+    # Lengths 0, 1, 15, 17, full tile multiples, ones at and across the
+    # scoring-wave (2048) and scoring-workgroup (8192) boundaries, and a
+    # capacity that is not a tile multiple; positions beyond each length
+    # hold poison.
+    inp = synth.make_inputs(2, seq_lens=[0, 1, 15, 17, 2047, 2048, 2049, 4096, 8191, 8192, 8193,
+                                         12000], ncap=12011)
     out, idx, _ = gpu_fused(sd, inp)
     check_fused(inp, out, idx, label="ragged bhnd")
     assert (idx[0] == -1).all() and (out[0] == 0).all()
