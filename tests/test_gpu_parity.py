@@ -289,10 +289,11 @@ def test_long_candidate_lists(sd, name, ratio):
 
 
 def test_clustered_candidates_overflow_to_the_exact_fallback(sd):
-    # 400 consecutive keys close to head 0's query direction: all of them
-    # pass head 0's threshold inside one scoring wave, more than its staging
-    # area holds, so the row must take the exact fallback.
-    inp = make("w2", seed=15, B=1, N=12000, ratio=50.0)
+    # 400 consecutive keys close to head 0's query direction: with 8 heads
+    # per group a row's staging area holds 128 keys per scoring wave (of at
+    # least 256 keys), and the cluster puts more than that into one wave, so
+    # the row must take the exact fallback.
+    inp = make("w2", seed=15, B=1, N=12000, ratio=50.0, Hq=64, Hkv=8)
     rng = np.random.default_rng(15)
     q0 = synth.bf16_to_f32(inp.q[0, 0]).astype(np.float64)
     base = 3.0 * q0 / np.linalg.norm(q0) * np.sqrt(inp.d)
