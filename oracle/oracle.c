@@ -317,11 +317,16 @@ int32_t oracle_select_f32(int B, int R, int64_t ncap, const float *scores,
  * Softmax attention of one query head over a given set of positions
  * (scaled dot-product attention restricted to the set).  z_j = scale*(q.k_j),
  * w_j = exp(z_j - max z) / sum exp(z - max z), o = sum_j w_j v_j.
- * absw[i] = sum_j w_j |v_j[i]| (the magnitude of the summed terms, used by
- * the tests to scale floating-point tolerances).  An empty set gives o = 0.
+ * With per-position weights omega (Section 4: the sparse backend attends
+ * given the index set and associated weights; the formula is not given, and
+ * the reading here is that omega_j >= 0 multiplies exp(z_j - max z) in both
+ * the numerator and the normaliser): w_j = omega_j exp(z_j - max z) /
+ * sum omega exp(z - max z).  absw[i] = sum_j w_j |v_j[i]| (the magnitude of
+ * the summed terms, used by the tests to scale floating-point tolerances).
+ * An empty set, or weights summing to zero, gives o = 0.
  */
 static void attend_head(const problem *p, int b, int h, double scale,
-                        const int32_t *set, int64_t k, double *qbuf,
+                        const int32_t *set, const float *omega, int64_t k, double *qbuf,
                         double *kbuf, double *z, double *o, double *absw) {
   int G = p->Hq / p->Hkv;
   int g = h / G;
@@ -336,7 +341,12 @@ static void attend_head(const problem *p, int b, int h, double scale,
     if (z[t] > m) m = z[t];
   }
   double Z = 0.0;
-  for (int64_t t = 0; t < k; ++t) { z[t] = exp(z[t] - m); Z += z[t]; }
+  for (int64_t t = 0; t < k; ++t) {
+    z[t] = exp(z[t] - m);
+    if (omega) z[t] *= (double)omega[t];
+    Z += z[t];
+  }
+  if (!(Z > 0.0)) return;
   for (int64_t t = 0; t < k; ++t) {
     double w = z[t] / Z;
     load_vec(p->V->data, p->V->dtype, cache_row_offset(p->V, p->Hkv, d, b, g, set[t]), d, kbuf);
@@ -351,14 +361,15 @@ static void attend_head(const problem *p, int b, int h, double scale,
  * Attention over caller-given index sets idx[b][row][0..k_max), each row
  * holding its positions followed by -1 padding (rows are query heads, or KV
  * heads in group-shared mode, where each query head of the group uses the
- * group's set).  out and absw are [B][Hq][d] doubles.
+ * group's set).  weights: nullable float [B][R][k_max] aligned with idx (the
+ * weighted form above; must be >= 0 and finite).  out and absw are
+ * [B][Hq][d] doubles.
  */
-int32_t oracle_attend(int B, int Hq, int Hkv, int d, const void *q,
-                      int32_t q_dtype, const oracle_cache *K,
-                      const oracle_cache *V, const int32_t *seq_lens,
-                      int32_t group_shared, double scale, int64_t k_max,
-                      const int32_t *idx, double *out, double *absw,
-                      int nthreads) {
+static int32_t attend_sets(int B, int Hq, int Hkv, int d, const void *q, int32_t q_dtype,
+                           const oracle_cache *K, const oracle_cache *V,
+                           const int32_t *seq_lens, int32_t group_shared, double scale,
+                           int64_t k_max, const int32_t *idx, const float *weights,
+                           double *out, double *absw, int nthreads) {
   problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared);
   int rc = check_problem(&p, 1);
   if (rc) return rc;
@@ -372,6 +383,10 @@ int32_t oracle_attend(int B, int Hq, int Hkv, int d, const void *q,
       int32_t j = idx[r * k_max + t];
       if (j == -1) break;
       if (j < 0 || j >= seq_lens[b]) return ORACLE_EINVAL;
+      if (weights) {
+        float wv = weights[r * k_max + t];
+        if (!(wv >= 0.0f) || isinf(wv)) return ORACLE_EINVAL;
+      }
     }
   }
   set_threads(nthreads);
@@ -381,15 +396,38 @@ int32_t oracle_attend(int B, int Hq, int Hkv, int d, const void *q,
     int b = (int)(bh / Hq), h = (int)(bh % Hq);
     int row = group_shared ? h / G : h;
     const int32_t *set = idx + ((int64_t)b * R + row) * k_max;
+    const float *omega = weights ? weights + ((int64_t)b * R + row) * k_max : NULL;
     int64_t k = 0;
     while (k < k_max && set[k] != -1) ++k;
     double *buf = (double *)malloc(sizeof(double) * (size_t)(2 * d + (k > 0 ? k : 1)));
     if (!buf) { failed = 1; continue; }
-    attend_head(&p, b, h, scale, set, k, buf, buf + d, buf + 2 * d, out + bh * d,
+    attend_head(&p, b, h, scale, set, omega, k, buf, buf + d, buf + 2 * d, out + bh * d,
                 absw ? absw + bh * d : NULL);
     free(buf);
   }
   return failed ? ORACLE_ENOMEM : ORACLE_OK;
+}
+
+int32_t oracle_attend(int B, int Hq, int Hkv, int d, const void *q,
+                      int32_t q_dtype, const oracle_cache *K,
+                      const oracle_cache *V, const int32_t *seq_lens,
+                      int32_t group_shared, double scale, int64_t k_max,
+                      const int32_t *idx, double *out, double *absw,
+                      int nthreads) {
+  return attend_sets(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared, scale, k_max, idx,
+                     NULL, out, absw, nthreads);
+}
+
+/* The weighted form (Section 4's sparse backend: index sets and weights). */
+int32_t oracle_attend_weighted(int B, int Hq, int Hkv, int d, const void *q,
+                               int32_t q_dtype, const oracle_cache *K,
+                               const oracle_cache *V, const int32_t *seq_lens,
+                               int32_t group_shared, double scale, int64_t k_max,
+                               const int32_t *idx, const float *weights, double *out,
+                               double *absw, int nthreads) {
+  if (!weights) return ORACLE_EINVAL;
+  return attend_sets(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared, scale, k_max, idx,
+                     weights, out, absw, nthreads);
 }
 
 /*

@@ -59,6 +59,11 @@ def lib() -> C.CDLL:
                                     C.c_double, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
                                     C.c_int]
         L.oracle_sparse_attention.restype = C.c_int32
+        L.oracle_attend_weighted.restype = C.c_int32
+        L.oracle_attend_weighted.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p,
+                                             C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                             C.c_int32, C.c_double, C.c_int64, C.c_void_p,
+                                             C.c_void_p, C.c_void_p, C.c_void_p, C.c_int]
         L.oracle_sparse_attention.argtypes = [
             C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int32, C.POINTER(_Cache),
             C.POINTER(_Cache), C.c_void_p, C.c_double, C.c_int32, C.c_int32, C.c_double,
@@ -181,6 +186,30 @@ def attend(inp, idx: np.ndarray, scale: float = 0.0, nthreads: int = 0):
                                _dtype_code(inp.dtype), C.byref(K), C.byref(V), lens.ctypes.data,
                                int(inp.group_shared), float(scale), ix.shape[2], ix.ctypes.data,
                                out.ctypes.data, absw.ctypes.data, nthreads), "attend")
+    return out, absw
+
+
+def attend_weighted(inp, idx: np.ndarray, weights: np.ndarray, scale: float = 0.0,
+                    nthreads: int = 0):
+    """Weighted softmax attention over given index sets: weights [B, R, k_max]
+    (float32, >= 0) aligned with idx; returns (out, absw) in float64."""
+    keep: list = []
+    K = _cache(inp, inp.k, keep)
+    V = _cache(inp, inp.v, keep)
+    q = np.ascontiguousarray(inp.q)
+    lens = np.ascontiguousarray(inp.seq_lens, dtype=np.int32)
+    ix = np.ascontiguousarray(idx, dtype=np.int32)
+    wt = np.ascontiguousarray(weights, dtype=np.float32)
+    if wt.shape != ix.shape:
+        raise ValueError("weights must have the shape of idx")
+    out = np.empty((inp.B, inp.Hq, inp.d), dtype=np.float64)
+    absw = np.empty_like(out)
+    _check(lib().oracle_attend_weighted(inp.B, inp.Hq, inp.Hkv, inp.d, q.ctypes.data,
+                                        _dtype_code(inp.dtype), C.byref(K), C.byref(V),
+                                        lens.ctypes.data, int(inp.group_shared), float(scale),
+                                        ix.shape[2], ix.ctypes.data, wt.ctypes.data,
+                                        out.ctypes.data, absw.ctypes.data, nthreads),
+           "attend_weighted")
     return out, absw
 
 

@@ -276,6 +276,65 @@ def test_softmax_weights_sum_to_one_and_output_in_hull():
             assert (r2["absw"][b, h] >= np.abs(r2["out"][b, h]) - 1e-12).all()
 
 
+# --------------------------------------------------------------------------
+# Weighted attention over given sets (Section 4: the sparse backend attends
+# given the index set and associated weights; reading: w_j proportional to
+# omega_j exp(z_j)).  Pinned to a library routine: scaled dot-product
+# attention with the additive mask log(omega).
+# --------------------------------------------------------------------------
+
+def _random_sets(rng, B, R, N, k):
+    idx = np.stack([np.stack([np.sort(rng.choice(N, size=k, replace=False)) for _ in range(R)])
+                    for _ in range(B)]).astype(np.int32)
+    return idx
+
+
+def test_weighted_attention_is_sdpa_with_log_weight_mask():
+    rng = np.random.default_rng(21)
+    B, Hq, Hkv, N, d, k = 2, 4, 2, 40, 16, 9
+    q = rng.standard_normal((B, Hq, d)).astype(np.float32)
+    K = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    V = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    p = problem(q, K, V, Hkv=Hkv)
+    idx = _random_sets(rng, B, Hq, N, k)
+    w = rng.uniform(0.05, 3.0, size=idx.shape).astype(np.float32)
+    out, _ = O.attend_weighted(p, idx, w)
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hq):
+            S = idx[b, h]
+            kt = torch.from_numpy(K[b, h // G, S].astype(np.float64))[None, None]
+            vt = torch.from_numpy(V[b, h // G, S].astype(np.float64))[None, None]
+            qt = torch.from_numpy(q[b, h].astype(np.float64))[None, None, None]
+            mask = torch.from_numpy(np.log(w[b, h].astype(np.float64)))[None, None, None]
+            ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, attn_mask=mask)
+            np.testing.assert_allclose(out[b, h], ref[0, 0, 0].numpy(), rtol=0, atol=1e-12)
+
+
+def test_weighted_attention_special_cases():
+    rng = np.random.default_rng(22)
+    B, Hq, N, d, k = 1, 3, 30, 8, 6
+    q = rng.standard_normal((B, Hq, d)).astype(np.float32)
+    K = rng.standard_normal((N, d)).astype(np.float32)
+    V = rng.standard_normal((N, d)).astype(np.float32)
+    p = problem(q, np.broadcast_to(K, (1, 1, N, d)), np.broadcast_to(V, (1, 1, N, d)))
+    idx = _random_sets(rng, B, Hq, N, k)
+    plain, _ = O.attend(p, idx)
+    ones, _ = O.attend_weighted(p, idx, np.ones(idx.shape, np.float32))
+    np.testing.assert_array_equal(ones, plain)                       # weights 1: unweighted
+    const, _ = O.attend_weighted(p, idx, np.full(idx.shape, 7.5, np.float32))
+    np.testing.assert_allclose(const, plain, rtol=0, atol=1e-13)     # scale invariant
+    hot = np.zeros(idx.shape, np.float32)
+    hot[..., 2] = 1.0                                                # one position kept
+    one, _ = O.attend_weighted(p, idx, hot)
+    for h in range(Hq):
+        np.testing.assert_array_equal(one[0, h], V[idx[0, h, 2]].astype(np.float64))
+    zero, _ = O.attend_weighted(p, idx, np.zeros(idx.shape, np.float32))
+    assert (zero == 0).all()                                         # no weight: zero output
+    with pytest.raises(RuntimeError):
+        O.attend_weighted(p, idx, -hot)                              # negative weights rejected
+
+
 def test_empty_sequence_gives_zero_output_and_no_indices():
     rng = np.random.default_rng(8)
     q = rng.standard_normal((2, 2, 8))

@@ -37,6 +37,9 @@ MUTANTS = {
     "indices_left_in_score_order": ("qsort(idx, (size_t)k, sizeof(int32_t), by_int32_asc);", ""),
     "value_row_from_key_cache": ("load_vec(p->V->data, p->V->dtype, cache_row_offset(p->V,",
                                  "load_vec(p->K->data, p->K->dtype, cache_row_offset(p->K,"),
+    "weights_squared": ("if (omega) z[t] *= (double)omega[t];",
+                        "if (omega) z[t] *= (double)omega[t] * (double)omega[t];"),
+    "weights_ignored": ("if (omega) z[t] *= (double)omega[t];", "if (omega) z[t] *= 1.0;"),
     "row_scores_skip_last_position": ("for (int64_t j = 0; j < L; ++j) {\n    load_vec(p->K->data",
                                       "for (int64_t j = 0; j + 1 < L; ++j) {\n    load_vec(p->K->data"),
 }
