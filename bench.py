@@ -96,6 +96,133 @@ def cpu_baseline(inp, n_seq):
                       f"score+select+attend in float64, {dt:.2f} s wall"}
 
 
+# Table 1 of the paper (H100 80GB HBM3, FP16, GQA 32/8, d 128, page 16, NHD,
+# 128K context): FlashInfer dense decode ms per batch size and the sparse
+# backend's speedup over it per sparsity.  Context for the MI355X sweep, not
+# a target of the same hardware.
+TABLE1_RATIOS = [2, 4, 10, 20, 50, 100, 200, 500]
+TABLE1_H100 = {
+    1: (0.19, [0.32, 0.63, 1.45, 2.58, 5.57, 10.25, 11.05, 11.14]),
+    4: (0.72, [0.33, 0.66, 1.64, 3.18, 7.45, 13.36, 24.25, 42.04]),
+    8: (1.50, [0.38, 0.77, 1.90, 3.75, 8.88, 16.82, 29.64, 76.14]),
+    16: (3.08, [0.45, 0.89, 2.21, 4.35, 10.54, 20.09, 37.32, 76.77]),
+}
+
+
+def time_calls(torch, fn, steps, warmup):
+    """Mean ms per call over `steps` calls after `warmup`, by events on the
+    current stream around the whole run (no event between calls)."""
+    for _ in range(warmup):
+        fn()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def time_graph(torch, fn, steps, warmup):
+    """Mean ms per call with `steps` calls captured in one HIP graph and
+    replayed (kernel time without the host's per-call work); also returns
+    whether the replay left the same output as the eager calls.  fn() returns
+    its output tensor."""
+    for _ in range(warmup):  # eager: also sizes the library workspace before capture
+        ref = fn()
+    torch.cuda.synchronize()
+    ref = ref.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(steps):
+            out = fn()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(out, ref))
+    del g
+    return e0.elapsed_time(e1) / steps, same
+
+
+def backend_table(args):
+    """Table 1's shape on one MI355X: dense decode attention against the
+    weighted sparse backend on irregular index lists, batch 1/4/8/16, 128K
+    context, GQA 32/8, paged NHD (page 16), bfloat16.  Prints one JSON line."""
+    import torch
+    from paper_2605_24168_amd import sparse_decode as sd
+    from paper_2605_24168_amd import synth
+
+    torch.cuda.set_device(0)
+    N, Hq, Hkv, d = 131072, 32, 8, 128
+    batches = [1, 4, 8, 16]
+    log("drawing the 16 x 128K paged cache on the GPU")
+    t = synth.backend_sweep_inputs(B=max(batches), N=N, Hq=Hq, Hkv=Hkv, seed=args.seed)
+    torch.cuda.synchronize()
+    rows = []
+    for B in batches:
+        q = t["q"][:B].contiguous()
+        cache = sd.KVCache(k=t["k"], v=t["v"], layout="paged",
+                           block_table=t["block_table"][:B].contiguous())
+        lens = t["seq_lens"][:B].contiguous()
+        out = torch.empty_like(q)
+        dense_fn = lambda: sd.sparse_decode_dense_attention(q, cache, lens, out=out)
+        dense_eager = time_calls(torch, dense_fn, args.steps, args.warmup)
+        dense_ms, same = time_graph(torch, dense_fn, args.steps, args.warmup)
+        dense_bytes = B * Hkv * N * d * 2 * 2 + 2 * B * Hq * d * 2
+        entry = {"batch": B, "dense_ms": round(dense_ms, 4), "dense_eager_ms": round(dense_eager, 4),
+                 "dense_GBps": round(dense_bytes / (dense_ms * 1e-3) / 1e9, 1),
+                 "dense_frac_of_peak": round(dense_bytes / (dense_ms * 1e-3) / 1e9
+                                             / HBM_PEAK_GBPS, 4),
+                 "graph_replay_matches_eager": same,
+                 "h100_flashinfer_ms": TABLE1_H100[B][0], "sparse": {}}
+        log(f"B={B}: dense {dense_ms:.4f} ms ({entry['dense_GBps']} GB/s), "
+            f"eager {dense_eager:.4f} ms")
+        for i, S in enumerate(TABLE1_RATIOS):
+            k = int(round(N / S))
+            idx, w = synth.backend_sweep_sets(B * Hq, N, k, seed=args.seed)
+            idx, w = idx.view(B, Hq, k), w.view(B, Hq, k)
+            sp = sd.Sparsity(ratio=float(S))
+            fn = lambda: sd.sparse_decode_attend_weighted(q, cache, lens, idx, w, sp, out=out)
+            eager = time_calls(torch, fn, args.steps, args.warmup)
+            ms, same = time_graph(torch, fn, args.steps, args.warmup)
+            sparse_bytes = B * Hq * k * (2 * d * 2 + 8) + 2 * B * Hq * d * 2
+            entry["graph_replay_matches_eager"] &= same
+            entry["sparse"][f"{S}x"] = {
+                "k": k, "ms": round(ms, 4), "eager_ms": round(eager, 4),
+                "speedup": round(dense_ms / ms, 3),
+                "eager_speedup": round(dense_eager / eager, 3),
+                "GBps": round(sparse_bytes / (ms * 1e-3) / 1e9, 1),
+                "h100_speedup": TABLE1_H100[B][1][i]}
+            log(f"  {S}x (k={k}): {ms:.4f} ms (eager {eager:.4f}), speedup {dense_ms / ms:.2f}x "
+                f"(H100: {TABLE1_H100[B][1][i]}x)")
+            del idx, w
+        rows.append(entry)
+    rec = {
+        "table": "sparse backend vs dense decode (Table 1 shape)",
+        "steps": args.steps, "warmup": args.warmup,
+        "config": {"q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "context": N,
+                   "layout": "paged NHD, page 16, random page order", "dtype": "bf16",
+                   "index_lists": "uniform random distinct positions per query head, "
+                                  "weights U[0.05, 3)"},
+        "timing": "ms: K calls captured in one HIP graph and replayed, events around the "
+                  "replay (kernel time, as a kernel benchmark measures it); eager_ms: K calls "
+                  "back to back through the Python binding (adds its per-call host work)",
+        "dense_bytes": "all K and V rows of the batch",
+        "sparse_bytes": "per query head and kept position one K and one V row (256 B each), "
+                        "its index and weight",
+        "rows": rows,
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,12 +235,19 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device to device once (a plain "
                          "copy of known size that scales hardware traffic counters)")
+    ap.add_argument("--table1", action="store_true",
+                    help="instead of the default line, sweep dense decode against the "
+                         "weighted sparse backend in Table 1's shape (batch 1/4/8/16, "
+                         "2x-500x, 128K, GQA 32/8, paged)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the method's data-parallel shards (sequences or KV "
               "heads) need no exchange, so only --gpus 1 is supported", file=sys.stderr)
         sys.exit(2)
+    if args.table1:
+        backend_table(args)
+        return
 
     import torch
     from oracle import oracle as O
@@ -177,6 +311,19 @@ def main():
     sd.set_profiling(False)
     prof = sd.profile_mean()
 
+    # Dense decode attention over the same cache: the full-attention baseline.
+    dense = None
+    if inp.dtype == "bf16" and inp.G <= 8:
+        log(f"timing dense decode attention over {args.steps} steps")
+        dense_ms = time_calls(torch, lambda: sd.sparse_decode_dense_attention(q, cache, lens,
+                                                                              out=out),
+                              args.steps, args.warmup)
+        dense_b = sum(int(L) for L in inp.seq_lens) * inp.Hkv * inp.d * 2 * 2
+        dense = {"ms_per_step": dense_ms,
+                 "GBps": dense_b / (dense_ms * 1e-3) / 1e9,
+                 "frac_of_peak": dense_b / (dense_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                 "sparse_speedup": dense_ms / ms_step}
+
     key_b, gather_b, small_b = path_bytes(inp, ks)
     total_b = key_b + gather_b + small_b
     path_gbps = total_b / (ms_step * 1e-3) / 1e9
@@ -230,6 +377,7 @@ def main():
                           "total_ms")},
             "repaired_rows_last_step": prof["repaired_rows"],
         },
+        "dense_baseline": dense,
     }
     del q, cache, lens, out, idx, ws
     if args.copy_mib > 0:

@@ -145,6 +145,41 @@ sd_status sparse_decode_attend(const sd_tensor *q, const sd_kv *K, const sd_kv *
                                const sd_sparsity *sparsity, sd_tensor *out, void *stream);
 
 /*
+ * Weighted attention restricted to given positions (Section 4: the paper's
+ * sparse backend attends a given sparse index list together with a weight
+ * per index).  As sparse_decode_attend, with entry t of row (b, r) carrying
+ * the weight omega = weights[b, r, t]: out[b, h] = sum_j w_j V_j with
+ * w_j = omega_j exp(z_j - m) / sum over the row's usable entries of
+ * omega exp(z - m), i.e. softmax attention with log(omega) added to each
+ * logit.  Weights must be finite and >= 0 (others give undefined, memory-safe
+ * results); an entry of weight 0 is skipped, and a row whose usable weights
+ * are all 0 gives zeros.  All ones reproduce sparse_decode_attend.
+ *   weights f32 [B, R, k_max], the shape of idx
+ *   out     [B, Hq, 128], dtype of q
+ */
+sd_status sparse_decode_attend_weighted(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                        const int32_t *seq_lens, const sd_tensor *idx,
+                                        const sd_tensor *weights, const sd_sparsity *sparsity,
+                                        sd_tensor *out, void *stream);
+
+/*
+ * Dense decode attention over every cached position: out[b, h] =
+ * sum_{j < L_b} softmax(z)_j V_j with z_j = scale * q_h . K_j, the
+ * full-attention baseline that Table 1 measures the sparse backend against
+ * (it reads all of K and V).  A sequence with L_b = 0 gives zeros.
+ *   q [B, Hq, 128] bfloat16; K, V bfloat16 caches of one layout
+ *   (float32, or more than 8 query heads per KV head, returns
+ *   SD_ERR_UNSUPPORTED)
+ *   softmax_scale > 0, or <= 0 for 1/sqrt(128)
+ *   out [B, Hq, 128] bfloat16
+ * Uses the library workspace: sparse_decode_dense_workspace_size bytes.
+ */
+sd_status sparse_decode_dense_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                        const int32_t *seq_lens, float softmax_scale,
+                                        sd_tensor *out, void *stream);
+sd_status sparse_decode_dense_workspace_size(const sd_tensor *q, const sd_kv *K, size_t *bytes);
+
+/*
  * The whole decode-step method fused: score every cached key, keep the exact
  * top-k per row, attend over the kept rows.  Results equal
  * sparse_decode_score -> sparse_decode_topk -> sparse_decode_attend, except

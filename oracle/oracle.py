@@ -213,6 +213,35 @@ def attend_weighted(inp, idx: np.ndarray, weights: np.ndarray, scale: float = 0.
     return out, absw
 
 
+def dense_attention(inp, scale: float = 0.0, nthreads: int = 0, batch=None):
+    """Dense decode attention over every position j < L_b (Table 1's
+    full-attention baseline): attention over the index set of all positions.
+    batch: optional list of sequences to compute (others are left as NaN).
+    Returns out [B, Hq, d] float64."""
+    out = np.full((inp.B, inp.Hq, inp.d), np.nan)
+    for b in (range(inp.B) if batch is None else batch):
+        sub = _one_sequence(inp, b)
+        L = int(inp.seq_lens[b])
+        idx = np.broadcast_to(np.arange(max(L, 1), dtype=np.int32) if L else
+                              np.full(1, -1, np.int32), (1, sub.rows, max(L, 1)))
+        out[b], _ = attend(sub, np.ascontiguousarray(idx), scale, nthreads)
+    return out
+
+
+def _one_sequence(inp, b: int):
+    """Sequence b of a decode step as a batch of one (views, no copies of the cache)."""
+    import copy
+    one = copy.copy(inp)
+    one.B = 1
+    one.q = inp.q[b:b + 1]
+    one.seq_lens = np.asarray(inp.seq_lens)[b:b + 1]
+    if inp.layout == "paged":
+        one.block_table = inp.block_table[b:b + 1]
+    else:
+        one.k, one.v = inp.k[b:b + 1], inp.v[b:b + 1]
+    return one
+
+
 def sparse_attention(inp, k_max: int | None = None, k_override=None, scale: float = 0.0,
                      nthreads: int = 0) -> dict:
     """The whole method: returns dict(idx, tau, out, absw)."""

@@ -237,6 +237,21 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
 
 sd_status hip_status(hipError_t e) { return e == hipSuccess ? SD_OK : SD_ERR_HIP; }
 
+// The sparsity fields the dense path reads: none but the softmax scale.
+sd_sparsity dense_sparsity(float softmax_scale) {
+  sd_sparsity sp{};
+  sp.ratio = 1.0;
+  sp.softmax_scale = softmax_scale;
+  return sp;
+}
+
+// Partials of the dense decode kernels (at least one aligned unit).
+size_t dense_part_bytes(const sd::Params &p) {
+  const int wk = sd::dense_wave_keys(p);
+  const size_t n = (size_t)p.B * p.Hq * sd::dense_nsplit(p, wk) * sd::kPartStride * 4;
+  return align_up(n > 0 ? n : 1);
+}
+
 // The current device's workspace, at least `bytes` long.
 sd_status get_workspace(size_t bytes, DevState *&ds, char *&base) {
   int dev = 0;
@@ -421,6 +436,78 @@ sd_status sparse_decode_attend(const sd_tensor *q, const sd_kv *K, const sd_kv *
   const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   return hip_status(sd::launch_attend(p, w, (const int32_t *)idx->data, out->data, false,
                                       (hipStream_t)stream));
+}
+
+sd_status sparse_decode_attend_weighted(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                        const int32_t *seq_lens, const sd_tensor *idx,
+                                        const sd_tensor *weights, const sd_sparsity *sp,
+                                        sd_tensor *out, void *stream) {
+  Shape s{};
+  sd_status st = check_problem(q, K, V, sp, s);
+  if (st) return st;
+  if (!V) return SD_ERR_INVALID_ARG;
+  if (!idx || idx->ndim != 3 || idx->dtype != SD_I32 || idx->shape[0] != s.B ||
+      idx->shape[1] != s.R || idx->shape[2] < 0)
+    return SD_ERR_INVALID_ARG;
+  const int64_t k_max = idx->shape[2];
+  if (k_max > INT32_MAX / 2) return SD_ERR_UNSUPPORTED;
+  if (!weights || weights->ndim != 3 || weights->dtype != SD_F32)
+    return SD_ERR_INVALID_ARG;
+  for (int i = 0; i < 3; ++i)
+    if (weights->shape[i] != idx->shape[i]) return SD_ERR_INVALID_ARG;
+  st = check_out(out, s, q->dtype);
+  if (st) return st;
+  if (s.B == 0) return SD_OK;
+  if (!seq_lens || (k_max > 0 && (!idx->data || !weights->data))) return SD_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lk(g_mu);
+  const Layout L = layout_for(s, k_max, false, sp);
+  DevState *ds = nullptr;
+  char *base = nullptr;
+  st = get_workspace(L.total, ds, base);
+  if (st) return st;
+  const sd::Work w = carve(base, L, false);
+  sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
+  p.weights = (const float *)weights->data;
+  return hip_status(sd::launch_attend(p, w, (const int32_t *)idx->data, out->data, false,
+                                      (hipStream_t)stream));
+}
+
+sd_status sparse_decode_dense_workspace_size(const sd_tensor *q, const sd_kv *K, size_t *bytes) {
+  if (!bytes) return SD_ERR_INVALID_ARG;
+  const sd_sparsity sp = dense_sparsity(0.f);
+  Shape s{};
+  sd_status st = check_problem(q, K, nullptr, &sp, s);
+  if (st) return st;
+  if (!s.bf16 || s.G > sd::kDenseMaxGroup) return SD_ERR_UNSUPPORTED;
+  const sd::Params p = make_params(q, K, nullptr, nullptr, &sp, s, 0);
+  *bytes = dense_part_bytes(p);
+  return SD_OK;
+}
+
+sd_status sparse_decode_dense_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                        const int32_t *seq_lens, float softmax_scale,
+                                        sd_tensor *out, void *stream) {
+  const sd_sparsity sp = dense_sparsity(softmax_scale);
+  Shape s{};
+  sd_status st = check_problem(q, K, V, &sp, s);
+  if (st) return st;
+  if (!V) return SD_ERR_INVALID_ARG;
+  if (!s.bf16 || s.G > sd::kDenseMaxGroup) return SD_ERR_UNSUPPORTED;
+  st = check_out(out, s, q->dtype);
+  if (st) return st;
+  if (s.B == 0) return SD_OK;
+  if (!seq_lens) return SD_ERR_INVALID_ARG;
+  sd::Params p = make_params(q, K, V, seq_lens, &sp, s, 0);
+  sd::DenseWork dw{};
+  dw.wave_keys = sd::dense_wave_keys(p);
+  dw.nsplit = sd::dense_nsplit(p, dw.wave_keys);
+  std::lock_guard<std::mutex> lk(g_mu);
+  DevState *ds = nullptr;
+  char *base = nullptr;
+  st = get_workspace(dense_part_bytes(p), ds, base);
+  if (st) return st;
+  dw.part = (float *)base;
+  return hip_status(sd::launch_dense_attention(p, dw, out->data, (hipStream_t)stream));
 }
 
 sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,

@@ -23,6 +23,8 @@ constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
 constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the fallback scoring
 constexpr int kSelectWideRows = 256; // fewer rows: 1024-thread selection workgroups
+constexpr int kDenseWaveKeysMax = 8192; // keys per work item of the dense decode kernel
+constexpr int kDenseMaxGroup = 8;     // query heads per KV head of the dense decode kernel
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -53,6 +55,8 @@ struct Params {
   int32_t rounding;
   int32_t k_max;
   int64_t ncap;
+  const float *weights;        // [B, R, k_max] per-entry weights of the index
+                               // lists (weighted attention), or null
 };
 
 // Scratch carved from the library workspace (see the host orchestration).
@@ -76,6 +80,13 @@ struct Work {
   int32_t blk_cap;     // entries per packed block: kChunkCap, or kCandBuf
   int32_t nsplit;
   int32_t force_repair;  // every row takes the exact fallback
+};
+
+// Scratch of the dense decode kernels.
+struct DenseWork {
+  float *part;         // [B*Hq][nsplit][kPartStride] key-range partials
+  int32_t wave_keys;   // keys per work item (a multiple of kTile)
+  int32_t nsplit;      // key ranges per sequence: ceil(ncap / wave_keys)
 };
 
 // ---------------------------------------------------------------------------
@@ -413,6 +424,60 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
   }
   T = prefix;
   need_eq = krem;
+}
+
+// ---------------------------------------------------------------------------
+// Log-sum-exp merge of split partials.  pp points at nsp partials of one
+// output row, kPartStride floats apart, each (m, l, o[128]): a maximum m of
+// the split's logits, l = sum exp(z - m) and o = sum exp(z - m) v.  The merged
+// row is sum_q e^(m_q - M) o_q / sum_q e^(m_q - M) l_q with M = max m_q (zeros
+// when no split holds an entry).  Run by a block of kMergeThreads: the maxima
+// and scale factors in parallel, then each channel's sum over the partials by
+// the two halves of the block, several loads in flight per thread.  Returns
+// channel threadIdx.x & 127's value (meaningful where threadIdx.x < 128).
+// Every thread of the block must call it.
+// ---------------------------------------------------------------------------
+constexpr int kMergeThreads = 256;
+constexpr int kMergeChunk = 1024;  // partials whose scale factors sit in LDS at once
+
+struct MergeShared {
+  float f[kMergeChunk];
+  float red[kMergeThreads / 64];
+  float half_o[kHeadDim];
+};
+
+__device__ __forceinline__ float merge_partials(const float *pp, int nsp, MergeShared &sh) {
+  const int tid = threadIdx.x, c = tid & (kHeadDim - 1), half = tid >> 7;
+  float m = -__builtin_inff();
+  for (int q = tid; q < nsp; q += kMergeThreads) m = fmaxf(m, pp[(int64_t)q * kPartStride]);
+  const float M = block_max<kMergeThreads>(m, sh.red);
+  float ls = 0.f, o = 0.f;
+  for (int q0 = 0; q0 < nsp; q0 += kMergeChunk) {
+    const int n = (nsp - q0) < kMergeChunk ? (nsp - q0) : kMergeChunk;
+    const float *base = pp + (int64_t)q0 * kPartStride;
+    for (int q = tid; q < n; q += kMergeThreads) {
+      const float mq = base[(int64_t)q * kPartStride];
+      const float f = mq == -__builtin_inff() ? 0.f : expf(mq - M);
+      sh.f[q] = f;
+      ls += f * base[(int64_t)q * kPartStride + 1];
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int q = half; q < n; q += 2) o += sh.f[q] * base[(int64_t)q * kPartStride + 2 + c];
+    __syncthreads();
+  }
+  // Sum of the l terms over the block; the two halves' channel sums.
+  float t = ls;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) t += __shfl_xor(t, off);
+  if (lane_id() == 0) sh.red[wave_id()] = t;
+  if (half == 1) sh.half_o[c] = o;
+  __syncthreads();
+  float sum = 0.f;
+#pragma unroll
+  for (int w = 0; w < kMergeThreads / 64; ++w) sum += sh.red[w];
+  o += sh.half_o[c];
+  return sum > 0.f ? o / sum : 0.f;
 }
 
 // ---------------------------------------------------------------------------

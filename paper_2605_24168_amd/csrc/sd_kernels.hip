@@ -1073,10 +1073,22 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   __syncthreads();
   if (recompute) {
     // Per-head maxima: every wave reduces its share, one barrier, then
-    // thread h combines the waves.
+    // thread h combines the waves.  With per-entry weights omega the logit
+    // becomes z + log(omega), so that exp(z' - m) = omega * exp(z - m) and
+    // the maximum (shared by all splits through the merge) stays finite for
+    // any positive weights; an entry of weight 0 is skipped.
+    const float *wrow = p.weights ? p.weights + (int64_t)row * p.k_max + e0 : nullptr;
     for (int h = 0; h < nh; ++h) {
       float m = -__builtin_inff();
-      for (int t = tid; t < n; t += kBlock) m = fmaxf(m, e_l[h * split + t]);
+      for (int t = tid; t < n; t += kBlock) {
+        float z = e_l[h * split + t];
+        if (wrow) {
+          const float om = wrow[t];
+          z = om > 0.f ? z + logf(om) : -__builtin_inff();
+          e_l[h * split + t] = z;
+        }
+        m = fmaxf(m, z);
+      }
       m = wave_max(m);
       if (l == 0) hmax[wv][h] = m;
     }
@@ -1194,30 +1206,18 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   }
 }
 
-// Log-sum-exp merge of split partials: grid = B*Hq output rows, 128 threads
-// (one per channel).  Rows that fit one split were written by k_attend.
+// Log-sum-exp merge of split partials: grid = B*Hq output rows, blocks of
+// kMergeThreads.  Rows that fit one split were written by k_attend.
 template <bool BF16, bool FUSED>
-__global__ __launch_bounds__(kHeadDim) void k_merge(Params p, Work w, void *out, int split) {
-  const int bh = blockIdx.x, b = bh / p.Hq, h = bh % p.Hq;
-  const int r = p.group_shared ? h / p.G : h;
-  (void)r;
+__global__ __launch_bounds__(kMergeThreads) void k_merge(Params p, Work w, void *out, int split) {
+  __shared__ MergeShared sh;
+  const int bh = blockIdx.x, b = bh / p.Hq;
   const int L = seq_len(p, b);
   const int n_list = attend_list_len(p, b, L, FUSED);
   const int nsp = (n_list + split - 1) / split;
   if (nsp <= 1 || L == 0) return;  // written directly by k_attend
-  const int c = threadIdx.x;
-  const float *pp = w.part + (int64_t)bh * w.nsplit * kPartStride;
-  float M = -__builtin_inff();
-  for (int q = 0; q < nsp; ++q) M = fmaxf(M, pp[q * kPartStride]);
-  float o = 0.f, ls = 0.f;
-  if (M != -__builtin_inff()) {
-    for (int q = 0; q < nsp; ++q) {
-      const float f = expf(pp[q * kPartStride] - M);
-      ls += f * pp[q * kPartStride + 1];
-      o += f * pp[q * kPartStride + 2 + c];
-    }
-  }
-  store_out<BF16>(out, (int64_t)bh * kHeadDim + c, ls > 0.f ? o / ls : 0.f);
+  const float v = merge_partials(w.part + (int64_t)bh * w.nsplit * kPartStride, nsp, sh);
+  if (threadIdx.x < kHeadDim) store_out<BF16>(out, (int64_t)bh * kHeadDim + threadIdx.x, v);
 }
 
 // ---------------------------------------------------------------------------
@@ -1360,11 +1360,11 @@ hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, voi
   if (nsplit > 1) {
     const unsigned rows = (unsigned)(p.B * p.Hq);
     if (p.bf16) {
-      if (fused) k_merge<true, true><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
-      else k_merge<true, false><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
+      if (fused) k_merge<true, true><<<rows, kMergeThreads, 0, st>>>(p, w, out, split);
+      else k_merge<true, false><<<rows, kMergeThreads, 0, st>>>(p, w, out, split);
     } else {
-      if (fused) k_merge<false, true><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
-      else k_merge<false, false><<<rows, kHeadDim, 0, st>>>(p, w, out, split);
+      if (fused) k_merge<false, true><<<rows, kMergeThreads, 0, st>>>(p, w, out, split);
+      else k_merge<false, false><<<rows, kMergeThreads, 0, st>>>(p, w, out, split);
     }
   }
   return hipGetLastError();

@@ -28,5 +28,9 @@ int attend_nsplit(const Params &p);
 hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st);
 hipError_t launch_topk(const Params &p, const float *scores, int32_t *idx, float *vals,
                        hipStream_t st);
+// Dense decode attention over every position (bfloat16 caches).
+int dense_wave_keys(const Params &p);
+int dense_nsplit(const Params &p, int wave_keys);
+hipError_t launch_dense_attention(const Params &p, const DenseWork &dw, void *out, hipStream_t st);
 
 }  // namespace sd

@@ -9,6 +9,8 @@ names follow the C ABI in include/sparse_decode.h:
     sparse_decode_topk(scores, seq_lens, sparsity, k_max)    -> idx (, vals)
     sparse_decode_attend(q, cache, seq_lens, idx, sparsity)  -> out
     sparse_decode_attention(q, cache, seq_lens, sparsity)    -> (out, idx)
+    sparse_decode_attend_weighted(q, cache, seq_lens, idx, weights, sparsity) -> out
+    sparse_decode_dense_attention(q, cache, seq_lens)        -> out
 
 Importing this module raises if the library has not been built; nothing here
 falls back to another implementation.
@@ -68,6 +70,15 @@ lib.sparse_decode_topk.argtypes = [_P(SdTensor), C.c_void_p, _P(SdSparsity), _P(
 lib.sparse_decode_attend.restype = C.c_int
 lib.sparse_decode_attend.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p, _P(SdTensor),
                                      _P(SdSparsity), _P(SdTensor), C.c_void_p]
+lib.sparse_decode_attend_weighted.restype = C.c_int
+lib.sparse_decode_attend_weighted.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p,
+                                              _P(SdTensor), _P(SdTensor), _P(SdSparsity),
+                                              _P(SdTensor), C.c_void_p]
+lib.sparse_decode_dense_attention.restype = C.c_int
+lib.sparse_decode_dense_attention.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p,
+                                              C.c_float, _P(SdTensor), C.c_void_p]
+lib.sparse_decode_dense_workspace_size.restype = C.c_int
+lib.sparse_decode_dense_workspace_size.argtypes = [_P(SdTensor), _P(SdKv), _P(C.c_size_t)]
 lib.sparse_decode_attention.restype = C.c_int
 lib.sparse_decode_attention.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p,
                                         _P(SdSparsity), _P(SdTensor), _P(SdTensor), C.c_void_p]
@@ -249,6 +260,46 @@ def sparse_decode_attend(q, cache: KVCache, seq_lens, idx, sparsity: Sparsity, o
                                     C.byref(ci), C.byref(sp), C.byref(co), _stream(stream)),
            "sparse_decode_attend")
     return out
+
+
+def sparse_decode_attend_weighted(q, cache: KVCache, seq_lens, idx, weights, sparsity: Sparsity,
+                                  out=None, stream=None):
+    """Attention of each query head over its listed positions, entry t of a
+    row weighted by weights[b, r, t] (float32, the shape of idx)."""
+    _need_device(seq_lens, "seq_lens", torch.int32)
+    _need_device(weights, "weights", torch.float32)
+    if out is None:
+        out = torch.empty_like(q)
+    sp = sparsity.c()
+    cq, kk, kv = _tensor(q, "q"), cache.c("k"), cache.c("v")
+    ci, cw, co = _tensor(idx, "idx"), _tensor(weights, "weights"), _tensor(out, "out")
+    _check(lib.sparse_decode_attend_weighted(C.byref(cq), C.byref(kk), C.byref(kv),
+                                             seq_lens.data_ptr(), C.byref(ci), C.byref(cw),
+                                             C.byref(sp), C.byref(co), _stream(stream)),
+           "sparse_decode_attend_weighted")
+    return out
+
+
+def sparse_decode_dense_attention(q, cache: KVCache, seq_lens, softmax_scale: float = 0.0,
+                                  out=None, stream=None):
+    """Dense decode attention over every cached position (bfloat16)."""
+    _need_device(seq_lens, "seq_lens", torch.int32)
+    if out is None:
+        out = torch.empty_like(q)
+    cq, kk, kv, co = _tensor(q, "q"), cache.c("k"), cache.c("v"), _tensor(out, "out")
+    _check(lib.sparse_decode_dense_attention(C.byref(cq), C.byref(kk), C.byref(kv),
+                                             seq_lens.data_ptr(), float(softmax_scale),
+                                             C.byref(co), _stream(stream)),
+           "sparse_decode_dense_attention")
+    return out
+
+
+def dense_workspace_size(q, cache: KVCache) -> int:
+    n = C.c_size_t(0)
+    cq, kk = _tensor(q, "q"), cache.c("k")
+    _check(lib.sparse_decode_dense_workspace_size(C.byref(cq), C.byref(kk), C.byref(n)),
+           "sparse_decode_dense_workspace_size")
+    return int(n.value)
 
 
 def sparse_decode_attention(q, cache: KVCache, seq_lens, sparsity: Sparsity, out=None, idx=None,

@@ -41,7 +41,8 @@ PAGE_SIZE = 16
 ROOT_SEED = 260524168
 POISON = 64.0  # written to allocated-but-unused positions (never a valid key)
 
-TAG_Q, TAG_K, TAG_V, TAG_PLANT, TAG_SCALE, TAG_LENS, TAG_PAGES, TAG_CENTROID = range(8)
+(TAG_Q, TAG_K, TAG_V, TAG_PLANT, TAG_SCALE, TAG_LENS, TAG_PAGES, TAG_CENTROID, TAG_SETS,
+ TAG_WEIGHTS) = range(10)
 
 
 @dataclasses.dataclass
@@ -303,3 +304,74 @@ def make_inputs(cfg: int, seed: int = 0, *, B: Optional[int] = None, N: Optional
         seq_lens=lens, layout=s.layout, ncap=int(ncap), ratio=float(s.ratio),
         rounding=s.rounding, group_shared=bool(s.group_shared), page_size=PAGE_SIZE,
         block_table=block_table, planted=planted)
+
+
+def index_sets(inp: DecodeInputs, k: int, seed: int = 0, k_max: Optional[int] = None,
+               extra_invalid: int = 0) -> np.ndarray:
+    """Irregular index lists for the attend-only backend (Table 1 imposes no
+    block structure): row (b, r) holds min(k, L_b) distinct positions drawn
+    uniformly from [0, L_b), ascending, then -1 padding up to k_max.  With
+    extra_invalid > 0 that many entries of each row (within k_max) are
+    replaced by positions the attention must skip (-1 or >= L_b)."""
+    k_max = k if k_max is None else k_max
+    idx = np.full((inp.B, inp.rows, k_max), -1, dtype=np.int32)
+    for b in range(inp.B):
+        L = int(inp.seq_lens[b])
+        n = min(k, L, k_max)
+        rng = _rng(0, seed, b, 0, TAG_SETS)
+        for r in range(inp.rows):
+            if n:
+                idx[b, r, :n] = np.sort(rng.choice(L, size=n, replace=False))
+            if extra_invalid and k_max:
+                at = rng.choice(k_max, size=min(extra_invalid, k_max), replace=False)
+                idx[b, r, at] = np.where(rng.random(at.size) < 0.5, -1, L + rng.integers(0, 64, at.size))
+    return idx
+
+
+def index_weights(shape, seed: int = 0, zero_frac: float = 0.0) -> np.ndarray:
+    """Per-entry weights for index lists: U[0.05, 3), a fraction zero_frac of
+    them exactly 0."""
+    rng = _rng(0, seed, 0, 0, TAG_WEIGHTS)
+    w = rng.uniform(0.05, 3.0, size=shape).astype(np.float32)
+    if zero_frac:
+        w[rng.random(shape) < zero_frac] = 0.0
+    return w
+
+
+def backend_sweep_inputs(B: int = 16, N: int = 131072, Hq: int = 32, Hkv: int = 8,
+                         seed: int = 0, device="cuda"):
+    """The kernel-benchmark shape of Table 1 drawn directly on the GPU (host
+    generation of 8.6 GB would dominate a sweep): B sequences of N positions
+    in a paged NHD cache (page 16) with a random physical page order, bfloat16
+    K, V ~ N(0, 1) and q ~ N(0, 1) / sqrt(d).  Returns a dict of device
+    tensors: q [B, Hq, d], k and v [pages, 16, Hkv, d], block_table
+    [B, N / 16] int32, seq_lens [B] int32."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(ROOT_SEED * 1000 + seed)
+    per = -(-N // PAGE_SIZE)
+    pages = B * per
+    perm = torch.randperm(pages, generator=gen, device=device).to(torch.int32)
+    shape = (pages, PAGE_SIZE, Hkv, HEAD_DIM)
+    k = torch.randn(shape, generator=gen, device=device, dtype=torch.float32).to(torch.bfloat16)
+    v = torch.randn(shape, generator=gen, device=device, dtype=torch.float32).to(torch.bfloat16)
+    q = (torch.randn((B, Hq, HEAD_DIM), generator=gen, device=device) /
+         math.sqrt(HEAD_DIM)).to(torch.bfloat16)
+    return {"q": q, "k": k, "v": v, "block_table": perm.view(B, per).contiguous(),
+            "seq_lens": torch.full((B,), N, dtype=torch.int32, device=device)}
+
+
+def backend_sweep_sets(rows: int, N: int, k: int, seed: int = 0, device="cuda"):
+    """Irregular index lists on the GPU for the backend sweep: each of `rows`
+    rows holds k distinct positions of [0, N), uniform, ascending (no block
+    structure), with weights U[0.05, 3).  Returns (idx int32, weights f32)."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(ROOT_SEED * 1000 + 7919 * seed + k)
+    idx = torch.empty((rows, k), dtype=torch.int32, device=device)
+    for r0 in range(0, rows, 64):  # bounded temporary: 64 rows of N keys at a time
+        r1 = min(rows, r0 + 64)
+        keys = torch.rand((r1 - r0, N), generator=gen, device=device)
+        idx[r0:r1] = torch.sort(torch.topk(keys, k, dim=1, sorted=False).indices, dim=1).values
+    w = torch.rand((rows, k), generator=gen, device=device) * 2.95 + 0.05
+    return idx, w

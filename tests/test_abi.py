@@ -159,6 +159,59 @@ def test_stage_entry_points_reject_invalid_arguments(sd):
                                        C.byref(wrong_rows), C.byref(sp), C.byref(out), None) == -1
 
 
+def test_weighted_attend_rejects_invalid_weights(sd):
+    q, K, V, lens, sp, out, idx = valid_parts(sd)
+
+    def call(w):
+        return sd.lib.sparse_decode_attend_weighted(C.byref(q), C.byref(K), C.byref(V), lens,
+                                                    C.byref(idx), w, C.byref(sp), C.byref(out),
+                                                    None)
+    assert call(None) == -1
+    assert call(C.byref(tensor(sd, (2, 32, 204), sd.SD_F32))) == -1   # shape differs from idx
+    assert call(C.byref(tensor(sd, (2, 32, 205), sd.SD_BF16))) == -1  # not float32
+    assert call(C.byref(tensor(sd, (2, 8, 205), sd.SD_F32))) == -1
+    w = tensor(sd, (2, 32, 205), sd.SD_F32, data=None)                # k_max > 0, no data
+    assert call(C.byref(w)) == -1
+
+
+@pytest.mark.parametrize("defect,code", [
+    ("f32", -2), ("group_16", -2), ("seq_lens_null", -1), ("out_wrong_shape", -1),
+    ("scale_nan", -1), ("v_missing", -1), ("out_dtype", -1),
+])
+def test_dense_attention_rejects_invalid_arguments(sd, defect, code):
+    q, K, V, lens, sp, out, idx = valid_parts(sd)
+    scale = 0.0
+    if defect == "f32":
+        q.dtype = K.t.dtype = V.t.dtype = out.dtype = sd.SD_F32
+    elif defect == "group_16":
+        q, K, V, lens, sp, out, idx = valid_parts(sd, Hq=64, Hkv=4)
+    elif defect == "seq_lens_null":
+        lens = None
+    elif defect == "out_wrong_shape":
+        out.shape[1] = 16
+    elif defect == "scale_nan":
+        scale = math.nan
+    elif defect == "out_dtype":
+        out.dtype = sd.SD_F32
+    vref = None if defect == "v_missing" else C.byref(V)
+    assert sd.lib.sparse_decode_dense_attention(C.byref(q), C.byref(K), vref, lens, scale,
+                                                C.byref(out), None) == code
+
+
+def test_dense_workspace_grows_with_the_cache(sd):
+    sizes = []
+    for N in (4096, 65536, 131072):
+        q, K, *_ = valid_parts(sd, B=4, N=N)
+        n = C.c_size_t(0)
+        assert sd.lib.sparse_decode_dense_workspace_size(C.byref(q), C.byref(K), C.byref(n)) == 0
+        sizes.append(n.value)
+    assert 0 < sizes[0] <= sizes[1] <= sizes[2]
+    q, K, *_ = valid_parts(sd)
+    K.t.dtype = q.dtype = sd.SD_F32
+    n = C.c_size_t(0)
+    assert sd.lib.sparse_decode_dense_workspace_size(C.byref(q), C.byref(K), C.byref(n)) == -2
+
+
 def test_empty_batch_is_a_no_op(sd):
     q = tensor(sd, (0, 32, 128))
     K, V = bhnd(sd, 0, 8, 4096), bhnd(sd, 0, 8, 4096)

@@ -335,6 +335,35 @@ def test_weighted_attention_special_cases():
         O.attend_weighted(p, idx, -hot)                              # negative weights rejected
 
 
+def test_dense_attention_is_plain_sdpa_over_each_sequence():
+    rng = np.random.default_rng(23)
+    B, Hq, Hkv, N, d = 3, 6, 2, 37, 16
+    q = rng.standard_normal((B, Hq, d)).astype(np.float32)
+    K = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    V = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    lens = [37, 0, 5]
+    p = problem(q, K, V, seq_lens=lens, Hkv=Hkv)
+    out = O.dense_attention(p)
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hq):
+            L = lens[b]
+            if L == 0:
+                assert (out[b, h] == 0).all()
+                continue
+            kt = torch.from_numpy(K[b, h // G, :L].astype(np.float64))[None, None]
+            vt = torch.from_numpy(V[b, h // G, :L].astype(np.float64))[None, None]
+            qt = torch.from_numpy(q[b, h].astype(np.float64))[None, None, None]
+            ref = torch.nn.functional.scaled_dot_product_attention(qt, kt, vt)
+            np.testing.assert_allclose(out[b, h], ref[0, 0, 0].numpy(), rtol=0, atol=1e-12)
+    # The same step in the paged layout, and a subset of the batch.
+    pp = to_paged(p, 4, seed=3)
+    np.testing.assert_array_equal(O.dense_attention(pp), out)
+    part = O.dense_attention(p, batch=[2])
+    np.testing.assert_array_equal(part[2], out[2])
+    assert np.isnan(part[0]).all()
+
+
 def test_empty_sequence_gives_zero_output_and_no_indices():
     rng = np.random.default_rng(8)
     q = rng.standard_normal((2, 2, 8))

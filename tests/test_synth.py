@@ -98,3 +98,28 @@ def test_mixture_keys_are_clustered():
     d2 = ((sample[:, None, :] - kf[None, :, :]) ** 2).sum(-1)
     d2[np.arange(200), np.arange(200)] = np.inf
     assert np.median(np.sqrt(d2.min(1))) < 6.0
+
+
+def test_index_sets_and_weights_for_the_attend_only_backend():
+    inp = synth.make_inputs(4, seed=0, B=3, seq_lens=[0, 20, 500], N=512)
+    a = synth.index_sets(inp, 50, seed=4, k_max=64)
+    b = synth.index_sets(inp, 50, seed=4, k_max=64)
+    np.testing.assert_array_equal(a, b)
+    assert a.shape == (3, inp.rows, 64)
+    assert (a[0] == -1).all()                       # empty sequence: all padding
+    for bb, n in ((1, 20), (2, 50)):
+        L = int(inp.seq_lens[bb])
+        row = a[bb]
+        assert (row[:, n:] == -1).all()
+        live = row[:, :n]
+        assert ((live >= 0) & (live < L)).all()
+        assert (np.diff(live, axis=1) > 0).all()   # distinct, ascending
+    c = synth.index_sets(inp, 50, seed=4, k_max=64, extra_invalid=5)
+    for r in range(inp.rows):
+        bad = (c[2, r] < 0) | (c[2, r] >= 500)
+        assert bad.sum() >= 5
+    w = synth.index_weights(a.shape, seed=1, zero_frac=0.25)
+    assert w.dtype == np.float32 and w.shape == a.shape
+    assert (w >= 0).all() and (w < 3.0).all()
+    assert 0.15 < (w == 0).mean() < 0.35
+    np.testing.assert_array_equal(w, synth.index_weights(a.shape, seed=1, zero_frac=0.25))
