@@ -185,6 +185,54 @@ int32_t oracle_select_row(const double *scores, int64_t L, int64_t k,
   return ORACLE_OK;
 }
 
+/*
+ * Forced positions, the scaffolding of the paper's long-context runs (the
+ * SWE-Bench appendix keeps 128 sink and 128 local positions besides the
+ * exact top-k; the extreme top-K sweep keeps 64 sinks): the first n_sink
+ * and the last n_local positions of a sequence are always attended, and
+ * the exact top-k budget kh covers the positions in between.  Sinks take
+ * precedence when the two overlap.
+ */
+static void forced_counts(int64_t L, int64_t n_sink, int64_t n_local, int64_t *ns, int64_t *nl) {
+  *ns = n_sink < L ? n_sink : L;
+  *nl = n_local < L - *ns ? n_local : L - *ns;
+}
+
+/*
+ * The kept set of one row with forced positions: positions 0..ns-1, then
+ * the exact top-kh of positions ns..L-nl-1 (scores descending, positions
+ * ascending on ties; ascending in idx), then L-nl..L-1, then -1 padding to
+ * k_max.  tau gets the kh-th largest middle score (NaN when kh = 0).
+ */
+int32_t oracle_select_forced(const double *scores, int64_t L, int64_t n_sink, int64_t n_local,
+                             int64_t kh, int64_t k_max, int32_t *idx, double *tau) {
+  if (L < 0 || n_sink < 0 || n_local < 0 || kh < 0) return ORACLE_EINVAL;
+  int64_t ns, nl;
+  forced_counts(L, n_sink, n_local, &ns, &nl);
+  int64_t mid = L - ns - nl;
+  if (kh > mid || ns + kh + nl > k_max) return ORACLE_EINVAL;
+  for (int64_t t = 0; t < ns; ++t) idx[t] = (int32_t)t;
+  int rc = oracle_select_row(scores + ns, mid, kh, kh, idx + ns, tau);
+  if (rc) return rc;
+  for (int64_t t = 0; t < kh; ++t) idx[ns + t] += (int32_t)ns;
+  for (int64_t t = 0; t < nl; ++t) idx[ns + kh + t] = (int32_t)(L - nl + t);
+  for (int64_t t = ns + kh + nl; t < k_max; ++t) idx[t] = -1;
+  return ORACLE_OK;
+}
+
+/* Heavy budget of a row with forced positions: the ratio (or override) rule
+ * on the whole sequence, capped by the positions left between the forced
+ * ones; and the row's total. */
+static int64_t heavy_budget(int64_t L, double ratio, int32_t rounding, const int32_t *k_override,
+                            int b, int64_t n_sink, int64_t n_local, int64_t *total) {
+  int64_t ns, nl;
+  forced_counts(L, n_sink, n_local, &ns, &nl);
+  int64_t kh = row_budget(L, ratio, rounding, k_override, b);
+  if (kh > L - ns - nl) kh = L - ns - nl;
+  if (total) *total = ns + nl + kh;
+  return kh;
+}
+
 typedef struct {
   int B, Hq, Hkv, d;
   const void *q;
@@ -288,13 +336,17 @@ int32_t oracle_scores(int B, int Hq, int Hkv, int d, const void *q,
 int32_t oracle_select_f32(int B, int R, int64_t ncap, const float *scores,
                           const int32_t *seq_lens, double ratio,
                           int32_t rounding, const int32_t *k_override,
+                          int64_t n_sink, int64_t n_local,
                           int64_t k_max, int32_t *idx, double *tau,
                           int nthreads) {
   if (B < 0 || R <= 0 || !scores || !seq_lens || !idx || !(ratio > 0.0))
     return ORACLE_EINVAL;
+  if (n_sink < 0 || n_local < 0) return ORACLE_EINVAL;
   for (int b = 0; b < B; ++b) {
+    int64_t total;
     if (seq_lens[b] < 0 || seq_lens[b] > ncap) return ORACLE_EINVAL;
-    if (row_budget(seq_lens[b], ratio, rounding, k_override, b) > k_max) return ORACLE_EINVAL;
+    heavy_budget(seq_lens[b], ratio, rounding, k_override, b, n_sink, n_local, &total);
+    if (total > k_max) return ORACLE_EINVAL;
   }
   set_threads(nthreads);
   int rc_all = ORACLE_OK;
@@ -305,8 +357,9 @@ int32_t oracle_select_f32(int B, int R, int64_t ncap, const float *scores,
     double *row = (double *)malloc(sizeof(double) * (size_t)(L > 0 ? L : 1));
     if (!row) { rc_all = ORACLE_ENOMEM; continue; }
     for (int64_t j = 0; j < L; ++j) row[j] = (double)scores[r * ncap + j];
-    int64_t k = row_budget(L, ratio, rounding, k_override, b);
-    int rc = oracle_select_row(row, L, k, k_max, idx + r * k_max, tau ? tau + r : NULL);
+    int64_t kh = heavy_budget(L, ratio, rounding, k_override, b, n_sink, n_local, NULL);
+    int rc = oracle_select_forced(row, L, n_sink, n_local, kh, k_max, idx + r * k_max,
+                                  tau ? tau + r : NULL);
     if (rc) rc_all = rc;
     free(row);
   }
@@ -441,16 +494,20 @@ int32_t oracle_sparse_attention(int B, int Hq, int Hkv, int d, const void *q,
                                 const oracle_cache *V, const int32_t *seq_lens,
                                 double ratio, int32_t rounding,
                                 int32_t group_shared, double scale,
-                                const int32_t *k_override, int64_t k_max,
+                                const int32_t *k_override, int64_t n_sink,
+                                int64_t n_local, int64_t k_max,
                                 int32_t *idx, double *tau, double *out,
                                 double *absw, int nthreads) {
   problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared);
   int rc = check_problem(&p, 1);
   if (rc) return rc;
-  if (!idx || !out || !(ratio > 0.0)) return ORACLE_EINVAL;
+  if (!idx || !out || !(ratio > 0.0) || n_sink < 0 || n_local < 0) return ORACLE_EINVAL;
   int R = group_shared ? Hkv : Hq;
-  for (int b = 0; b < B; ++b)
-    if (row_budget(seq_lens[b], ratio, rounding, k_override, b) > k_max) return ORACLE_EINVAL;
+  for (int b = 0; b < B; ++b) {
+    int64_t total;
+    heavy_budget(seq_lens[b], ratio, rounding, k_override, b, n_sink, n_local, &total);
+    if (total > k_max) return ORACLE_EINVAL;
+  }
   set_threads(nthreads);
   int rc_all = ORACLE_OK;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -460,8 +517,9 @@ int32_t oracle_sparse_attention(int B, int Hq, int Hkv, int d, const void *q,
     double *buf = (double *)malloc(sizeof(double) * (size_t)(2 * d + (L > 0 ? L : 1)));
     if (!buf) { rc_all = ORACLE_ENOMEM; continue; }
     row_scores(&p, b, row, buf, buf + d, buf + 2 * d);
-    int64_t k = row_budget(L, ratio, rounding, k_override, b);
-    int rc1 = oracle_select_row(buf + 2 * d, L, k, k_max, idx + r * k_max, tau ? tau + r : NULL);
+    int64_t kh = heavy_budget(L, ratio, rounding, k_override, b, n_sink, n_local, NULL);
+    int rc1 = oracle_select_forced(buf + 2 * d, L, n_sink, n_local, kh, k_max, idx + r * k_max,
+                                   tau ? tau + r : NULL);
     if (rc1) rc_all = rc1;
     free(buf);
   }

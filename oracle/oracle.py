@@ -52,7 +52,10 @@ def lib() -> C.CDLL:
         L.oracle_select_f32.restype = C.c_int32
         L.oracle_select_f32.argtypes = [C.c_int, C.c_int, C.c_int64, C.c_void_p, C.c_void_p,
                                         C.c_double, C.c_int32, C.c_void_p, C.c_int64,
-                                        C.c_void_p, C.c_void_p, C.c_int]
+                                        C.c_int64, C.c_int64, C.c_void_p, C.c_void_p, C.c_int]
+        L.oracle_select_forced.restype = C.c_int32
+        L.oracle_select_forced.argtypes = [C.c_void_p, C.c_int64, C.c_int64, C.c_int64,
+                                           C.c_int64, C.c_int64, C.c_void_p, C.c_void_p]
         L.oracle_attend.restype = C.c_int32
         L.oracle_attend.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int32,
                                     C.POINTER(_Cache), C.POINTER(_Cache), C.c_void_p, C.c_int32,
@@ -67,7 +70,8 @@ def lib() -> C.CDLL:
         L.oracle_sparse_attention.argtypes = [
             C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int32, C.POINTER(_Cache),
             C.POINTER(_Cache), C.c_void_p, C.c_double, C.c_int32, C.c_int32, C.c_double,
-            C.c_void_p, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int]
+            C.c_void_p, C.c_int64, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
+            C.c_void_p, C.c_int]
         L.oracle_max_threads.restype = C.c_int32
         L.oracle_max_threads.argtypes = [C.c_int]
         _lib = L
@@ -151,14 +155,43 @@ def scores(inp, nthreads: int = 0) -> np.ndarray:
     return out
 
 
+def forced_of(inp) -> tuple:
+    """(n_sink, n_local) of a decode step (0, 0 unless the step sets them)."""
+    return int(getattr(inp, "n_sink", 0) or 0), int(getattr(inp, "n_local", 0) or 0)
+
+
+def select_forced(scores: np.ndarray, n_sink: int, n_local: int, kh: int,
+                  k_max: int | None = None):
+    """Kept set of one float64 score row with forced positions: the first
+    n_sink and last n_local positions, plus the exact top-kh in between;
+    returns (ascending idx padded with -1 to k_max, tau)."""
+    s = np.ascontiguousarray(scores, dtype=np.float64)
+    L = len(s)
+    ns = min(n_sink, L)
+    nl = min(n_local, L - ns)
+    k_max = ns + nl + kh if k_max is None else k_max
+    idx = np.empty(max(k_max, 1), dtype=np.int32)
+    tau = np.empty(1, dtype=np.float64)
+    _check(lib().oracle_select_forced(s.ctypes.data, L, int(n_sink), int(n_local), int(kh),
+                                      int(k_max), idx.ctypes.data, tau.ctypes.data),
+           "select_forced")
+    return idx[:k_max], float(tau[0])
+
+
 def k_max_for(inp) -> int:
-    """Largest budget any sequence of this cache capacity can need."""
-    return budget(inp.ncap, inp.ratio, inp.rounding)
+    """Largest budget any sequence of this cache capacity can need (forced
+    positions included)."""
+    ns, nl = forced_of(inp)
+    n = int(inp.ncap)
+    fs = min(ns, n)
+    fl = min(nl, n - fs)
+    return fs + fl + min(budget(n, inp.ratio, inp.rounding), n - fs - fl)
 
 
 def select_f32(scores_f32: np.ndarray, seq_lens, ratio: float, rounding: int, k_max: int,
-               k_override=None, nthreads: int = 0):
-    """Exact top-k over given float32 scores [B, R, ncap]; returns (idx, tau)."""
+               k_override=None, nthreads: int = 0, n_sink: int = 0, n_local: int = 0):
+    """Exact top-k over given float32 scores [B, R, ncap] (with forced
+    positions when n_sink or n_local is set); returns (idx, tau)."""
     s = np.ascontiguousarray(scores_f32, dtype=np.float32)
     B, R, ncap = s.shape
     lens = np.ascontiguousarray(seq_lens, dtype=np.int32)
@@ -166,8 +199,9 @@ def select_f32(scores_f32: np.ndarray, seq_lens, ratio: float, rounding: int, k_
     idx = np.empty((B, R, k_max), dtype=np.int32)
     tau = np.empty((B, R), dtype=np.float64)
     _check(lib().oracle_select_f32(B, R, ncap, s.ctypes.data, lens.ctypes.data, float(ratio),
-                                   int(rounding), _ptr(ko), int(k_max), idx.ctypes.data,
-                                   tau.ctypes.data, nthreads), "select_f32")
+                                   int(rounding), _ptr(ko), int(n_sink), int(n_local),
+                                   int(k_max), idx.ctypes.data, tau.ctypes.data, nthreads),
+           "select_f32")
     return idx, tau
 
 
@@ -244,7 +278,8 @@ def _one_sequence(inp, b: int):
 
 def sparse_attention(inp, k_max: int | None = None, k_override=None, scale: float = 0.0,
                      nthreads: int = 0) -> dict:
-    """The whole method: returns dict(idx, tau, out, absw)."""
+    """The whole method: returns dict(idx, tau, out, absw).  Forced positions
+    come from the step's n_sink / n_local attributes when it has them."""
     keep: list = []
     K = _cache(inp, inp.k, keep)
     V = _cache(inp, inp.v, keep)
@@ -259,8 +294,9 @@ def sparse_attention(inp, k_max: int | None = None, k_override=None, scale: floa
     _check(lib().oracle_sparse_attention(
         inp.B, inp.Hq, inp.Hkv, inp.d, q.ctypes.data, _dtype_code(inp.dtype), C.byref(K),
         C.byref(V), lens.ctypes.data, float(inp.ratio), int(inp.rounding),
-        int(inp.group_shared), float(scale), _ptr(ko), int(k_max), idx.ctypes.data,
-        tau.ctypes.data, out.ctypes.data, absw.ctypes.data, nthreads), "sparse_attention")
+        int(inp.group_shared), float(scale), _ptr(ko), *forced_of(inp), int(k_max),
+        idx.ctypes.data, tau.ctypes.data, out.ctypes.data, absw.ctypes.data, nthreads),
+        "sparse_attention")
     return {"idx": idx, "tau": tau, "out": out, "absw": absw}
 
 

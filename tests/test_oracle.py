@@ -210,6 +210,86 @@ def test_select_f32_uses_float32_values_exactly():
 
 
 # --------------------------------------------------------------------------
+# Selection with forced sink and local positions.
+# --------------------------------------------------------------------------
+
+def test_forced_selection_matches_enumeration_of_the_middle():
+    rng = np.random.default_rng(31)
+    for trial in range(80):
+        L = int(rng.integers(0, 12))
+        ns, nl = int(rng.integers(0, 5)), int(rng.integers(0, 5))
+        s = rng.integers(-3, 4, L).astype(np.float64)
+        fs = min(ns, L)
+        fl = min(nl, L - fs)
+        mid = list(range(fs, L - fl))
+        for kh in range(0, len(mid) + 1):
+            idx, tau = O.select_forced(s, ns, nl, kh, k_max=L + 3)
+            # the exact top-kh of the middle positions alone, then the union
+            heavy = [mid[i] for i in brute_force_topk([s[j] for j in mid], kh)]
+            want = sorted(set(range(fs)) | set(heavy) | set(range(L - fl, L)))
+            assert list(idx[:len(want)]) == want, (L, ns, nl, kh)
+            assert (idx[len(want):] == -1).all()
+            if kh:
+                assert tau == min(s[j] for j in heavy)
+            else:
+                assert math.isnan(tau)
+
+
+def test_forced_selection_special_cases():
+    rng = np.random.default_rng(32)
+    s = rng.standard_normal(40)
+    for k in (0, 1, 7, 40):
+        a, ta = O.select_forced(s, 0, 0, k, k_max=45)   # nothing forced: plain top-k
+        b, tb = O.select_row(s, k, k_max=45)
+        np.testing.assert_array_equal(a, b)
+        assert (math.isnan(ta) and math.isnan(tb)) or ta == tb
+    # Forced positions are kept whatever their scores, and never use budget.
+    s = np.array([9.0, -5.0, 1.0, 2.0, 3.0, 8.0, -9.0, -7.0])
+    idx, _ = O.select_forced(s, 2, 2, 1)
+    assert list(idx) == [0, 1, 5, 6, 7]                  # middle top-1 is position 5
+    idx, _ = O.select_forced(s, 2, 2, 0)
+    assert list(idx) == [0, 1, 6, 7]
+    # Forced windows covering the sequence keep every position once.
+    idx, _ = O.select_forced(s, 5, 5, 0, k_max=9)
+    assert list(idx) == list(range(8)) + [-1]
+    idx, _ = O.select_forced(s, 20, 3, 0)
+    assert list(idx) == list(range(8))
+    with pytest.raises(O.OracleError):
+        O.select_forced(s, 2, 2, 5)                      # more heavy than the middle holds
+
+
+def test_forced_positions_in_the_whole_method():
+    rng = np.random.default_rng(33)
+    B, Hq, N, d = 2, 3, 50, 16
+    q = rng.standard_normal((B, Hq, d)).astype(np.float32)
+    K = rng.standard_normal((B, 1, N, d)).astype(np.float32)
+    V = rng.standard_normal((B, 1, N, d)).astype(np.float32)
+    p = problem(q, K, V, seq_lens=[50, 9], ratio=10.0)     # heavy k = 5 and 1
+    p.n_sink, p.n_local = 4, 3
+    r = O.sparse_attention(p)
+    assert r["idx"].shape[2] == O.k_max_for(p) == 4 + 3 + 5
+    sc = O.scores(p)
+    for b, (L, kh) in enumerate(((50, 5), (9, 1))):
+        for h in range(Hq):
+            want, _ = O.select_forced(sc[b, h, :L], 4, 3, kh, k_max=12)
+            np.testing.assert_array_equal(r["idx"][b, h], want)
+    # The same sets through the plain attention give the same output.
+    out, _ = O.attend(p, r["idx"])
+    np.testing.assert_array_equal(out, r["out"])
+    # Forced windows plus budget covering everything: dense attention.
+    p.n_sink, p.n_local = 25, 25
+    full = O.sparse_attention(p)
+    np.testing.assert_allclose(full["out"], O.dense_attention(p), rtol=0, atol=1e-12)
+    # The float32 selection entry point agrees.
+    p.n_sink, p.n_local = 4, 3
+    s32 = np.nan_to_num(sc, nan=-np.inf).astype(np.float32)
+    idx32, _ = O.select_f32(s32, p.seq_lens, 10.0, 0, 12, n_sink=4, n_local=3)
+    ref32 = np.array([[O.select_forced(s32[b, h, :L].astype(np.float64), 4, 3, kh, k_max=12)[0]
+                       for h in range(Hq)] for b, (L, kh) in enumerate(((50, 5), (9, 1)))])
+    np.testing.assert_array_equal(idx32, ref32)
+
+
+# --------------------------------------------------------------------------
 # Attention: dense limit, special cases, invariants.
 # --------------------------------------------------------------------------
 

@@ -40,6 +40,10 @@ MUTANTS = {
     "weights_squared": ("if (omega) z[t] *= (double)omega[t];",
                         "if (omega) z[t] *= (double)omega[t] * (double)omega[t];"),
     "weights_ignored": ("if (omega) z[t] *= (double)omega[t];", "if (omega) z[t] *= 1.0;"),
+    "forced_sinks_compete_for_budget": ("int rc = oracle_select_row(scores + ns, mid, kh, kh, idx + ns, tau);",
+                                        "int rc = oracle_select_row(scores, mid, kh, kh, idx + ns, tau);"),
+    "local_window_off_by_one": ("idx[ns + kh + t] = (int32_t)(L - nl + t);",
+                                "idx[ns + kh + t] = (int32_t)(L - nl + t - 1);"),
     "row_scores_skip_last_position": ("for (int64_t j = 0; j < L; ++j) {\n    load_vec(p->K->data",
                                       "for (int64_t j = 0; j + 1 < L; ++j) {\n    load_vec(p->K->data"),
 }
