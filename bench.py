@@ -46,14 +46,17 @@ def kernel_hash() -> str:
 def path_bytes(inp, ks):
     """Algorithmic HBM bytes of one step: every key once, the kept value rows,
     q, out and idx.  (Per-head mode gathers one value row per query head and
-    kept position; group-shared mode one key and one value row per KV head.)"""
+    kept position, plus its key row when forced positions make the attention
+    recompute its logits; group-shared mode one key and one value row per KV
+    head.)"""
     e = 2 if inp.dtype == "bf16" else 4
     row = inp.d * e
     key_stream = sum(int(L) for L in inp.seq_lens) * inp.Hkv * row
     if inp.group_shared:
         gather = sum(int(k) for k in ks) * inp.Hkv * 2 * row
     else:
-        gather = sum(int(k) for k in ks) * inp.Hq * row
+        per_entry = 2 * row if inp.n_sink + inp.n_local > 0 else row
+        gather = sum(int(k) for k in ks) * inp.Hq * per_entry
     k_max = max(int(k) for k in ks)
     small = 2 * inp.B * inp.Hq * row + inp.B * inp.rows * k_max * 4
     return key_stream, gather, small
@@ -72,7 +75,7 @@ def counters_traffic():
     return c.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(inp, n_seq):
+def cpu_baseline(inp, n_seq, k_max, fixed_k=None):
     import dataclasses
     from oracle import oracle as O
     bs = list(range(min(n_seq, inp.B)))
@@ -89,7 +92,9 @@ def cpu_baseline(inp, n_seq):
     threads = max(1, min(threads, 16))
     used = O.max_threads(threads)
     t0 = time.perf_counter()
-    O.sparse_attention(sub, k_max=O.k_max_for(inp), nthreads=threads)
+    import numpy as np
+    ko = None if fixed_k is None else np.full(len(bs), fixed_k, np.int32)
+    O.sparse_attention(sub, k_max=k_max, k_override=ko, nthreads=threads)
     dt = time.perf_counter() - t0
     return {"value": len(bs) / dt, "unit": "queries/s", "cores": used, "kind": "oracle",
             "sample": f"{len(bs)} of {inp.B} sequences ({len(bs) * inp.rows} rows), "
@@ -125,11 +130,12 @@ def time_calls(torch, fn, steps, warmup):
     return e0.elapsed_time(e1) / steps
 
 
-def time_graph(torch, fn, steps, warmup):
-    """Mean ms per call with `steps` calls captured in one HIP graph and
-    replayed (kernel time without the host's per-call work); also returns
-    whether the replay left the same output as the eager calls.  fn() returns
-    its output tensor."""
+def time_graph(torch, fn, steps, warmup, replays=5):
+    """Mean ms per call with `steps` calls captured in one HIP graph, replayed
+    `replays` times back to back (kernel time without the host's per-call
+    work; the replays overlap each graph's launch with the previous one's
+    kernels); also returns whether the replay left the same output as the
+    eager calls.  fn() returns its output tensor."""
     for _ in range(warmup):  # eager: also sizes the library workspace before capture
         ref = fn()
     torch.cuda.synchronize()
@@ -144,12 +150,13 @@ def time_graph(torch, fn, steps, warmup):
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record()
-    g.replay()
+    for _ in range(replays):
+        g.replay()
     e1.record()
     torch.cuda.synchronize()
     same = bool(torch.equal(out, ref))
     del g
-    return e0.elapsed_time(e1) / steps, same
+    return e0.elapsed_time(e1) / (steps * replays), same
 
 
 def backend_table(args):
@@ -212,9 +219,10 @@ def backend_table(args):
                    "layout": "paged NHD, page 16, random page order", "dtype": "bf16",
                    "index_lists": "uniform random distinct positions per query head, "
                                   "weights U[0.05, 3)"},
-        "timing": "ms: K calls captured in one HIP graph and replayed, events around the "
-                  "replay (kernel time, as a kernel benchmark measures it); eager_ms: K calls "
-                  "back to back through the Python binding (adds its per-call host work)",
+        "timing": "ms: K calls captured in one HIP graph, replayed 5 times back to back "
+                  "between events (kernel time, as a kernel benchmark measures it); eager_ms: "
+                  "K calls back to back through the Python binding (adds its per-call host "
+                  "work)",
         "dense_bytes": "all K and V rows of the batch",
         "sparse_bytes": "per query head and kept position one K and one V row (256 B each), "
                         "its index and weight",
@@ -235,6 +243,14 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device to device once (a plain "
                          "copy of known size that scales hardware traffic counters)")
+    ap.add_argument("--sink", type=int, default=0,
+                    help="forced first positions of every sequence (sink window)")
+    ap.add_argument("--local", type=int, default=0,
+                    help="forced last positions of every sequence (local window)")
+    ap.add_argument("--ratio", type=float, default=None,
+                    help="sparsity S (top-k budget round(L/S)) instead of the workload's")
+    ap.add_argument("--fixed-k", type=int, default=None,
+                    help="top-k budget K for every sequence instead of the ratio rule")
     ap.add_argument("--table1", action="store_true",
                     help="instead of the default line, sweep dense decode against the "
                          "weighted sparse backend in Table 1's shape (batch 1/4/8/16, "
@@ -257,12 +273,24 @@ def main():
     torch.cuda.set_device(0)
     log(f"generating workload {args.workload} ({synth.NAMES[args.workload]})")
     t0 = time.perf_counter()
-    inp = synth.make_inputs(args.workload, seed=args.seed)
+    extra = {} if args.ratio is None else {"ratio": args.ratio}
+    inp = synth.make_inputs(args.workload, seed=args.seed, n_sink=args.sink, n_local=args.local,
+                            **extra)
     log(f"  generated in {time.perf_counter() - t0:.1f} s; copying to the GPU")
     q, cache, lens = sd.cache_from_inputs(inp)
-    sp = sd.sparsity_from_inputs(inp)
-    k_max = O.k_max_for(inp)
-    ks = [O.budget(int(L), inp.ratio, inp.rounding) for L in inp.seq_lens]
+    k_override = None
+    if args.fixed_k is not None:
+        k_override = torch.full((inp.B,), args.fixed_k, dtype=torch.int32, device="cuda")
+    sp = sd.sparsity_from_inputs(inp, k_override=k_override)
+    ks = []
+    for L in inp.seq_lens:  # list entries per sequence: forced positions + top-k
+        L = int(L)
+        ns = min(inp.n_sink, L)
+        nl = min(inp.n_local, L - ns)
+        kh = (min(args.fixed_k, L) if args.fixed_k is not None
+              else O.budget(L, inp.ratio, inp.rounding))
+        ks.append(ns + nl + min(kh, L - ns - nl))
+    k_max = O.k_max_for(inp) if args.fixed_k is None else max(ks)
     out = torch.empty_like(q)
     idx = torch.empty((inp.B, inp.rows, k_max), dtype=torch.int32, device="cuda")
     ws = torch.empty(sd.workspace_size(q, cache, sp, idx), dtype=torch.uint8, device="cuda")
@@ -349,7 +377,10 @@ def main():
         "config": {"workload": synth.NAMES[args.workload], "batch": inp.B, "q_heads": inp.Hq,
                    "kv_heads": inp.Hkv, "head_dim": inp.d, "context": int(inp.ncap),
                    "sparsity": inp.ratio, "k": ks[0] if len(set(ks)) == 1 else "per sequence",
-                   "layout": inp.layout, "group_shared": inp.group_shared},
+                   "layout": inp.layout, "group_shared": inp.group_shared,
+                   **({"n_sink": inp.n_sink, "n_local": inp.n_local}
+                      if inp.n_sink or inp.n_local else {}),
+                   **({"fixed_k": args.fixed_k} if args.fixed_k is not None else {})},
         "roofline": {
             "bound": "hbm",
             "kernel": "k_score_stream",
@@ -391,7 +422,7 @@ def main():
         del src, dst
     if args.cpu_sample > 0:
         log(f"timing the CPU oracle on {args.cpu_sample} sequences")
-        rec["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample)
+        rec["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample, k_max, args.fixed_k)
     else:
         rec["cpu_baseline"] = None
     print(json.dumps(rec), flush=True)

@@ -79,7 +79,16 @@ typedef struct {
   int32_t max_pages_per_seq;     /* paged: columns of block_table                 */
 } sd_kv;
 
-/* The sparsity rule (Table 1 caption: k = N / S per query head). */
+/* The sparsity rule (Table 1 caption: k = N / S per query head), with
+ * optional forced positions: the scaffolding of the paper's long-context runs
+ * keeps the first and last positions of each sequence besides the exact
+ * top-k (Sink(128) + Local(128) + OracleTopK in the SWE-Bench appendix; 64
+ * sinks in the extreme top-K sweep of Section 3).  With n_sink or n_local
+ * set, a row keeps positions [0, ns), the exact top-k_b of [ns, L_b - nl)
+ * (k_b capped by that range) and [L_b - nl, L_b), where ns = min(n_sink, L_b)
+ * and nl = min(n_local, L_b - ns); its list holds ns + k_b + nl entries, all
+ * ascending.  Positions that do not fit the list (k_override with a short
+ * idx) are dropped, local ones first. */
 typedef struct {
   double ratio;          /* S > 0.  k_b = clamp(R(L_b / S), 1, L_b) for L_b > 0, 0 for L_b = 0 */
   int32_t k_rounding;    /* R: 0 = nearest with halves up, 1 = ceiling                          */
@@ -90,6 +99,8 @@ typedef struct {
   float softmax_scale;   /* > 0, or <= 0 for 1/sqrt(d)                                          */
   const int32_t *k_override; /* optional device int32 [B]: k_b = clamp(k_override[b], 0,
                                 min(L_b, idx capacity)) instead of the ratio rule; NULL = unused */
+  int32_t n_sink;        /* >= 0: first positions of every sequence always kept (0 = none)     */
+  int32_t n_local;       /* >= 0: last positions of every sequence always kept (0 = none)      */
 } sd_sparsity;
 
 /* Stage timings of the last sparse_decode_attention call (profiling on). */
@@ -121,10 +132,12 @@ sd_status sparse_decode_score(const sd_tensor *q, const sd_kv *K, const int32_t 
 /*
  * Exact top-k of each score row (Section 3, exact oracle top-k): for row
  * (b, r) the k_b positions j < L_b that come first under (score descending,
- * position ascending), written in ascending position order, then -1.
+ * position ascending), written in ascending position order, then -1.  With
+ * forced positions (sd_sparsity), the top-k runs over the positions between
+ * them and the list holds sinks, top-k, local window.
  *   scores f32 [B, R, C] (e.g. from sparse_decode_score)
  *   idx    i32 [B, R, k_max], k_max >= the budget of a full sequence of C
- *   vals   f32 [B, R, k_max] or NULL: the score of each kept position,
+ *   vals   f32 [B, R, k_max] or NULL: the score of each listed position,
  *          -infinity in the padding
  */
 sd_status sparse_decode_topk(const sd_tensor *scores, const int32_t *seq_lens,
@@ -204,7 +217,9 @@ sd_status sparse_decode_workspace_size(const sd_tensor *q, const sd_kv *K,
  * needed.  Nothing is kept in the workspace between calls. */
 sd_status sparse_decode_set_workspace(void *dev_ptr, size_t bytes);
 
-/* k for a sequence of L positions under the ratio rule of `sparsity`. */
+/* Entries of the index list of a sequence of L positions under the ratio
+ * rule of `sparsity`: k, plus the forced positions when n_sink or n_local
+ * is set.  -1 for an invalid rule. */
 int64_t sparse_decode_budget(int64_t L, const sd_sparsity *sparsity);
 
 /* Profiling: while enabled, sparse_decode_attention records HIP events

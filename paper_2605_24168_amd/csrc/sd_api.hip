@@ -113,7 +113,16 @@ sd_status check_problem(const sd_tensor *q, const sd_kv *K, const sd_kv *V, cons
   if (sp->k_rounding != 0 && sp->k_rounding != 1) return SD_ERR_INVALID_ARG;
   if (!sp->k_override && !(sp->ratio > 0.0 && std::isfinite(sp->ratio))) return SD_ERR_INVALID_ARG;
   if (!std::isfinite(sp->softmax_scale)) return SD_ERR_INVALID_ARG;
+  if (sp->n_sink < 0 || sp->n_local < 0) return SD_ERR_INVALID_ARG;
   return SD_OK;
+}
+
+// Entries of a full-capacity row's list under the ratio rule: forced
+// positions plus the top-k budget.
+int64_t list_budget(int64_t L, const sd_sparsity *sp) {
+  const int64_t rule = sd::budget_rule(L, sp->ratio, sp->k_rounding);
+  const int Lc = (int)(L < INT32_MAX ? L : INT32_MAX);
+  return sd::row_plan(Lc, sp->n_sink, sp->n_local, rule, INT32_MAX).total;
 }
 
 // idx [B, R, k_max] int32 large enough for a full-capacity sequence.
@@ -123,8 +132,7 @@ sd_status check_idx(const sd_tensor *idx, const Shape &s, const sd_sparsity *sp,
   k_max = idx->shape[2];
   if (k_max > 0 && !idx->data) return SD_ERR_INVALID_ARG;
   if (k_max > INT32_MAX / 2) return SD_ERR_UNSUPPORTED;
-  if (!sp->k_override && k_max < sd::budget_rule(s.ncap, sp->ratio, sp->k_rounding))
-    return SD_ERR_INVALID_ARG;
+  if (!sp->k_override && k_max < list_budget(s.ncap, sp)) return SD_ERR_INVALID_ARG;
   return SD_OK;
 }
 
@@ -166,6 +174,8 @@ sd::Params make_params(const sd_tensor *q, const sd_kv *K, const sd_kv *V, const
   p.rounding = sp->k_rounding;
   p.k_max = (int32_t)k_max;
   p.ncap = s.ncap;
+  p.n_sink = sp->n_sink;
+  p.n_local = sp->n_local;
   return p;
 }
 
@@ -211,6 +221,8 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
   shape_only.G = s.G;
   shape_only.group_shared = group_shared;
   shape_only.k_max = (int32_t)k_max;
+  shape_only.n_sink = sp->n_sink;
+  shape_only.n_local = sp->n_local;
   L.nsplit = sd::attend_nsplit(shape_only);
   size_t off = 0;
   auto take = [&](size_t bytes) {
@@ -314,7 +326,8 @@ const char *sparse_decode_status_string(sd_status status) {
 
 int64_t sparse_decode_budget(int64_t L, const sd_sparsity *sp) {
   if (!sp || !(sp->ratio > 0.0) || !std::isfinite(sp->ratio)) return -1;
-  return sd::budget_rule(L, sp->ratio, sp->k_rounding);
+  if (sp->n_sink < 0 || sp->n_local < 0) return -1;
+  return list_budget(L, sp);
 }
 
 sd_status sparse_decode_set_profiling(int32_t enable) {
@@ -382,6 +395,7 @@ sd_status sparse_decode_topk(const sd_tensor *scores, const int32_t *seq_lens, c
   if (scores->shape[0] > 65535 || scores->shape[1] > 65535) return SD_ERR_UNSUPPORTED;
   if (sp->k_rounding != 0 && sp->k_rounding != 1) return SD_ERR_INVALID_ARG;
   if (!sp->k_override && !(sp->ratio > 0.0 && std::isfinite(sp->ratio))) return SD_ERR_INVALID_ARG;
+  if (sp->n_sink < 0 || sp->n_local < 0) return SD_ERR_INVALID_ARG;
   Shape s{};
   s.B = (int)scores->shape[0];
   s.R = (int)scores->shape[1];
@@ -406,6 +420,8 @@ sd_status sparse_decode_topk(const sd_tensor *scores, const int32_t *seq_lens, c
   p.R = s.R;
   p.k_max = (int32_t)k_max;
   p.ncap = s.ncap;
+  p.n_sink = sp->n_sink;
+  p.n_local = sp->n_local;
   return hip_status(sd::launch_topk(p, (const float *)scores->data, (int32_t *)idx->data,
                                     vals ? (float *)vals->data : nullptr, (hipStream_t)stream));
 }

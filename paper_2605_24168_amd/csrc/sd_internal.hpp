@@ -57,6 +57,7 @@ struct Params {
   int64_t ncap;
   const float *weights;        // [B, R, k_max] per-entry weights of the index
                                // lists (weighted attention), or null
+  int32_t n_sink, n_local;     // forced first / last positions of each sequence
 };
 
 // Scratch carved from the library workspace (see the host orchestration).
@@ -112,7 +113,36 @@ __device__ __forceinline__ int seq_len(const Params &p, int b) {
   return (int)L;
 }
 
-__device__ __forceinline__ int row_budget(const Params &p, int b, int L) {
+// What a row keeps.  The first ns and last nl positions of the sequence
+// are forced (the sink and local windows of the paper's long-context
+// scaffolding, kept besides the exact top-k); the exact top-kh runs over the
+// positions in between, [lo, hi).  kh is the ratio (or override) rule on the
+// whole sequence, capped by the middle and by the index list's length.  The
+// list holds the sinks, then the top-kh ascending, then the local window:
+// total entries, all ascending.  With nothing forced, lo = 0, hi = L and kh
+// is the plain budget.
+struct RowPlan {
+  int ns, nl, lo, hi, kh, total;
+};
+
+__host__ __device__ inline RowPlan row_plan(int L, int n_sink, int n_local, int64_t rule,
+                                            int k_max) {
+  RowPlan r;
+  r.ns = n_sink < L ? n_sink : L;
+  r.ns = r.ns < k_max ? r.ns : k_max;
+  r.nl = n_local < L - r.ns ? n_local : L - r.ns;
+  r.nl = r.nl < k_max - r.ns ? r.nl : k_max - r.ns;
+  r.lo = r.ns;
+  r.hi = L - r.nl;
+  int64_t k = rule;
+  if (k > r.hi - r.lo) k = r.hi - r.lo;
+  if (k > k_max - r.ns - r.nl) k = k_max - r.ns - r.nl;
+  r.kh = (int)(k > 0 ? k : 0);
+  r.total = r.ns + r.kh + r.nl;
+  return r;
+}
+
+__device__ __forceinline__ RowPlan row_plan(const Params &p, int b, int L) {
   int64_t k;
   if (p.k_override) {
     k = p.k_override[b];
@@ -121,8 +151,7 @@ __device__ __forceinline__ int row_budget(const Params &p, int b, int L) {
   } else {
     k = budget_rule(L, p.ratio, p.rounding);
   }
-  if (k > p.k_max) k = p.k_max;
-  return (int)k;
+  return row_plan(L, p.n_sink, p.n_local, k, p.k_max);
 }
 
 // Element offset of channel 0 of (sequence b, KV head g, position j).

@@ -74,7 +74,9 @@ constexpr int kPilotTiles = 4;
 __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
   const int bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
   const int L = seq_len(p, b);
-  const int m = L < kSampleMax ? L : kSampleMax;
+  const RowPlan rp = row_plan(p, b, L);  // samples come from the top-k range only
+  const int mid = rp.hi - rp.lo;
+  const int m = mid < kSampleMax ? mid : kSampleMax;
   const int ntiles = (m + kTile - 1) / kTile;
   const int l = lane_id(), col = l & 15, s = l >> 4;
   const int t0 = blockIdx.x * kWaves + wave_id();
@@ -87,7 +89,7 @@ __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
   for (int u = 0; u < kPilotTiles; ++u) {
     const int t = t0 + u * stride;
     const int si = t * kTile + col;
-    const int64_t pos = (t < ntiles && si < m) ? ((int64_t)si * L) / m : 0;
+    const int64_t pos = rp.lo + ((t < ntiles && si < m) ? ((int64_t)si * mid) / m : 0);
     load_k_bf16(p.K, kv_offset(p.K, b, g, pos), kf[u]);
   }
 #pragma unroll
@@ -125,6 +127,7 @@ __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
 // Every thread of the block must call it.
 // ---------------------------------------------------------------------------
 constexpr int kBuckets = 2048;
+constexpr int kPilotMinRank = 48;  // fewest sample ranks above the threshold
 
 template <int NT = kBlock>
 struct BucketShared {
@@ -256,17 +259,26 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __shared__ uint32_t range[kWaves][2];
   const int row = blockIdx.x, b = row / p.R;
   const int L = seq_len(p, b);
-  const int k = row_budget(p, b, L);
+  const RowPlan rp = row_plan(p, b, L);
+  const int k = rp.kh;
+  const int mid = rp.hi - rp.lo;  // the positions the top-k runs over
   if (threadIdx.x == 0 && row == 0) w.stats[0] = 0;
-  const int m = L < kSampleMax ? L : kSampleMax;
+  const int m = mid < kSampleMax ? mid : kSampleMax;
+  const int cap = kCandBuf / (p.group_shared ? 1 : p.G);
+  const int64_t span = mid < w.wave_keys ? mid : w.wave_keys;
   int r = k;
-  if (m < L) {
-    const int64_t rr = (5LL * k * m + 2LL * L - 1) / (2LL * L);
+  if (m < mid) {
+    const int64_t rr = (5LL * k * m + 2LL * mid - 1) / (2LL * mid);
     r = (int)(rr < m ? rr : m);
+    // A small rank leaves the candidate count a relative spread of about
+    // 1/sqrt(r): with k of a few dozen, one row in five would come up short
+    // of k.  Take at least kPilotMinRank (as far as the staging areas hold
+    // the candidates it lets through), which then passes far more than k.
+    const int64_t fit = (int64_t)cap * m / (2 * span);
+    const int rmin = (int)(kPilotMinRank < fit ? kPilotMinRank : fit);
+    if (r < rmin) r = rmin < m ? rmin : m;
     if (r < 1) r = 1;
   }
-  const int cap = kCandBuf / (p.group_shared ? 1 : p.G);
-  const int64_t span = L < w.wave_keys ? L : w.wave_keys;
   const bool dense = w.force_repair || 2LL * r * span > (int64_t)cap * m;
   if (k == 0 || dense) {
     if (threadIdx.x == 0) {
@@ -358,6 +370,11 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   if (c0 >= L) return;  // whole workgroup (every wave has the same chunk)
   const int64_t w0 = QUAD ? c0 : c0 + (int64_t)wv * wk;
   const int nvalid = w0 < L ? (int)((L - w0) < wk ? (L - w0) : wk) : 0;
+  // Candidates lie in the top-k range [lo, hi) of the sequence (forced
+  // positions are kept apart): wave-relative, [jlo, jhi).
+  const RowPlan rp = row_plan(p, b, L);
+  const int jlo = rp.lo > w0 ? (int)(rp.lo - w0) : 0;
+  const int jhi = (int)((int64_t)rp.hi - w0 < nvalid ? (int64_t)rp.hi - w0 : nvalid);
   const int l = lane_id(), col = l & 15, s = l >> 4;
   const int64_t row0 = GRP ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
   const int nrows = GRP ? 1 : p.G;
@@ -413,7 +430,7 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
     // Append the passing keys of one scored tile to their rows' areas;
     // keys past an area's end go to this lane's discard slot.
     auto filter = [&](f32x4 acc, int jl) {
-      const bool live = jl < nvalid;
+      const bool live = jl >= jlo && jl < jhi;
       if (GRP) acc[0] = group_sum(acc);
 #pragma unroll
       for (int r = 0; r < (GRP ? 1 : 4); ++r) {
@@ -622,7 +639,7 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   const int part = blockIdx.x, bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
   const int nrows = p.group_shared ? 1 : p.G;
   const int L = seq_len(p, b);
-  const int k = row_budget(p, b, L);
+  const int k = row_plan(p, b, L).kh;
   const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
   const int tid = threadIdx.x;
   if (tid < kMaxGroup) {
@@ -661,9 +678,10 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
 // kept scores (or -inf), when vals is not null.
 // ---------------------------------------------------------------------------
 struct DenseSrc {
-  const float *row;
+  const float *row;  // scores of positions base, base + 1, ...
+  uint32_t base;
   __device__ __forceinline__ uint32_t key(int i) const { return f2key(row[i]); }
-  __device__ __forceinline__ uint32_t pos(int i) const { return (uint32_t)i; }
+  __device__ __forceinline__ uint32_t pos(int i) const { return base + (uint32_t)i; }
 };
 
 // The candidates of one row, chunk by chunk: chunk c contributes
@@ -781,16 +799,23 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
   __shared__ BucketShared<NT> bs;
   bool weights_done = false;
   const int row = blockIdx.x, b = row / p.R;
-  const bool weights = MODE != 1 && !p.group_shared;
   const int L = seq_len(p, b);
-  const int k = row_budget(p, b, L);
-  int32_t *irow = idx + (int64_t)row * p.k_max;
-  float *vrow = vals ? vals + (int64_t)row * p.k_max : nullptr;
+  // The row's list: its forced sinks, the exact top-k of [lo, hi), then its
+  // forced local window.
+  const RowPlan rp = row_plan(p, b, L);
+  const bool forced = rp.ns + rp.nl > 0;
+  const bool weights = MODE != 1 && !p.group_shared && !forced;
+  const int k = rp.kh;
+  int32_t *lrow = idx + (int64_t)row * p.k_max;
+  float *lvals = vals ? vals + (int64_t)row * p.k_max : nullptr;
+  int32_t *irow = lrow + rp.ns;
+  float *vrow = lvals ? lvals + rp.ns : nullptr;
   const int tid = threadIdx.x;
   if (k > 0) {
     if (MODE == 0 && w.flags[row]) {  // the exact fallback: full scores
       if (tid == 0) atomicAdd(&w.stats[0], 1);
-      select_and_write<NT>(DenseSrc{w.dense + (int64_t)row * p.ncap}, L, k, hist, &sh, irow, vrow);
+      select_and_write<NT>(DenseSrc{w.dense + (int64_t)row * p.ncap + rp.lo, (uint32_t)rp.lo},
+                           rp.hi - rp.lo, k, hist, &sh, irow, vrow);
     } else if (MODE == 0) {
       // Candidates: at least k of them and no overflow (else flagged).
       const int ck = w.chunk_keys;
@@ -847,13 +872,22 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
         select_and_write<NT>(src, total, k, hist, &sh, irow, vrow);
       }
     } else {
-      select_and_write<NT>(DenseSrc{dense + (int64_t)row * ld}, L, k, hist, &sh, irow, vrow);
+      select_and_write<NT>(DenseSrc{dense + (int64_t)row * ld + rp.lo, (uint32_t)rp.lo},
+                           rp.hi - rp.lo, k, hist, &sh, irow, vrow);
     }
     if (weights && !weights_done) kept_scores_to_weights<NT>(vrow, k, p.scale, ftmp);
   }
-  for (int i = k + tid; i < p.k_max; i += NT) {
-    irow[i] = -1;
-    if (vrow) vrow[i] = -__builtin_inff();
+  // Forced positions (their scores, for the stand-alone selection), then
+  // the padding.
+  for (int i = tid; i < rp.ns + rp.nl; i += NT) {
+    const int slot = i < rp.ns ? i : rp.ns + k + (i - rp.ns);
+    const int pos = i < rp.ns ? i : rp.hi + (i - rp.ns);
+    lrow[slot] = pos;
+    if (lvals) lvals[slot] = MODE == 1 ? dense[(int64_t)row * ld + pos] : 0.f;
+  }
+  for (int i = rp.total + tid; i < p.k_max; i += NT) {
+    lrow[i] = -1;
+    if (lvals) lvals[i] = -__builtin_inff();
   }
 }
 
@@ -923,11 +957,13 @@ __device__ __forceinline__ void store_out(void *out, int64_t off, float v) {
 }
 
 __device__ __forceinline__ int attend_list_len(const Params &p, int b, int L, bool fused) {
-  return fused ? row_budget(p, b, L) : p.k_max;
+  return fused ? row_plan(p, b, L).total : p.k_max;
 }
 
-__host__ __device__ inline bool attend_recompute(bool fused, int group_shared) {
-  return !fused || group_shared;
+// Logits are recomputed from the key rows unless the selection formed the
+// softmax weights already (fused per-head rows without forced positions).
+__host__ __device__ inline bool attend_recompute(bool fused, const Params &p) {
+  return !fused || p.group_shared || p.n_sink + p.n_local > 0;
 }
 
 // Byte offsets of the dynamic LDS areas of k_attend (host and device agree).
@@ -967,7 +1003,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   const int n_list = attend_list_len(p, b, L, FUSED);
   const int nsp = (n_list + split - 1) / split;
   const int tid = threadIdx.x, l = lane_id(), col = l & 15, sub = l >> 4, wv = wave_id();
-  const bool recompute = attend_recompute(FUSED, grp);
+  const bool recompute = attend_recompute(FUSED, p);
   const AttLds lay(split, nh, recompute);
   char *dyn = (char *)att_dyn;
   int64_t *voff_l = (int64_t *)(dyn + lay.voff);
@@ -1300,6 +1336,7 @@ hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st) {
 
 constexpr int kAttendWorkgroups = 1024;   // enough to fill the chip
 constexpr int kAttendLdsMax = 60 * 1024;  // dynamic LDS of one attend workgroup
+constexpr int kAttendMinEntries = 64;     // fewest list entries worth a workgroup of their own
 
 // Positions per attend workgroup: about kAttendWorkgroups workgroups over
 // all rows, at least 64 positions each, within the LDS budget.
@@ -1307,9 +1344,9 @@ int attend_split(const Params &p, int k_max_positions, bool fused) {
   const int64_t rows = (int64_t)p.B * p.R;
   const int64_t k_max = k_max_positions > 0 ? k_max_positions : 1;
   const int nh = p.group_shared ? p.G : 1;
-  const bool rc = attend_recompute(fused, p.group_shared);
+  const bool rc = attend_recompute(fused, p);
   int64_t nsplit = (kAttendWorkgroups + rows - 1) / rows;
-  const int64_t most = (k_max + 63) / 64;
+  const int64_t most = (k_max + kAttendMinEntries - 1) / kAttendMinEntries;
   if (nsplit > most) nsplit = most;
   if (nsplit < 1) nsplit = 1;
   int64_t split = (k_max + nsplit - 1) / nsplit;
@@ -1335,7 +1372,7 @@ hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, voi
                          hipStream_t st) {
   const int split = attend_split(p, p.k_max, fused);
   const size_t lds = (size_t)AttLds(split, p.group_shared ? p.G : 1,
-                                    attend_recompute(fused, p.group_shared)).total;
+                                    attend_recompute(fused, p)).total;
   const int64_t kk = p.k_max > 0 ? p.k_max : 1;
   const int nsplit = (int)((kk + split - 1) / split);
   const dim3 grid(nsplit, p.B * p.R);

@@ -50,7 +50,8 @@ class SdKv(C.Structure):
 
 class SdSparsity(C.Structure):
     _fields_ = [("ratio", C.c_double), ("k_rounding", C.c_int32), ("group_shared", C.c_int32),
-                ("softmax_scale", C.c_float), ("k_override", C.c_void_p)]
+                ("softmax_scale", C.c_float), ("k_override", C.c_void_p),
+                ("n_sink", C.c_int32), ("n_local", C.c_int32)]
 
 
 class SdProfile(C.Structure):
@@ -121,13 +122,16 @@ class Sparsity:
     group_shared: bool = False
     softmax_scale: float = 0.0          # <= 0: 1/sqrt(128)
     k_override: Optional[torch.Tensor] = None   # int32 [B] on the device
+    n_sink: int = 0                     # first positions always kept
+    n_local: int = 0                    # last positions always kept
 
     def c(self) -> SdSparsity:
         ko = self.k_override
         if ko is not None:
             _need_device(ko, "k_override", torch.int32)
         return SdSparsity(float(self.ratio), int(self.rounding), int(bool(self.group_shared)),
-                          float(self.softmax_scale), ko.data_ptr() if ko is not None else None)
+                          float(self.softmax_scale), ko.data_ptr() if ko is not None else None,
+                          int(self.n_sink), int(self.n_local))
 
 
 @dataclasses.dataclass
@@ -389,4 +393,6 @@ def cache_from_inputs(inp, device="cuda") -> tuple:
 
 
 def sparsity_from_inputs(inp, **kw) -> Sparsity:
+    kw.setdefault("n_sink", int(getattr(inp, "n_sink", 0) or 0))
+    kw.setdefault("n_local", int(getattr(inp, "n_local", 0) or 0))
     return Sparsity(ratio=inp.ratio, rounding=inp.rounding, group_shared=inp.group_shared, **kw)

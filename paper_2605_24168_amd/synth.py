@@ -66,6 +66,8 @@ class DecodeInputs:
     page_size: int = PAGE_SIZE
     block_table: Optional[np.ndarray] = None   # int32 [B, max_pages] (paged)
     planted: Optional[dict] = None             # (b, g) -> (positions, heads)
+    n_sink: int = 0                            # forced first positions (0 = none)
+    n_local: int = 0                           # forced last positions (0 = none)
 
     @property
     def G(self) -> int:
@@ -187,7 +189,8 @@ def make_inputs(cfg: int, seed: int = 0, *, B: Optional[int] = None, N: Optional
                 seq_lens: Optional[list] = None, ncap: Optional[int] = None,
                 layout: Optional[str] = None, dtype: Optional[str] = None,
                 ratio: Optional[float] = None, group_shared: Optional[bool] = None,
-                threads: Optional[int] = None) -> DecodeInputs:
+                threads: Optional[int] = None, n_sink: int = 0,
+                n_local: int = 0) -> DecodeInputs:
     """Draw the inputs of workload ``cfg`` (1..5).  Keyword overrides shrink or
     reshape a workload for tests (e.g. a ragged batch with ``seq_lens``)."""
     s = dataclasses.replace(DEFAULTS[cfg])
@@ -303,7 +306,7 @@ def make_inputs(cfg: int, seed: int = 0, *, B: Optional[int] = None, N: Optional
         name=NAMES[cfg], B=s.B, Hq=s.Hq, Hkv=s.Hkv, d=d, dtype=s.dtype, q=q, k=k, v=v,
         seq_lens=lens, layout=s.layout, ncap=int(ncap), ratio=float(s.ratio),
         rounding=s.rounding, group_shared=bool(s.group_shared), page_size=PAGE_SIZE,
-        block_table=block_table, planted=planted)
+        block_table=block_table, planted=planted, n_sink=int(n_sink), n_local=int(n_local))
 
 
 def index_sets(inp: DecodeInputs, k: int, seed: int = 0, k_max: Optional[int] = None,

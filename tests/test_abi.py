@@ -71,8 +71,8 @@ def paged(sd, P=100, Hkv=8, d=128, page=16, max_pages=64, dtype=None):
     return kv
 
 
-def sparsity(sd, ratio=20.0, rounding=0, group=0, scale=0.0):
-    return sd.SdSparsity(ratio, rounding, group, scale, None)
+def sparsity(sd, ratio=20.0, rounding=0, group=0, scale=0.0, sink=0, local=0):
+    return sd.SdSparsity(ratio, rounding, group, scale, None, sink, local)
 
 
 def call_attention(sd, q, K, V, lens, sp, out, idx):
@@ -226,6 +226,26 @@ def test_budget_rule_matches_the_printed_k_values(sd):
     assert f(1048576, 100) == 10486 and f(8192, 50, 1) == 164 and f(131072, 50, 1) == 2622
     assert f(0, 10) == 0 and f(3, 100) == 1 and f(10, 0.5) == 10
     assert f(10, 0.0) == -1
+
+
+def test_forced_positions_in_the_budget_and_checks(sd):
+    f = lambda L, s, ns, nl: sd.lib.sparse_decode_budget(L, C.byref(sparsity(sd, s, 0, 0, 0.0,
+                                                                              ns, nl)))
+    assert f(4096, 20, 128, 128) == 128 + 128 + 205
+    assert f(4096, 20, 64, 0) == 64 + 205
+    assert f(100, 10, 64, 64) == 100          # windows cover the sequence: no heavy budget
+    assert f(300, 10, 64, 64) == 64 + 64 + 30
+    assert f(0, 10, 64, 64) == 0
+    assert f(4096, 20, -1, 0) == -1
+    q, K, V, lens, sp, out, idx = valid_parts(sd)
+    sp.n_sink, sp.n_local = 128, 128
+    assert call_attention(sd, q, K, V, lens, sp, out, idx) == -1   # idx too short now
+    idx.shape[2] = 461
+    out.data = None
+    assert call_attention(sd, q, K, V, lens, sp, out, idx) == -1   # only out's pointer is wrong
+    out.data = FAKE
+    sp.n_local = -1
+    assert call_attention(sd, q, K, V, lens, sp, out, idx) == -1
 
 
 def test_workspace_size_and_status_strings(sd):
