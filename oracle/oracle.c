@@ -241,10 +241,24 @@ typedef struct {
   const oracle_cache *V;
   const int32_t *seq_lens;
   int32_t group_shared;
+  /* Low-channel indexer (Double Sparsity, Table 2 and Section 4): when lab
+   * is set, selection scores come from a label cache holding nlab of the
+   * d channels of every key; column c of KV head g's labels is channel
+   * channels[g * nlab + c] (the query's channel it multiplies). */
+  const oracle_cache *lab;
+  int nlab;
+  const int32_t *channels;
 } problem;
 
 static int check_problem(const problem *p, int need_v) {
   if (p->B < 0 || p->Hq <= 0 || p->Hkv <= 0 || p->d <= 0) return ORACLE_EINVAL;
+  if (p->lab) {
+    if (p->nlab <= 0 || p->nlab > p->d || !p->channels) return ORACLE_EINVAL;
+    for (int64_t i = 0; i < (int64_t)p->Hkv * p->nlab; ++i)
+      if (p->channels[i] < 0 || p->channels[i] >= p->d) return ORACLE_EINVAL;
+    for (int b = 0; b < p->B; ++b)
+      if (p->seq_lens[b] < 0 || check_cache(p->lab, b, p->seq_lens[b])) return ORACLE_EINVAL;
+  }
   if (p->Hq % p->Hkv != 0) return ORACLE_EINVAL;
   if (!p->q || !p->K || !p->seq_lens) return ORACLE_EINVAL;
   if (need_v && !p->V) return ORACLE_EINVAL;
@@ -270,12 +284,23 @@ static void row_scores(const problem *p, int b, int row, double *qbuf,
   int h0 = p->group_shared ? row * G : row;
   int nh = p->group_shared ? G : 1;
   for (int64_t j = 0; j < L; ++j) {
-    load_vec(p->K->data, p->K->dtype, cache_row_offset(p->K, p->Hkv, p->d, b, g, j),
-             p->d, kbuf);
     double s = 0.0;
-    for (int t = 0; t < nh; ++t) {
-      load_vec(p->q, p->q_dtype, ((int64_t)b * p->Hq + h0 + t) * p->d, p->d, qbuf);
-      s += dot(qbuf, kbuf, p->d);
+    if (p->lab) {
+      /* Approximate score: the query's label channels times the key's labels. */
+      const int32_t *ch = p->channels + (int64_t)g * p->nlab;
+      load_vec(p->lab->data, p->lab->dtype, cache_row_offset(p->lab, p->Hkv, p->nlab, b, g, j),
+               p->nlab, kbuf);
+      for (int t = 0; t < nh; ++t) {
+        load_vec(p->q, p->q_dtype, ((int64_t)b * p->Hq + h0 + t) * p->d, p->d, qbuf);
+        for (int c = 0; c < p->nlab; ++c) s += qbuf[ch[c]] * kbuf[c];
+      }
+    } else {
+      load_vec(p->K->data, p->K->dtype, cache_row_offset(p->K, p->Hkv, p->d, b, g, j),
+               p->d, kbuf);
+      for (int t = 0; t < nh; ++t) {
+        load_vec(p->q, p->q_dtype, ((int64_t)b * p->Hq + h0 + t) * p->d, p->d, qbuf);
+        s += dot(qbuf, kbuf, p->d);
+      }
     }
     out[j] = s;
   }
@@ -289,6 +314,7 @@ static problem make_problem(int B, int Hq, int Hkv, int d, const void *q,
   p.B = B; p.Hq = Hq; p.Hkv = Hkv; p.d = d;
   p.q = q; p.q_dtype = q_dtype; p.K = K; p.V = V;
   p.seq_lens = seq_lens; p.group_shared = group_shared;
+  p.lab = NULL; p.nlab = 0; p.channels = NULL;
   return p;
 }
 
@@ -303,14 +329,13 @@ static int set_threads(int nthreads) {
 }
 
 /* Scores of every row: out[b][row][j] for j < L_b; NaN for L_b <= j < ncap. */
-int32_t oracle_scores(int B, int Hq, int Hkv, int d, const void *q,
-                      int32_t q_dtype, const oracle_cache *K,
-                      const int32_t *seq_lens, int32_t group_shared,
-                      int64_t ncap, double *out, int nthreads) {
-  problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, K, NULL, seq_lens, group_shared);
+static int32_t scores_impl(const problem *pp, int64_t ncap, double *out, int nthreads) {
+  const problem p = *pp;
+  int B = p.B, d = p.d;
+  const int32_t *seq_lens = p.seq_lens;
   int rc = check_problem(&p, 0);
   if (rc) return rc;
-  int R = group_shared ? Hkv : Hq;
+  int R = p.group_shared ? p.Hkv : p.Hq;
   for (int b = 0; b < B; ++b)
     if (seq_lens[b] > ncap) return ORACLE_EINVAL;
   set_threads(nthreads);
@@ -326,6 +351,28 @@ int32_t oracle_scores(int B, int Hq, int Hkv, int d, const void *q,
     free(qbuf);
   }
   return failed ? ORACLE_ENOMEM : ORACLE_OK;
+}
+
+int32_t oracle_scores(int B, int Hq, int Hkv, int d, const void *q,
+                      int32_t q_dtype, const oracle_cache *K,
+                      const int32_t *seq_lens, int32_t group_shared,
+                      int64_t ncap, double *out, int nthreads) {
+  problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, K, NULL, seq_lens, group_shared);
+  return scores_impl(&p, ncap, out, nthreads);
+}
+
+/* Approximate selection scores of the low-channel indexer: for position j,
+ * the sum over label columns c of q[channels[g][c]] * labels[j][c] (summed
+ * over the group's query heads in group-shared mode).  NaN at j >= L_b. */
+int32_t oracle_label_scores(int B, int Hq, int Hkv, int d, const void *q,
+                            int32_t q_dtype, const oracle_cache *labels, int nlab,
+                            const int32_t *channels, const int32_t *seq_lens,
+                            int32_t group_shared, int64_t ncap, double *out, int nthreads) {
+  problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, labels, NULL, seq_lens, group_shared);
+  p.lab = labels;
+  p.nlab = nlab;
+  p.channels = channels;
+  return scores_impl(&p, ncap, out, nthreads);
 }
 
 /*
@@ -489,16 +536,13 @@ int32_t oracle_attend_weighted(int B, int Hq, int Hkv, int d, const void *q,
  * idx: [B][R][k_max] ascending positions then -1.  tau: [B][R] k-th largest
  * selection score (NaN when k = 0), nullable.  out, absw: [B][Hq][d].
  */
-int32_t oracle_sparse_attention(int B, int Hq, int Hkv, int d, const void *q,
-                                int32_t q_dtype, const oracle_cache *K,
-                                const oracle_cache *V, const int32_t *seq_lens,
-                                double ratio, int32_t rounding,
-                                int32_t group_shared, double scale,
-                                const int32_t *k_override, int64_t n_sink,
-                                int64_t n_local, int64_t k_max,
-                                int32_t *idx, double *tau, double *out,
-                                double *absw, int nthreads) {
-  problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared);
+static int32_t sparse_attention_impl(const problem *pp, double ratio, int32_t rounding,
+                                     double scale, const int32_t *k_override, int64_t n_sink,
+                                     int64_t n_local, int64_t k_max, int32_t *idx, double *tau,
+                                     double *out, double *absw, int nthreads) {
+  const problem p = *pp;
+  int B = p.B, Hq = p.Hq, Hkv = p.Hkv, d = p.d, group_shared = p.group_shared;
+  const int32_t *seq_lens = p.seq_lens;
   int rc = check_problem(&p, 1);
   if (rc) return rc;
   if (!idx || !out || !(ratio > 0.0) || n_sink < 0 || n_local < 0) return ORACLE_EINVAL;
@@ -524,8 +568,44 @@ int32_t oracle_sparse_attention(int B, int Hq, int Hkv, int d, const void *q,
     free(buf);
   }
   if (rc_all) return rc_all;
-  return oracle_attend(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared,
+  return oracle_attend(B, Hq, Hkv, d, p.q, p.q_dtype, p.K, p.V, seq_lens, group_shared,
                        scale, k_max, idx, out, absw, nthreads);
+}
+
+int32_t oracle_sparse_attention(int B, int Hq, int Hkv, int d, const void *q,
+                                int32_t q_dtype, const oracle_cache *K,
+                                const oracle_cache *V, const int32_t *seq_lens,
+                                double ratio, int32_t rounding,
+                                int32_t group_shared, double scale,
+                                const int32_t *k_override, int64_t n_sink,
+                                int64_t n_local, int64_t k_max,
+                                int32_t *idx, double *tau, double *out,
+                                double *absw, int nthreads) {
+  problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared);
+  return sparse_attention_impl(&p, ratio, rounding, scale, k_override, n_sink, n_local, k_max,
+                               idx, tau, out, absw, nthreads);
+}
+
+/*
+ * The method with the low-channel indexer in place of exact scores (Table 2:
+ * an 8-channel, 16-bit Double Sparsity indexer chooses the positions): the
+ * top-k (with any forced positions) runs on the label scores above; the
+ * attention over the kept positions uses the full keys and values.
+ */
+int32_t oracle_label_attention(int B, int Hq, int Hkv, int d, const void *q,
+                               int32_t q_dtype, const oracle_cache *K,
+                               const oracle_cache *V, const oracle_cache *labels, int nlab,
+                               const int32_t *channels, const int32_t *seq_lens,
+                               double ratio, int32_t rounding, int32_t group_shared,
+                               double scale, const int32_t *k_override, int64_t n_sink,
+                               int64_t n_local, int64_t k_max, int32_t *idx, double *tau,
+                               double *out, double *absw, int nthreads) {
+  problem p = make_problem(B, Hq, Hkv, d, q, q_dtype, K, V, seq_lens, group_shared);
+  p.lab = labels;
+  p.nlab = nlab;
+  p.channels = channels;
+  return sparse_attention_impl(&p, ratio, rounding, scale, k_override, n_sink, n_local, k_max,
+                               idx, tau, out, absw, nthreads);
 }
 
 /* Number of threads OpenMP will use for the next parallel region. */

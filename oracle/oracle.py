@@ -72,6 +72,16 @@ def lib() -> C.CDLL:
             C.POINTER(_Cache), C.c_void_p, C.c_double, C.c_int32, C.c_int32, C.c_double,
             C.c_void_p, C.c_int64, C.c_int64, C.c_int64, C.c_void_p, C.c_void_p, C.c_void_p,
             C.c_void_p, C.c_int]
+        L.oracle_label_scores.restype = C.c_int32
+        L.oracle_label_scores.argtypes = [C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p,
+                                          C.c_int32, C.POINTER(_Cache), C.c_int, C.c_void_p,
+                                          C.c_void_p, C.c_int32, C.c_int64, C.c_void_p, C.c_int]
+        L.oracle_label_attention.restype = C.c_int32
+        L.oracle_label_attention.argtypes = [
+            C.c_int, C.c_int, C.c_int, C.c_int, C.c_void_p, C.c_int32, C.POINTER(_Cache),
+            C.POINTER(_Cache), C.POINTER(_Cache), C.c_int, C.c_void_p, C.c_void_p, C.c_double,
+            C.c_int32, C.c_int32, C.c_double, C.c_void_p, C.c_int64, C.c_int64, C.c_int64,
+            C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_int]
         L.oracle_max_threads.restype = C.c_int32
         L.oracle_max_threads.argtypes = [C.c_int]
         _lib = L
@@ -297,6 +307,50 @@ def sparse_attention(inp, k_max: int | None = None, k_override=None, scale: floa
         int(inp.group_shared), float(scale), _ptr(ko), *forced_of(inp), int(k_max),
         idx.ctypes.data, tau.ctypes.data, out.ctypes.data, absw.ctypes.data, nthreads),
         "sparse_attention")
+    return {"idx": idx, "tau": tau, "out": out, "absw": absw}
+
+
+def label_scores(inp, labels: np.ndarray, channels: np.ndarray, nthreads: int = 0) -> np.ndarray:
+    """float64 approximate scores [B, R, ncap] of the low-channel indexer
+    (NaN at j >= L_b).  labels: the label cache in the step's layout with
+    nlab channels per key; channels: int32 [Hkv, nlab], the query channel
+    each label column multiplies."""
+    keep: list = []
+    lab = _cache(inp, labels, keep)
+    ch = np.ascontiguousarray(channels, dtype=np.int32)
+    q = np.ascontiguousarray(inp.q)
+    lens = np.ascontiguousarray(inp.seq_lens, dtype=np.int32)
+    out = np.empty((inp.B, inp.rows, inp.ncap), dtype=np.float64)
+    _check(lib().oracle_label_scores(inp.B, inp.Hq, inp.Hkv, inp.d, q.ctypes.data,
+                                     _dtype_code(inp.dtype), C.byref(lab), ch.shape[1],
+                                     ch.ctypes.data, lens.ctypes.data, int(inp.group_shared),
+                                     inp.ncap, out.ctypes.data, nthreads), "label_scores")
+    return out
+
+
+def label_attention(inp, labels: np.ndarray, channels: np.ndarray, k_max: int | None = None,
+                    k_override=None, scale: float = 0.0, nthreads: int = 0) -> dict:
+    """The method with the low-channel indexer choosing the positions:
+    returns dict(idx, tau, out, absw)."""
+    keep: list = []
+    K = _cache(inp, inp.k, keep)
+    V = _cache(inp, inp.v, keep)
+    lab = _cache(inp, labels, keep)
+    ch = np.ascontiguousarray(channels, dtype=np.int32)
+    q = np.ascontiguousarray(inp.q)
+    lens = np.ascontiguousarray(inp.seq_lens, dtype=np.int32)
+    k_max = k_max_for(inp) if k_max is None else k_max
+    ko = None if k_override is None else np.ascontiguousarray(k_override, dtype=np.int32)
+    idx = np.empty((inp.B, inp.rows, k_max), dtype=np.int32)
+    tau = np.empty((inp.B, inp.rows), dtype=np.float64)
+    out = np.empty((inp.B, inp.Hq, inp.d), dtype=np.float64)
+    absw = np.empty_like(out)
+    _check(lib().oracle_label_attention(
+        inp.B, inp.Hq, inp.Hkv, inp.d, q.ctypes.data, _dtype_code(inp.dtype), C.byref(K),
+        C.byref(V), C.byref(lab), ch.shape[1], ch.ctypes.data, lens.ctypes.data,
+        float(inp.ratio), int(inp.rounding), int(inp.group_shared), float(scale), _ptr(ko),
+        *forced_of(inp), int(k_max), idx.ctypes.data, tau.ctypes.data, out.ctypes.data,
+        absw.ctypes.data, nthreads), "label_attention")
     return {"idx": idx, "tau": tau, "out": out, "absw": absw}
 
 

@@ -290,6 +290,98 @@ def test_forced_positions_in_the_whole_method():
 
 
 # --------------------------------------------------------------------------
+# Low-channel indexer (label cache of a few channels per key).
+# --------------------------------------------------------------------------
+
+def _labels_from(K, channels):
+    """Label cache [B, Hkv, N, nlab] holding each KV head's label channels."""
+    B, Hkv, N, d = K.shape
+    return np.stack([K[:, g][:, :, channels[g]] for g in range(Hkv)], axis=1)
+
+
+def test_label_scores_are_integer_exact():
+    rng = np.random.default_rng(41)
+    B, Hq, Hkv, N, d, nl = 2, 6, 3, 19, 16, 4
+    q = rng.integers(-4, 5, (B, Hq, d)).astype(np.float32)
+    K = rng.integers(-4, 5, (B, Hkv, N, d)).astype(np.float32)
+    ch = np.stack([rng.choice(d, nl, replace=False) for _ in range(Hkv)]).astype(np.int32)
+    lab = rng.integers(-4, 5, (B, Hkv, N, nl)).astype(np.float32)   # independent of K
+    p = problem(q, K, K, Hkv=Hkv)
+    got = O.label_scores(p, lab, ch)
+    G = Hq // Hkv
+    qi, li = q.astype(np.int64), lab.astype(np.int64)
+    for b in range(B):
+        for h in range(Hq):
+            g = h // G
+            want = li[b, g] @ qi[b, h, ch[g]]
+            np.testing.assert_array_equal(got[b, h], want.astype(np.float64))
+    # Group-shared rows sum their heads; permuting label columns together
+    # with their channels changes nothing.
+    pg = problem(q, K, K, Hkv=Hkv, group_shared=True)
+    gs = O.label_scores(pg, lab, ch)
+    for b in range(B):
+        for g in range(Hkv):
+            np.testing.assert_array_equal(gs[b, g], got[b, g * G:(g + 1) * G].sum(axis=0))
+    perm = rng.permutation(nl)
+    np.testing.assert_array_equal(O.label_scores(p, lab[..., perm], ch[:, perm]), got)
+
+
+def test_label_indexer_with_the_channels_q_uses_is_the_exact_method():
+    # When q is zero outside the label channels and the labels are those
+    # channels of K, the approximate scores are the exact ones: the same
+    # sets and outputs as the exact method (channels ascending keep the
+    # summation order, so bit for bit).
+    rng = np.random.default_rng(42)
+    B, Hq, Hkv, N, d, nl = 2, 4, 2, 64, 32, 8
+    ch = np.stack([np.sort(rng.choice(d, nl, replace=False)) for _ in range(Hkv)]).astype(np.int32)
+    q = rng.standard_normal((B, Hq, d)).astype(np.float32)
+    G = Hq // Hkv
+    for h in range(Hq):
+        mask = np.zeros(d, bool)
+        mask[ch[h // G]] = True
+        q[:, h, ~mask] = 0.0
+    K = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    V = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    p = problem(q, K, V, Hkv=Hkv, ratio=8.0, seq_lens=[64, 37])
+    lab = _labels_from(K, ch)
+    np.testing.assert_array_equal(O.label_scores(p, lab, ch), O.scores(p))
+    a, e = O.label_attention(p, lab, ch), O.sparse_attention(p)
+    np.testing.assert_array_equal(a["idx"], e["idx"])
+    np.testing.assert_array_equal(a["out"], e["out"])
+
+
+def test_label_indexer_selects_on_labels_and_attends_on_full_keys():
+    rng = np.random.default_rng(43)
+    B, Hq, Hkv, N, d, nl = 1, 2, 1, 40, 16, 2
+    q = rng.standard_normal((B, Hq, d)).astype(np.float32)
+    K = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    V = rng.standard_normal((B, Hkv, N, d)).astype(np.float32)
+    ch = np.array([[3, 11]], np.int32)
+    lab = rng.standard_normal((B, Hkv, N, nl)).astype(np.float32)
+    p = problem(q, K, V, Hkv=Hkv, ratio=8.0)                    # k = 5
+    r = O.label_attention(p, lab, ch)
+    ls = O.label_scores(p, lab, ch)
+    for h in range(Hq):
+        want, tau = O.select_row(ls[0, h], 5)
+        np.testing.assert_array_equal(r["idx"][0, h], want)     # chosen by label scores
+        assert r["tau"][0, h] == tau
+    out, _ = O.attend(p, r["idx"])                              # attended with full K, V
+    np.testing.assert_array_equal(r["out"], out)
+    # The paged layout gives the same result; forced positions apply too.
+    pp = to_paged(p, 4, seed=1)
+    lab_p = np.full((pp.k.shape[0], 4, Hkv, nl), 99.0, np.float32)
+    for j in range(N):
+        page = pp.block_table[0, j // 4]
+        lab_p[page, j % 4] = lab[0, :, j]
+    np.testing.assert_array_equal(O.label_attention(pp, lab_p, ch)["idx"], r["idx"])
+    p.n_sink, p.n_local = 2, 3
+    f = O.label_attention(p, lab, ch)
+    for h in range(Hq):
+        want, _ = O.select_forced(ls[0, h], 2, 3, 5)
+        np.testing.assert_array_equal(f["idx"][0, h], want)
+
+
+# --------------------------------------------------------------------------
 # Attention: dense limit, special cases, invariants.
 # --------------------------------------------------------------------------
 

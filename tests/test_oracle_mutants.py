@@ -44,8 +44,12 @@ MUTANTS = {
                                         "int rc = oracle_select_row(scores, mid, kh, kh, idx + ns, tau);"),
     "local_window_off_by_one": ("idx[ns + kh + t] = (int32_t)(L - nl + t);",
                                 "idx[ns + kh + t] = (int32_t)(L - nl + t - 1);"),
-    "row_scores_skip_last_position": ("for (int64_t j = 0; j < L; ++j) {\n    load_vec(p->K->data",
-                                      "for (int64_t j = 0; j + 1 < L; ++j) {\n    load_vec(p->K->data"),
+    "label_channel_ignored": ("for (int c = 0; c < p->nlab; ++c) s += qbuf[ch[c]] * kbuf[c];",
+                              "for (int c = 0; c < p->nlab; ++c) s += qbuf[c] * kbuf[c];"),
+    "label_channels_of_head_0": ("const int32_t *ch = p->channels + (int64_t)g * p->nlab;",
+                                 "const int32_t *ch = p->channels;"),
+    "row_scores_skip_last_position": ("for (int64_t j = 0; j < L; ++j) {\n    double s = 0.0;\n    if (p->lab)",
+                                      "for (int64_t j = 0; j + 1 < L; ++j) {\n    double s = 0.0;\n    if (p->lab)"),
 }
 
 
