@@ -43,19 +43,21 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def path_bytes(inp, ks):
-    """Algorithmic HBM bytes of one step: every key once, the kept value rows,
-    q, out and idx.  (Per-head mode gathers one value row per query head and
-    kept position, plus its key row when forced positions make the attention
-    recompute its logits; group-shared mode one key and one value row per KV
-    head.)"""
+def path_bytes(inp, ks, labels=False):
+    """Algorithmic HBM bytes of one step: every key (or, with the label
+    indexer, every 16-byte label row) once, the kept value rows, q, out and
+    idx.  (Per-head mode gathers one value row per query head and kept
+    position, plus its key row when the attention recomputes its logits:
+    forced positions or label selection; group-shared mode one key and one
+    value row per KV head.)"""
     e = 2 if inp.dtype == "bf16" else 4
     row = inp.d * e
-    key_stream = sum(int(L) for L in inp.seq_lens) * inp.Hkv * row
+    key_stream = sum(int(L) for L in inp.seq_lens) * inp.Hkv * (16 if labels else row)
     if inp.group_shared:
         gather = sum(int(k) for k in ks) * inp.Hkv * 2 * row
     else:
-        per_entry = 2 * row if inp.n_sink + inp.n_local > 0 else row
+        recompute = labels or inp.n_sink + inp.n_local > 0
+        per_entry = 2 * row if recompute else row
         gather = sum(int(k) for k in ks) * inp.Hq * per_entry
     k_max = max(int(k) for k in ks)
     small = 2 * inp.B * inp.Hq * row + inp.B * inp.rows * k_max * 4
@@ -75,7 +77,7 @@ def counters_traffic():
     return c.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(inp, n_seq, k_max, fixed_k=None):
+def cpu_baseline(inp, n_seq, k_max, fixed_k=None, labels=None):
     import dataclasses
     from oracle import oracle as O
     bs = list(range(min(n_seq, inp.B)))
@@ -94,7 +96,12 @@ def cpu_baseline(inp, n_seq, k_max, fixed_k=None):
     t0 = time.perf_counter()
     import numpy as np
     ko = None if fixed_k is None else np.full(len(bs), fixed_k, np.int32)
-    O.sparse_attention(sub, k_max=k_max, k_override=ko, nthreads=threads)
+    if labels is None:
+        O.sparse_attention(sub, k_max=k_max, k_override=ko, nthreads=threads)
+    else:  # (label cache in the key cache's layout, channels)
+        lab, ch = labels
+        sub_lab = lab if inp.layout == "paged" else lab[bs]
+        O.label_attention(sub, sub_lab, ch, k_max=k_max, k_override=ko, nthreads=threads)
     dt = time.perf_counter() - t0
     return {"value": len(bs) / dt, "unit": "queries/s", "cores": used, "kind": "oracle",
             "sample": f"{len(bs)} of {inp.B} sequences ({len(bs) * inp.rows} rows), "
@@ -111,6 +118,22 @@ TABLE1_H100 = {
     4: (0.72, [0.33, 0.66, 1.64, 3.18, 7.45, 13.36, 24.25, 42.04]),
     8: (1.50, [0.38, 0.77, 1.90, 3.75, 8.88, 16.82, 29.64, 76.14]),
     16: (3.08, [0.45, 0.89, 2.21, 4.35, 10.54, 20.09, 37.32, 76.77]),
+}
+
+
+# Table 2 of the paper (H100, FP16, 128K, page 16): FlashInfer dense ms and
+# the speedup of the sparse backend with an 8-channel 16-bit Double Sparsity
+# indexer choosing the positions, GQA 32/8 and MHA 32/32.  Context only.
+TABLE2_RATIOS = [2, 5, 10, 20, 50, 100]
+TABLE2_H100 = {
+    "gqa": {1: (0.19, [0.28, 0.56, 0.83, 1.12, 1.46, 1.65]),
+            4: (0.72, [0.32, 0.67, 1.06, 1.52, 2.11, 2.45]),
+            8: (1.50, [0.36, 0.75, 1.18, 1.68, 2.30, 2.66]),
+            16: (3.08, [0.41, 0.85, 1.31, 1.82, 2.46, 2.81])},
+    "mha": {1: (0.70, [0.91, 1.62, 2.18, 2.68, 3.14, 3.37]),
+            4: (2.79, [1.02, 1.86, 2.56, 3.17, 3.74, 4.00]),
+            8: (5.61, [1.12, 2.00, 2.71, 3.32, 3.86, 4.11]),
+            16: (11.18, [1.22, 2.13, 2.84, 3.43, 3.94, 4.17])},
 }
 
 
@@ -231,6 +254,93 @@ def backend_table(args):
     print(json.dumps(rec), flush=True)
 
 
+def indexer_table(args):
+    """Table 2's shape on one MI355X: dense decode attention against the
+    method with the 8-channel label indexer choosing the positions (label
+    stream, exact top-k on label scores, attention on full keys and
+    values), batch 1/4/8/16, 128K context, GQA 32/8 and MHA 32/32, paged NHD,
+    bfloat16.  Prints one JSON line."""
+    import torch
+    from paper_2605_24168_amd import sparse_decode as sd
+    from paper_2605_24168_amd import synth
+
+    torch.cuda.set_device(0)
+    N, Hq, d = 131072, 32, 128
+    batches = [1, 4, 8, 16]
+    modes = []
+    for mode, Hkv in (("gqa", 8), ("mha", 32)):
+        log(f"drawing the 16 x 128K paged cache ({mode}, {Hq}q/{Hkv}kv) on the GPU")
+        t = synth.backend_sweep_inputs(B=max(batches), N=N, Hq=Hq, Hkv=Hkv, seed=args.seed)
+        ch_np = synth.label_channels(Hkv, seed=args.seed)
+        ch = torch.from_numpy(ch_np).cuda()
+        # label cache: each KV head's label channels of every key (bf16 copies)
+        # label cache [pages, Hkv, 16, 8]: each KV head's label channels of
+        # every key (bf16 copies), head-major inside a page
+        lab = torch.stack([t["k"][:, :, g, :].index_select(2, ch[g].long())
+                           for g in range(Hkv)], dim=1).contiguous()
+        labels = sd.Labels(t=lab, channels=ch)
+        torch.cuda.synchronize()
+        rows = []
+        for B in batches:
+            q = t["q"][:B].contiguous()
+            cache = sd.KVCache(k=t["k"], v=t["v"], layout="paged",
+                               block_table=t["block_table"][:B].contiguous())
+            lens = t["seq_lens"][:B].contiguous()
+            out = torch.empty_like(q)
+            dense_fn = lambda: sd.sparse_decode_dense_attention(q, cache, lens, out=out)
+            dense_ms, _ = time_graph(torch, dense_fn, args.steps, args.warmup)
+            kv_bytes = B * Hkv * N * d * 2 * 2
+            entry = {"batch": B, "dense_ms": round(dense_ms, 4),
+                     "dense_GBps": round(kv_bytes / (dense_ms * 1e-3) / 1e9, 1),
+                     "h100_flashinfer_ms": TABLE2_H100[mode][B][0], "indexed": {}}
+            log(f"{mode} B={B}: dense {dense_ms:.4f} ms ({entry['dense_GBps']} GB/s)")
+            for i, S in enumerate(TABLE2_RATIOS):
+                sp = sd.Sparsity(ratio=float(S))
+                k_max = sd.k_max_of(cache, sp)
+                idx = torch.empty((B, Hq, k_max), dtype=torch.int32, device="cuda")
+                ws = torch.empty(sd.workspace_size(q, cache, sp, idx), dtype=torch.uint8,
+                                 device="cuda")
+                sd.set_workspace(ws)
+                fn = lambda: sd.sparse_decode_label_attention(q, cache, labels, lens, sp, out=out,
+                                                              idx=idx)[0]
+                eager = time_calls(torch, fn, args.steps, args.warmup)
+                ms, same = time_graph(torch, fn, args.steps, args.warmup)
+                sd.set_profiling(True)
+                for _ in range(args.steps):
+                    fn()
+                torch.cuda.synchronize()
+                sd.set_profiling(False)
+                prof = sd.profile_mean()
+                sd.set_workspace(None)
+                del ws, idx
+                entry["indexed"][f"{S}x"] = {
+                    "k": int(round(N / S)), "ms": round(ms, 4), "eager_ms": round(eager, 4),
+                    "speedup": round(dense_ms / ms, 3),
+                    "h100_speedup": TABLE2_H100[mode][B][1][i],
+                    "graph_replay_matches_eager": same,
+                    "stage_ms": {k_: round(prof[k_], 4) for k_ in
+                                 ("pilot_ms", "score_ms", "select_ms", "repair_ms",
+                                  "attend_ms")},
+                    "fallback_rows": prof["repaired_rows"]}
+                log(f"  {S}x: {ms:.4f} ms, speedup {dense_ms / ms:.2f}x "
+                    f"(H100: {TABLE2_H100[mode][B][1][i]}x), stages {entry['indexed'][f'{S}x']['stage_ms']}")
+            rows.append(entry)
+        modes.append({"mode": mode, "q_heads": Hq, "kv_heads": Hkv, "rows": rows})
+        del t, lab, labels
+        torch.cuda.empty_cache()
+    rec = {
+        "table": "label indexer + sparse attention vs dense decode (Table 2 shape)",
+        "steps": args.steps, "warmup": args.warmup,
+        "config": {"head_dim": d, "context": N, "layout": "paged NHD, page 16, random page order",
+                   "dtype": "bf16", "labels": "8 bf16 channels per key, uniform random channels "
+                                              "per KV head (uncalibrated)"},
+        "timing": "ms: K calls captured in one HIP graph, replayed 5 times (kernel time); "
+                  "stage_ms: events between the stages (profiling on)",
+        "modes": modes,
+    }
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -251,6 +361,13 @@ def main():
                     help="sparsity S (top-k budget round(L/S)) instead of the workload's")
     ap.add_argument("--fixed-k", type=int, default=None,
                     help="top-k budget K for every sequence instead of the ratio rule")
+    ap.add_argument("--labels", action="store_true",
+                    help="select with the 8-channel label indexer (bf16 workloads) instead of "
+                         "exact scores")
+    ap.add_argument("--table2", action="store_true",
+                    help="instead of the default line, sweep dense decode against the method "
+                         "with the 8-channel label indexer in Table 2's shape (batch 1/4/8/16, "
+                         "2x-100x, 128K, GQA 32/8 and MHA 32/32, paged)")
     ap.add_argument("--table1", action="store_true",
                     help="instead of the default line, sweep dense decode against the "
                          "weighted sparse backend in Table 1's shape (batch 1/4/8/16, "
@@ -263,6 +380,9 @@ def main():
         sys.exit(2)
     if args.table1:
         backend_table(args)
+        return
+    if args.table2:
+        indexer_table(args)
         return
 
     import torch
@@ -295,16 +415,29 @@ def main():
     idx = torch.empty((inp.B, inp.rows, k_max), dtype=torch.int32, device="cuda")
     ws = torch.empty(sd.workspace_size(q, cache, sp, idx), dtype=torch.uint8, device="cuda")
     sd.set_workspace(ws)
+    labels = host_labels = None
+    if args.labels:
+        ch = synth.label_channels(inp.Hkv, seed=args.seed)
+        host_labels = (synth.label_cache(inp, ch), ch)
+        lab = synth.label_cache_device_layout(inp, host_labels[0])
+        labels = sd.Labels(t=torch.from_numpy(lab).view(torch.bfloat16).cuda(),
+                           channels=torch.from_numpy(ch).cuda())
     torch.cuda.synchronize()
+
+    def one_step():
+        if labels is None:
+            sd.sparse_decode_attention(q, cache, lens, sp, out=out, idx=idx)
+        else:
+            sd.sparse_decode_label_attention(q, cache, labels, lens, sp, out=out, idx=idx)
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
-        sd.sparse_decode_attention(q, cache, lens, sp, out=out, idx=idx)
+        one_step()
     torch.cuda.synchronize()
 
     def run_steps(n):
         for _ in range(n):
-            sd.sparse_decode_attention(q, cache, lens, sp, out=out, idx=idx)
+            one_step()
 
     # Timed region: K steps, uninstrumented (any HIP timing event adds about
     # 20 us per step to the path on this GPU, so none is recorded here).
@@ -352,14 +485,14 @@ def main():
                  "frac_of_peak": dense_b / (dense_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                  "sparse_speedup": dense_ms / ms_step}
 
-    key_b, gather_b, small_b = path_bytes(inp, ks)
+    key_b, gather_b, small_b = path_bytes(inp, ks, labels=args.labels)
     total_b = key_b + gather_b + small_b
     path_gbps = total_b / (ms_step * 1e-3) / 1e9
     q_bytes = inp.B * inp.Hq * inp.d * (2 if inp.dtype == "bf16" else 4)
     score_alg = key_b + q_bytes
     score_ms = score_prof["score_ms"]
     score_gbps = score_alg / (score_ms * 1e-3) / 1e9 if score_ms > 0 else None
-    traffic = counters_traffic()
+    traffic = None if args.labels else counters_traffic()  # counters are of the exact stream
 
     rec = {
         "metric": METRIC,
@@ -380,10 +513,11 @@ def main():
                    "layout": inp.layout, "group_shared": inp.group_shared,
                    **({"n_sink": inp.n_sink, "n_local": inp.n_local}
                       if inp.n_sink or inp.n_local else {}),
-                   **({"fixed_k": args.fixed_k} if args.fixed_k is not None else {})},
+                   **({"fixed_k": args.fixed_k} if args.fixed_k is not None else {}),
+                   **({"indexer": "8-channel bf16 labels"} if args.labels else {})},
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_score_stream",
+            "kernel": "k_score_stream" + (" (label rows)" if args.labels else ""),
             "achieved": score_gbps,
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
@@ -422,7 +556,8 @@ def main():
         del src, dst
     if args.cpu_sample > 0:
         log(f"timing the CPU oracle on {args.cpu_sample} sequences")
-        rec["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample, k_max, args.fixed_k)
+        rec["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample, k_max, args.fixed_k,
+                                           host_labels)
     else:
         rec["cpu_baseline"] = None
     print(json.dumps(rec), flush=True)

@@ -103,6 +103,19 @@ typedef struct {
   int32_t n_local;       /* >= 0: last positions of every sequence always kept (0 = none)      */
 } sd_sparsity;
 
+/* Label cache of the low-channel approximate indexer (Table 2 and Section 4:
+ * a Double Sparsity indexer on 8 channels of 16 bits, untuned): for every
+ * cached key, 8 of its d channels: [B, Hkv, Ncap, 8] beside a BHND cache;
+ * [P, Hkv, 16, 8] beside a paged one (the key pool's P pages, read through
+ * K's block table; head-major inside a page, so a KV head's 16 label rows
+ * of a page are one contiguous 256-byte run).  Column c
+ * of KV head g holds key channel channels[g * 8 + c]; the approximate score
+ * of a key for query head h is sum_c q_h[channels[g * 8 + c]] * label[c]. */
+typedef struct {
+  sd_tensor t;                 /* bfloat16 label cache, device memory          */
+  const int32_t *channels;     /* device int32 [Hkv, 8], values in [0, 128)    */
+} sd_labels;
+
 /* Stage timings of the last sparse_decode_attention call (profiling on). */
 typedef struct {
   float pilot_ms;      /* threshold estimation from a strided sample of keys      */
@@ -204,6 +217,26 @@ sd_status sparse_decode_dense_workspace_size(const sd_tensor *q, const sd_kv *K,
 sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
                                   const int32_t *seq_lens, const sd_sparsity *sparsity,
                                   sd_tensor *out, sd_tensor *idx, void *stream);
+
+/*
+ * The method with the low-channel indexer choosing the positions (Table 2):
+ * as sparse_decode_attention, but the exact top-k (with any forced
+ * positions) runs on the approximate label scores, one 16-byte label row per
+ * key instead of a 256-byte key row; the attention over the kept positions
+ * then uses the full keys and values.  bfloat16 only.  Uses the same
+ * workspace as sparse_decode_attention.
+ */
+sd_status sparse_decode_label_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                        const sd_labels *labels, const int32_t *seq_lens,
+                                        const sd_sparsity *sparsity, sd_tensor *out,
+                                        sd_tensor *idx, void *stream);
+
+/* Approximate label scores of every cached position, laid out as
+ * sparse_decode_score's (-infinity beyond each sequence).  K supplies the
+ * layout, capacity and block table only. */
+sd_status sparse_decode_label_score(const sd_tensor *q, const sd_kv *K, const sd_labels *labels,
+                                    const int32_t *seq_lens, const sd_sparsity *sparsity,
+                                    sd_tensor *scores, void *stream);
 
 /* Bytes of device workspace sparse_decode_attention and sparse_decode_attend
  * need for these shapes (idx gives k_max). */

@@ -143,6 +143,23 @@ sd_status check_out(const sd_tensor *out, const Shape &s, int dtype) {
   return SD_OK;
 }
 
+// A label cache of sd::kLabels bf16 channels per key: [B][Hkv][Ncap][8]
+// beside a contiguous cache, [pages][Hkv][16][8] beside a paged one.
+sd_status check_labels(const sd_labels *lab, const sd_kv *K, const Shape &s) {
+  if (!lab || !lab->t.data || !lab->channels || lab->t.ndim != 4) return SD_ERR_INVALID_ARG;
+  if (lab->t.dtype != SD_BF16 || !s.bf16) return SD_ERR_UNSUPPORTED;
+  if (lab->t.shape[3] != sd::kLabels) return SD_ERR_UNSUPPORTED;
+  if (K->layout == SD_KV_BHND) {
+    if (lab->t.shape[0] != s.B || lab->t.shape[1] != s.Hkv || lab->t.shape[2] != s.ncap)
+      return SD_ERR_INVALID_ARG;
+  } else {  // [pages][Hkv][16][8], the key pool's pages
+    if (lab->t.shape[0] != K->t.shape[0] || lab->t.shape[1] != s.Hkv ||
+        lab->t.shape[2] != K->page_size)
+      return SD_ERR_INVALID_ARG;
+  }
+  return SD_OK;
+}
+
 sd::KvView kv_view(const sd_kv *kv, int hkv, int64_t ncap) {
   sd::KvView v;
   v.base = kv->t.data;
@@ -184,13 +201,18 @@ sd::Params make_params(const sd_tensor *q, const sd_kv *K, const sd_kv *V, const
 // row, kCandBuf / rows entries, with 2x headroom.  With a sparsity ratio
 // (k ~ L / ratio) the largest wave with 2 * 2.5 * wave / ratio <= area is
 // taken (256 at least: rows that still do not fit are sent to the exact
-// fallback by the pilot); with per-sequence k the 2048-key wave.
-int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared) {
+// fallback by the pilot); with per-sequence k the 2048-key wave.  Label
+// rows are 16 bytes, so label waves go up to 8192 keys (set-up amortised
+// over as many bytes as a 512-key wave of key rows), as long as the grid
+// still has 2048 waves.
+int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool labels) {
   if (sp->k_override) return sd::kWaveKeysMax;
   const int rows = group_shared ? 1 : s.G;
   const double area = (double)(sd::kCandBuf / rows);
-  int wk = sd::kWaveKeysMax;
+  int wk = labels ? sd::kLabelWaveKeysMax : sd::kWaveKeysMax;
   while (wk > 256 && 5.0 * wk / sp->ratio > area) wk /= 2;
+  if (labels)
+    while (wk > sd::kWaveKeysMax && (int64_t)s.B * s.Hkv * ((s.ncap + wk - 1) / wk) < 2048) wk /= 2;
   return wk;
 }
 
@@ -201,11 +223,12 @@ struct Layout {
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
 };
 
-Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp) {
+Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp,
+                  bool labels = false) {
   Layout L{};
   const int group_shared = sp->group_shared ? 1 : 0;
   const int64_t rows = (int64_t)s.B * s.R;
-  L.wave_keys = wave_keys_for(s, sp, group_shared);
+  L.wave_keys = wave_keys_for(s, sp, group_shared, labels);
   // Paged caches with a multiple of 4 KV heads are scored one head per wave
   // over shared chunks of wave_keys keys (the workgroup reads four heads of
   // each page block together), unless that makes too many chunks for the
@@ -526,13 +549,23 @@ sd_status sparse_decode_dense_attention(const sd_tensor *q, const sd_kv *K, cons
   return hip_status(sd::launch_dense_attention(p, dw, out->data, (hipStream_t)stream));
 }
 
-sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
-                                  const int32_t *seq_lens, const sd_sparsity *sp, sd_tensor *out,
-                                  sd_tensor *idx, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// The fused call, with exact scores (labels null) or the low-channel
+// indexer's label scores choosing the positions.
+sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                         const sd_labels *labels, const int32_t *seq_lens,
+                         const sd_sparsity *sp, sd_tensor *out, sd_tensor *idx, void *stream) {
   Shape s{};
   sd_status st = check_problem(q, K, V, sp, s);
   if (st) return st;
   if (!V) return SD_ERR_INVALID_ARG;
+  if (labels) {
+    st = check_labels(labels, K, s);
+    if (st) return st;
+  }
   int64_t k_max = 0;
   st = check_idx(idx, s, sp, k_max);
   if (st) return st;
@@ -542,7 +575,7 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   if (!seq_lens) return SD_ERR_INVALID_ARG;
   const hipStream_t stream_h = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_mu);
-  const Layout L = layout_for(s, k_max, true, sp);
+  const Layout L = layout_for(s, k_max, true, sp, labels != nullptr);
   // One scoring workgroup per (chunk, sequence, KV head) on a 1-D grid.
   if ((int64_t)L.nchunk * s.B * s.Hkv > INT32_MAX) return SD_ERR_UNSUPPORTED;
   DevState *ds = nullptr;
@@ -552,7 +585,11 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   sd::Work w = carve(base, L, true);
   // float32 caches (small problems) take the full-score path for every row.
   if (!s.bf16) w.force_repair = 1;
-  const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
+  sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
+  if (labels) {
+    p.labels = (const uint16_t *)labels->t.data;
+    p.channels = labels->channels;
+  }
   int32_t *idx_ptr = (int32_t *)idx->data;
 
   const int prof_level = g_profiling.load();
@@ -601,6 +638,44 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
   }
   ds->stats = w.stats;
   return hip_status(e);
+}
+
+}  // namespace
+
+extern "C" {
+
+sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                  const int32_t *seq_lens, const sd_sparsity *sp, sd_tensor *out,
+                                  sd_tensor *idx, void *stream) {
+  return attention_impl(q, K, V, nullptr, seq_lens, sp, out, idx, stream);
+}
+
+sd_status sparse_decode_label_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                        const sd_labels *labels, const int32_t *seq_lens,
+                                        const sd_sparsity *sp, sd_tensor *out, sd_tensor *idx,
+                                        void *stream) {
+  if (!labels) return SD_ERR_INVALID_ARG;
+  return attention_impl(q, K, V, labels, seq_lens, sp, out, idx, stream);
+}
+
+sd_status sparse_decode_label_score(const sd_tensor *q, const sd_kv *K, const sd_labels *labels,
+                                    const int32_t *seq_lens, const sd_sparsity *sp,
+                                    sd_tensor *scores, void *stream) {
+  Shape s{};
+  sd_status st = check_problem(q, K, nullptr, sp, s);
+  if (st) return st;
+  st = check_labels(labels, K, s);
+  if (st) return st;
+  if (!seq_lens && s.B > 0) return SD_ERR_INVALID_ARG;
+  if (!scores || scores->ndim != 3 || scores->dtype != SD_F32) return SD_ERR_INVALID_ARG;
+  if (scores->shape[0] != s.B || scores->shape[1] != s.R || scores->shape[2] != s.ncap)
+    return SD_ERR_INVALID_ARG;
+  if (s.B == 0 || s.ncap == 0) return SD_OK;
+  if (!scores->data) return SD_ERR_INVALID_ARG;
+  sd::Params p = make_params(q, K, nullptr, seq_lens, sp, s, 0);
+  p.labels = (const uint16_t *)labels->t.data;
+  p.channels = labels->channels;
+  return hip_status(sd::launch_score_dense(p, (float *)scores->data, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -16,6 +16,7 @@ constexpr int kBlock = 256;        // threads per workgroup of every kernel
 constexpr int kWaves = kBlock / 64;
 constexpr int kMaxGroup = 16;      // query heads per KV head handled by one MFMA tile
 constexpr int kWaveKeysMax = 2048; // keys one scoring wave streams (at most)
+constexpr int kLabelWaveKeysMax = 8192;  // the same over label rows (16 bytes per key)
 constexpr int kCandBuf = 1024;     // candidates one scoring wave holds, over all its rows
 constexpr int kChunkCap = kWaves * kCandBuf;  // entries of one workgroup's packed block
 constexpr int kDenseChunk = 8192;  // keys per workgroup of the full-score kernels
@@ -25,10 +26,12 @@ constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the 
 constexpr int kSelectWideRows = 256; // fewer rows: 1024-thread selection workgroups
 constexpr int kDenseWaveKeysMax = 8192; // keys per work item of the dense decode kernel
 constexpr int kDenseMaxGroup = 8;     // query heads per KV head of the dense decode kernel
+constexpr int kLabels = 8;            // label channels per key of the low-channel indexer
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // ---------------------------------------------------------------------------
 // Problem description passed by value to every kernel.
@@ -58,6 +61,12 @@ struct Params {
   const float *weights;        // [B, R, k_max] per-entry weights of the index
                                // lists (weighted attention), or null
   int32_t n_sink, n_local;     // forced first / last positions of each sequence
+  // Low-channel indexer: when labels is set, selection scores come from a
+  // label cache of kLabels bf16 channels per key (layout: label_offset),
+  // read through K's block table when paged; column c of KV head g is key
+  // channel channels[g * kLabels + c].
+  const uint16_t *labels;
+  const int32_t *channels;     // [Hkv][kLabels]
 };
 
 // Scratch carved from the library workspace (see the host orchestration).
@@ -159,6 +168,16 @@ __device__ __forceinline__ int64_t kv_offset(const KvView &kv, int b, int g, int
   if (!kv.paged) return (((int64_t)b * kv.hkv + g) * kv.ncap + j) * kHeadDim;
   int64_t page = kv.block_table[(int64_t)b * kv.max_pages + (j >> 4)];
   return ((page * kTile + (j & 15)) * kv.hkv + g) * kHeadDim;
+}
+
+// Element offset of label row (sequence b, KV head g, position j).  Beside
+// a contiguous cache: [B][Hkv][Ncap][kLabels].  Beside a paged cache:
+// [pages][Hkv][16][kLabels] through K's block table -- head-major inside a
+// page, so a KV head's 16 label rows of a page are one 256-byte run.
+__device__ __forceinline__ int64_t label_offset(const KvView &kv, int b, int g, int64_t j) {
+  if (!kv.paged) return (((int64_t)b * kv.hkv + g) * kv.ncap + j) * kLabels;
+  int64_t page = kv.block_table[(int64_t)b * kv.max_pages + (j >> 4)];
+  return ((page * kv.hkv + g) * kTile + (j & 15)) * kLabels;
 }
 
 // Order-preserving 32-bit key of a float: larger float <=> larger key.
@@ -275,6 +294,82 @@ __device__ __forceinline__ f32x4 mfma_scores(const QFrag &qf, const KFrag &kf) {
                                                   0, 0);
   return acc;
 }
+
+// ---------------------------------------------------------------------------
+// Label scores (the low-channel indexer).  A key's label row is kLabels
+// bf16 channels, 16 bytes.  Every path computes a key's approximate score
+// the same way, so the stream, the fallback and the stand-alone scores agree
+// bit for bit: a fused multiply-add chain over the channels in order
+// (products of bf16 values are exact in float32).  In group-shared mode the
+// query side is first summed over the group's heads (in head order).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ u32x4 load_labels(const uint16_t *base, int64_t off) {
+  return __builtin_nontemporal_load((const u32x4 *)(base + off));
+}
+
+__device__ __forceinline__ void unpack_labels(u32x4 raw, float lab[kLabels]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    lab[2 * e] = bf16_to_f32(raw[e] & 0xFFFFu);
+    lab[2 * e + 1] = __uint_as_float(raw[e] & 0xFFFF0000u);
+  }
+}
+
+__device__ __forceinline__ float label_dot(const float *ql, const float lab[kLabels]) {
+  float s = 0.f;
+#pragma unroll
+  for (int c = 0; c < kLabels; ++c) s = fmaf(ql[c], lab[c], s);
+  return s;
+}
+
+// The query side of row (b, KV head g, head index h within the group): q's
+// label channels (channel indices clamped, so bad ones stay memory-safe),
+// or in group-shared mode (h < 0) their sum over the group's heads.
+__device__ __forceinline__ void q_label_row(const Params &p, int b, int g, int h,
+                                            float ql[kLabels]) {
+  const int32_t *ch = p.channels + (int64_t)g * kLabels;
+  const int h0 = h < 0 ? 0 : h, h1 = h < 0 ? p.G : h + 1;
+#pragma unroll
+  for (int c = 0; c < kLabels; ++c) {
+    int cc = ch[c];
+    cc = cc < 0 ? 0 : (cc >= kHeadDim ? kHeadDim - 1 : cc);
+    float v = 0.f;
+    for (int t = h0; t < h1; ++t)
+      v += bf16_to_f32(((const uint16_t *)p.q)[((int64_t)b * p.Hq + (int64_t)g * p.G + t) *
+                                                  kHeadDim + cc]);
+    ql[c] = v;
+  }
+}
+
+// Label scores in the MFMA result layout (for the pilot and the full-score
+// paths): lane (s, col) holds rows 4s+r of its key col.  Rows beyond G are
+// zero; in group-shared mode row 0 of lane group 0 holds the group's score
+// and every other row is zero, so group_sum returns it unchanged.
+struct LabelRows {
+  float ql[4][kLabels];
+  __device__ __forceinline__ void init(const Params &p, int b, int g) {
+    const int s = lane_id() >> 4;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int h = 4 * s + r;
+      const bool use = p.group_shared ? (s == 0 && r == 0) : h < p.G;
+      if (use) {
+        q_label_row(p, b, g, p.group_shared ? -1 : h, ql[r]);
+      } else {
+#pragma unroll
+        for (int c = 0; c < kLabels; ++c) ql[r][c] = 0.f;
+      }
+    }
+  }
+  __device__ __forceinline__ f32x4 score(u32x4 raw) const {
+    float lab[kLabels];
+    unpack_labels(raw, lab);
+    f32x4 acc;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] = label_dot(ql[r], lab);
+    return acc;
+  }
+};
 
 // float32 caches: the same result layout computed on the vector ALUs.
 // q_lds holds the group's queries [16][128] (rows >= G are zero).  Each dot

@@ -33,12 +33,15 @@ namespace sd {
 // ---------------------------------------------------------------------------
 // Scoring of one key per lane, in the MFMA result layout.
 // ---------------------------------------------------------------------------
-template <bool BF16>
+template <bool BF16, bool LABEL = false>
 struct Scorer {
   QFrag qf;
+  LabelRows lr;
   float *q_lds;
   __device__ __forceinline__ f32x4 score(const Params &p, int b, int g, int64_t j) const {
-    if constexpr (BF16) {
+    if constexpr (LABEL) {
+      return lr.score(load_labels(p.labels, label_offset(p.K, b, g, j)));
+    } else if constexpr (BF16) {
       KFrag kf;
       load_k_bf16(p.K, kv_offset(p.K, b, g, j), kf);
       return mfma_scores(qf, kf);
@@ -50,11 +53,13 @@ struct Scorer {
 
 // Shared prologue: query fragments (bf16) or the group's queries in LDS (f32).
 // Every thread of the block must call it.
-template <bool BF16>
-__device__ __forceinline__ void scorer_init(const Params &p, int b, int g, Scorer<BF16> &sc,
-                                            float *q_lds) {
+template <bool BF16, bool LABEL>
+__device__ __forceinline__ void scorer_init(const Params &p, int b, int g,
+                                            Scorer<BF16, LABEL> &sc, float *q_lds) {
   sc.q_lds = q_lds;
-  if constexpr (BF16) {
+  if constexpr (LABEL) {
+    sc.lr.init(p, b, g);
+  } else if constexpr (BF16) {
     load_q_bf16(p, b, g, sc.qf);
   } else {
     load_q_f32_lds(p, b, g, q_lds);
@@ -71,6 +76,8 @@ __device__ __forceinline__ void scorer_init(const Params &p, int b, int g, Score
 // ---------------------------------------------------------------------------
 constexpr int kPilotTiles = 4;
 
+// LABEL: the samples are scored by the low-channel indexer (label tiles).
+template <bool LABEL>
 __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
   const int bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
   const int L = seq_len(p, b);
@@ -83,14 +90,18 @@ __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
   const int stride = gridDim.x * kWaves;
   if (t0 >= ntiles) return;  // wave-uniform; no barriers in this kernel
   QFrag qf;
-  load_q_bf16(p, b, g, qf);
+  LabelRows lr;
+  if constexpr (LABEL) lr.init(p, b, g);
+  else load_q_bf16(p, b, g, qf);
   KFrag kf[kPilotTiles];
+  u32x4 lf[kPilotTiles];
 #pragma unroll
   for (int u = 0; u < kPilotTiles; ++u) {
     const int t = t0 + u * stride;
     const int si = t * kTile + col;
     const int64_t pos = rp.lo + ((t < ntiles && si < m) ? ((int64_t)si * mid) / m : 0);
-    load_k_bf16(p.K, kv_offset(p.K, b, g, pos), kf[u]);
+    if constexpr (LABEL) lf[u] = load_labels(p.labels, label_offset(p.K, b, g, pos));
+    else load_k_bf16(p.K, kv_offset(p.K, b, g, pos), kf[u]);
   }
 #pragma unroll
   for (int u = 0; u < kPilotTiles; ++u) {
@@ -98,7 +109,9 @@ __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
     if (t >= ntiles) break;  // wave-uniform
     const int si = t * kTile + col;
     const bool valid = si < m;
-    const f32x4 acc = mfma_scores(qf, kf[u]);
+    f32x4 acc;
+    if constexpr (LABEL) acc = lr.score(lf[u]);
+    else acc = mfma_scores(qf, kf[u]);
     if (!p.group_shared) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -279,7 +292,10 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
     if (r < rmin) r = rmin < m ? rmin : m;
     if (r < 1) r = 1;
   }
-  const bool dense = w.force_repair || 2LL * r * span > (int64_t)cap * m;
+  // Rows whose expected candidates per wave would fill more than half of a
+  // staging area take the exact fallback.  (r - 1): r is rounded up, and the
+  // wave size was chosen on the unrounded expectation.
+  const bool dense = w.force_repair || 2LL * (r - 1) * span > (int64_t)cap * m;
   if (k == 0 || dense) {
     if (threadIdx.x == 0) {
       w.flags[row] = k > 0 ? 1 : 0;
@@ -337,7 +353,16 @@ struct WaveLds {
 // of the workgroup of (quad q, chunk) scores KV head 4q + v over the whole
 // chunk, so the workgroup reads four of the heads of every page block
 // together; each wave then packs its own head's block.
-template <bool PAGED, bool GRP, bool QUAD>
+// LABEL: the low-channel indexer scores label rows (16 bytes per key) on
+// the vector ALUs instead of key rows; candidates, blocks and directory are
+// the same.
+constexpr int kLabelDepth = 8;  // 64-key label tiles in flight per wave (8 KB)
+// In label waves the key-tile LDS area holds the rows' query sides (at most
+// kMaxGroup * kLabels floats) and, after them, the wave's page ids.
+constexpr int kLabelPageBase = kMaxGroup * kLabels;
+static_assert(kLabelPageBase + kLabelWaveKeysMax / kTile <= 1024, "label page ids fit the tile area");
+
+template <bool PAGED, bool GRP, bool QUAD, bool LABEL>
 __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   static_assert(PAGED || !QUAD, "head quads are for the paged layout");
   __shared__ WaveLds wlds[kWaves];
@@ -386,7 +411,7 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
 
   if (nvalid > 0) {  // wave-uniform
     QFrag qf;
-    load_q_bf16(p, b, g, qf);
+    if constexpr (!LABEL) load_q_bf16(p, b, g, qf);
     // This lane filters rows 4s..4s+3 (heads of the group; heads beyond G
     // never pass) or, in group-shared mode, lanes 0..15 the group's one row.
     float th[4];
@@ -397,9 +422,12 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
       else th[r] = h < p.G ? w.theta[row0 + h] : __builtin_inff();
     }
     const int ntiles = (nvalid + kTile - 1) / kTile;
+    // Page ids of the wave's keys (label waves take longer ranges and keep
+    // them in the unused key-tile area).
+    int32_t *pg = LABEL ? (int32_t *)wl.tile + kLabelPageBase : wl.page;
     if (PAGED) {
       const int32_t *bt = p.K.block_table + (int64_t)b * p.K.max_pages + (w0 >> 4);
-      for (int i = l; i < ntiles; i += 64) wl.page[i] = bt[i];
+      for (int i = l; i < ntiles; i += 64) pg[i] = bt[i];
       __builtin_amdgcn_wave_barrier();  // every lane reads every page id
     }
     const char *kbase = (const char *)p.K.base;
@@ -443,35 +471,104 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
       }
     };
 
-    const int nsteps = (ntiles + kDepth - 1) / kDepth * kDepth;
-    u32x4 buf[kDepth][4];
-#pragma unroll
-    for (int d = 0; d < kDepth; ++d) {
-      load(d, buf[d]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // The scores of a tile are filtered one step later, after the next
-    // tile's loads and matrix ops are issued, so the appends (which wait on
-    // the matrix results) never hold up the stream.
-    f32x4 prev = {0.f, 0.f, 0.f, 0.f};
-    int prev_jl = nvalid;  // nothing to filter before the first tile
-    for (int tb = 0; tb < nsteps; tb += kDepth) {
-#pragma unroll
-      for (int u = 0; u < kDepth; ++u) {
-        const int ti = tb + u;
-        stage_tile(wl.tile, buf[u]);
-        load(ti + kDepth, buf[u]);
-        __builtin_amdgcn_wave_barrier();  // the tile is read back by other lanes
-        KFrag kf;
-        read_kfrag(wl.tile, kf);
-        __builtin_amdgcn_wave_barrier();  // and overwritten by the next step
-        const f32x4 acc = mfma_scores(qf, kf);
-        filter(prev, prev_jl);
-        prev = acc;
-        prev_jl = ti * kTile + col;
+    if constexpr (LABEL) {
+      // One key per lane: tiles of 64 keys, one 16-byte label row each
+      // (a fully coalesced 1 KB load), scored on the vector ALUs for every
+      // row of the group, kLabelDepth tiles in flight.  A row's keys that
+      // pass are appended to its area in position order (ballot + prefix
+      // count); a row that no key of the tile passes costs one compare.
+      float *qlw = (float *)wl.tile;  // the rows' query sides [nrows][kLabels]
+      if (l < nrows * kLabels) {
+        float ql[kLabels];
+        q_label_row(p, b, g, GRP ? -1 : l / kLabels, ql);
+        qlw[l] = ql[l % kLabels];
       }
+      float thr[kMaxGroup];
+      int cnt16[kMaxGroup];
+#pragma unroll
+      for (int h = 0; h < kMaxGroup; ++h) {
+        thr[h] = h < nrows ? w.theta[row0 + h] : __builtin_inff();
+        cnt16[h] = 0;
+      }
+      __builtin_amdgcn_wave_barrier();  // qlw is read by every lane
+      const int nt64 = (nvalid + 63) / 64;
+      const int64_t lslab = (((int64_t)b * p.K.hkv + g) * p.K.ncap + w0) * kLabels;
+      const int64_t page_el = (int64_t)kTile * p.K.hkv * kLabels;
+      auto lload = [&](int ti) -> u32x4 {
+        ti = ti < nt64 ? ti : nt64 - 1;
+        int j = ti * 64 + l;
+        j = j < last ? j : last;
+        const int64_t off = PAGED ? pg[j >> 4] * page_el + ((int64_t)g * kTile + (j & 15)) * kLabels
+                                  : lslab + (int64_t)j * kLabels;
+        return load_labels(p.labels, off);
+      };
+      const int nlsteps = (nt64 + kLabelDepth - 1) / kLabelDepth * kLabelDepth;
+      u32x4 lb[kLabelDepth];
+#pragma unroll
+      for (int d = 0; d < kLabelDepth; ++d) lb[d] = lload(d);
+      const uint64_t below = (1ull << l) - 1ull;
+      for (int tb = 0; tb < nlsteps; tb += kLabelDepth) {
+#pragma unroll
+        for (int u = 0; u < kLabelDepth; ++u) {
+          const int ti = tb + u;
+          float lab[kLabels];
+          unpack_labels(lb[u], lab);
+          lb[u] = lload(ti + kLabelDepth);
+          const int jl = ti * 64 + l;
+          const bool live = jl >= jlo && jl < jhi;
+#pragma unroll
+          for (int h = 0; h < kMaxGroup; ++h) {
+            if (h >= nrows) break;  // wave-uniform
+            const float sc = label_dot(qlw + h * kLabels, lab);
+            const bool pass = live && sc >= thr[h];
+            const uint64_t m = __ballot(pass);
+            if (m) {  // wave-uniform
+              const int slot = cnt16[h] + __popcll(m & below);
+              if (pass && slot < cap) wl.cand[h * cap + slot] = make_uint2(__float_as_uint(sc), (uint32_t)jl);
+              cnt16[h] += __popcll(m);
+            }
+          }
+        }
+      }
+      // Counts in the layout the packing below reads: lane group s holds
+      // rows 4s..4s+3.
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+#pragma unroll
+        for (int sg = 0; sg < 4; ++sg)
+          if (s == sg) cnt[r] = cnt16[4 * sg + r];
+      }
+    } else {
+      const int nsteps = (ntiles + kDepth - 1) / kDepth * kDepth;
+      u32x4 buf[kDepth][4];
+#pragma unroll
+      for (int d = 0; d < kDepth; ++d) {
+        load(d, buf[d]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // The scores of a tile are filtered one step later, after the next
+      // tile's loads and matrix ops are issued, so the appends (which wait on
+      // the matrix results) never hold up the stream.
+      f32x4 prev = {0.f, 0.f, 0.f, 0.f};
+      int prev_jl = nvalid;  // nothing to filter before the first tile
+      for (int tb = 0; tb < nsteps; tb += kDepth) {
+#pragma unroll
+        for (int u = 0; u < kDepth; ++u) {
+          const int ti = tb + u;
+          stage_tile(wl.tile, buf[u]);
+          load(ti + kDepth, buf[u]);
+          __builtin_amdgcn_wave_barrier();  // the tile is read back by other lanes
+          KFrag kf;
+          read_kfrag(wl.tile, kf);
+          __builtin_amdgcn_wave_barrier();  // and overwritten by the next step
+          const f32x4 acc = mfma_scores(qf, kf);
+          filter(prev, prev_jl);
+          prev = acc;
+          prev_jl = ti * kTile + col;
+        }
+      }
+      filter(prev, prev_jl);
     }
-    filter(prev, prev_jl);
   }
   if constexpr (QUAD) {
     // This wave's block: its rows one after another, each in position order.
@@ -587,13 +684,13 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
 // fill_tail, -inf for L_b <= j < ncap.  Every thread of the block must call
 // it (the f32 scorer stages the queries in LDS behind a barrier).
 // ---------------------------------------------------------------------------
-template <bool BF16>
+template <bool BF16, bool LABEL>
 __device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_t ld, int b, int g,
                                              int part, int parts, bool fill_tail, float *q_lds) {
   const int L = seq_len(p, b);
   const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
-  Scorer<BF16> sc;
-  scorer_init<BF16>(p, b, g, sc, q_lds);
+  Scorer<BF16, LABEL> sc;
+  scorer_init<BF16, LABEL>(p, b, g, sc, q_lds);
   const int64_t end = fill_tail ? p.ncap : (int64_t)L;
   const int64_t ntiles = (end + kTile - 1) / kTile;
   const int l = lane_id(), col = l & 15, s = l >> 4;
@@ -617,11 +714,12 @@ __device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_
 }
 
 // sparse_decode_score: grid = (parts, B*Hkv).
-template <bool BF16>
+template <bool BF16, bool LABEL>
 __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, int64_t ld) {
   __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
   const int bg = blockIdx.y;
-  dense_scores<BF16>(p, dst, ld, bg / p.Hkv, bg % p.Hkv, blockIdx.x, gridDim.x, true, q_lds);
+  dense_scores<BF16, LABEL>(p, dst, ld, bg / p.Hkv, bg % p.Hkv, blockIdx.x, gridDim.x, true,
+                            q_lds);
 }
 
 // Exact fallback, scoring.  grid = (kRepairParts, B*Hkv).  A row takes the
@@ -631,7 +729,7 @@ __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, in
 // per-chunk counts (part 0 records them in w.flags for the selection) and,
 // when a row of the group is flagged, scores its part of the group into
 // w.dense.
-template <bool BF16>
+template <bool BF16, bool LABEL>
 __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
   __shared__ int cnt[kMaxGroup], bad[kMaxGroup];
@@ -665,7 +763,7 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
     if (part == 0) w.flags[row0 + tid] = flag ? 1 : 0;
   }
   __syncthreads();
-  if (any) dense_scores<BF16>(p, w.dense, p.ncap, b, g, part, kRepairParts, false, q_lds);
+  if (any) dense_scores<BF16, LABEL>(p, w.dense, p.ncap, b, g, part, kRepairParts, false, q_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -961,9 +1059,10 @@ __device__ __forceinline__ int attend_list_len(const Params &p, int b, int L, bo
 }
 
 // Logits are recomputed from the key rows unless the selection formed the
-// softmax weights already (fused per-head rows without forced positions).
+// softmax weights already (fused per-head rows on exact scores without
+// forced positions).
 __host__ __device__ inline bool attend_recompute(bool fused, const Params &p) {
-  return !fused || p.group_shared || p.n_sink + p.n_local > 0;
+  return !fused || p.group_shared || p.n_sink + p.n_local > 0 || p.labels != nullptr;
 }
 
 // Byte offsets of the dynamic LDS areas of k_attend (host and device agree).
@@ -1264,7 +1363,8 @@ static inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1
 hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
   if (!w.force_repair) {
     const dim3 g1(kSampleMax / (kPilotTiles * kTile * kWaves), p.B * p.Hkv);
-    k_pilot_score<<<g1, kBlock, 0, st>>>(p, w);
+    if (p.labels) k_pilot_score<true><<<g1, kBlock, 0, st>>>(p, w);
+    else k_pilot_score<false><<<g1, kBlock, 0, st>>>(p, w);
   }
   k_pilot_select<<<p.B * p.R, kBlock, 0, st>>>(p, w);
   return hipGetLastError();
@@ -1292,14 +1392,18 @@ hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st, h
   if (w.force_repair) return hipSuccess;  // every row takes the fallback
   void (*kern)(Params, Work);
   int64_t wgs;
+  const bool gs = p.group_shared != 0, lab = p.labels != nullptr;
   if (stream_by_head_quads(w)) {
-    kern = p.group_shared ? k_score_stream<true, true, true> : k_score_stream<true, false, true>;
+    if (lab) kern = gs ? k_score_stream<true, true, true, true> : k_score_stream<true, false, true, true>;
+    else kern = gs ? k_score_stream<true, true, true, false> : k_score_stream<true, false, true, false>;
     wgs = (int64_t)w.nchunk * p.B * (p.Hkv / kWaves);
   } else if (p.K.paged) {
-    kern = p.group_shared ? k_score_stream<true, true, false> : k_score_stream<true, false, false>;
+    if (lab) kern = gs ? k_score_stream<true, true, false, true> : k_score_stream<true, false, false, true>;
+    else kern = gs ? k_score_stream<true, true, false, false> : k_score_stream<true, false, false, false>;
     wgs = (int64_t)w.nchunk * p.B * p.Hkv;
   } else {
-    kern = p.group_shared ? k_score_stream<false, true, false> : k_score_stream<false, false, false>;
+    if (lab) kern = gs ? k_score_stream<false, true, false, true> : k_score_stream<false, false, false, true>;
+    else kern = gs ? k_score_stream<false, true, false, false> : k_score_stream<false, false, false, false>;
     wgs = (int64_t)w.nchunk * p.B * p.Hkv;
   }
   return launch_with_events(kern, dim3((unsigned)wgs), p, w, st, t0, t1);
@@ -1329,8 +1433,9 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
 
 hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st) {
   const dim3 grid(kRepairParts, p.B * p.Hkv);
-  if (p.bf16) k_repair_score<true><<<grid, kBlock, 0, st>>>(p, w);
-  else k_repair_score<false><<<grid, kBlock, 0, st>>>(p, w);
+  if (p.labels) k_repair_score<true, true><<<grid, kBlock, 0, st>>>(p, w);
+  else if (p.bf16) k_repair_score<true, false><<<grid, kBlock, 0, st>>>(p, w);
+  else k_repair_score<false, false><<<grid, kBlock, 0, st>>>(p, w);
   return hipGetLastError();
 }
 
@@ -1409,8 +1514,9 @@ hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, voi
 
 hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st) {
   const dim3 grid(cdiv(p.ncap, kDenseChunk), p.B * p.Hkv);
-  if (p.bf16) k_score_dense<true><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
-  else k_score_dense<false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  if (p.labels) k_score_dense<true, true><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  else if (p.bf16) k_score_dense<true, false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  else k_score_dense<false, false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
   return hipGetLastError();
 }
 

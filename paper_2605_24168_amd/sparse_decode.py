@@ -11,6 +11,8 @@ names follow the C ABI in include/sparse_decode.h:
     sparse_decode_attention(q, cache, seq_lens, sparsity)    -> (out, idx)
     sparse_decode_attend_weighted(q, cache, seq_lens, idx, weights, sparsity) -> out
     sparse_decode_dense_attention(q, cache, seq_lens)        -> out
+    sparse_decode_label_attention(q, cache, labels, seq_lens, sparsity) -> (out, idx)
+    sparse_decode_label_score(q, cache, labels, seq_lens, sparsity)     -> scores
 
 Importing this module raises if the library has not been built; nothing here
 falls back to another implementation.
@@ -54,6 +56,10 @@ class SdSparsity(C.Structure):
                 ("n_sink", C.c_int32), ("n_local", C.c_int32)]
 
 
+class SdLabels(C.Structure):
+    _fields_ = [("t", SdTensor), ("channels", C.c_void_p)]
+
+
 class SdProfile(C.Structure):
     _fields_ = [("pilot_ms", C.c_float), ("score_ms", C.c_float), ("select_ms", C.c_float),
                 ("repair_ms", C.c_float), ("attend_ms", C.c_float), ("total_ms", C.c_float),
@@ -80,6 +86,13 @@ lib.sparse_decode_dense_attention.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), 
                                               C.c_float, _P(SdTensor), C.c_void_p]
 lib.sparse_decode_dense_workspace_size.restype = C.c_int
 lib.sparse_decode_dense_workspace_size.argtypes = [_P(SdTensor), _P(SdKv), _P(C.c_size_t)]
+lib.sparse_decode_label_attention.restype = C.c_int
+lib.sparse_decode_label_attention.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), _P(SdLabels),
+                                              C.c_void_p, _P(SdSparsity), _P(SdTensor),
+                                              _P(SdTensor), C.c_void_p]
+lib.sparse_decode_label_score.restype = C.c_int
+lib.sparse_decode_label_score.argtypes = [_P(SdTensor), _P(SdKv), _P(SdLabels), C.c_void_p,
+                                          _P(SdSparsity), _P(SdTensor), C.c_void_p]
 lib.sparse_decode_attention.restype = C.c_int
 lib.sparse_decode_attention.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p,
                                         _P(SdSparsity), _P(SdTensor), _P(SdTensor), C.c_void_p]
@@ -175,6 +188,23 @@ class KVCache:
 
 
 _DTYPES = {torch.float32: SD_F32, torch.bfloat16: SD_BF16, torch.int32: SD_I32}
+
+
+@dataclasses.dataclass
+class Labels:
+    """Label cache of the low-channel indexer: `t` holds 8 bf16 channels per
+    key, [B, Hkv, Ncap, 8] beside a contiguous cache or [pages, Hkv, 16, 8]
+    beside a paged one; `channels` (int32 [Hkv, 8], device) names the key
+    channel of each column."""
+    t: torch.Tensor
+    channels: torch.Tensor
+
+    def c(self) -> SdLabels:
+        _need_device(self.channels, "channels", torch.int32)
+        lab = SdLabels()
+        lab.t = _tensor(self.t, "labels")
+        lab.channels = self.channels.data_ptr()
+        return lab
 
 
 def _need_device(t: torch.Tensor, name: str, dtype=None) -> None:
@@ -324,6 +354,43 @@ def sparse_decode_attention(q, cache: KVCache, seq_lens, sparsity: Sparsity, out
                                        C.byref(sp), C.byref(co), C.byref(ci), _stream(stream)),
            "sparse_decode_attention")
     return out, idx
+
+
+def sparse_decode_label_attention(q, cache: KVCache, labels: Labels, seq_lens, sparsity: Sparsity,
+                                  out=None, idx=None, k_max: Optional[int] = None, stream=None):
+    """The method with the low-channel indexer choosing the positions:
+    returns (out [B, Hq, 128], idx [B, R, k_max])."""
+    _need_device(seq_lens, "seq_lens", torch.int32)
+    if out is None:
+        out = torch.empty_like(q)
+    if idx is None:
+        if k_max is None:
+            k_max = k_max_of(cache, sparsity)
+        idx = torch.empty((q.shape[0], rows_of(q, cache, sparsity), k_max), dtype=torch.int32,
+                          device=q.device)
+    sp, lab = sparsity.c(), labels.c()
+    cq, kk, kv = _tensor(q, "q"), cache.c("k"), cache.c("v")
+    co, ci = _tensor(out, "out"), _tensor(idx, "idx")
+    _check(lib.sparse_decode_label_attention(C.byref(cq), C.byref(kk), C.byref(kv), C.byref(lab),
+                                             seq_lens.data_ptr(), C.byref(sp), C.byref(co),
+                                             C.byref(ci), _stream(stream)),
+           "sparse_decode_label_attention")
+    return out, idx
+
+
+def sparse_decode_label_score(q, cache: KVCache, labels: Labels, seq_lens, sparsity: Sparsity,
+                              scores=None, stream=None):
+    """float32 approximate label scores [B, R, capacity] (-inf beyond each sequence)."""
+    _need_device(seq_lens, "seq_lens", torch.int32)
+    if scores is None:
+        scores = torch.empty((q.shape[0], rows_of(q, cache, sparsity), cache.capacity),
+                             dtype=torch.float32, device=q.device)
+    sp, lab = sparsity.c(), labels.c()
+    cq, kk, ks = _tensor(q, "q"), cache.c("k"), _tensor(scores, "scores")
+    _check(lib.sparse_decode_label_score(C.byref(cq), C.byref(kk), C.byref(lab),
+                                         seq_lens.data_ptr(), C.byref(sp), C.byref(ks),
+                                         _stream(stream)), "sparse_decode_label_score")
+    return scores
 
 
 def workspace_size(q, cache: KVCache, sparsity: Sparsity, idx) -> int:

@@ -42,7 +42,7 @@ ROOT_SEED = 260524168
 POISON = 64.0  # written to allocated-but-unused positions (never a valid key)
 
 (TAG_Q, TAG_K, TAG_V, TAG_PLANT, TAG_SCALE, TAG_LENS, TAG_PAGES, TAG_CENTROID, TAG_SETS,
- TAG_WEIGHTS) = range(10)
+ TAG_WEIGHTS, TAG_CHANNELS) = range(11)
 
 
 @dataclasses.dataclass
@@ -378,3 +378,40 @@ def backend_sweep_sets(rows: int, N: int, k: int, seed: int = 0, device="cuda"):
         idx[r0:r1] = torch.sort(torch.topk(keys, k, dim=1, sorted=False).indices, dim=1).values
     w = torch.rand((rows, k), generator=gen, device=device) * 2.95 + 0.05
     return idx, w
+
+
+N_LABELS = 8
+
+
+def label_channels(Hkv: int, seed: int = 0, n: int = N_LABELS) -> np.ndarray:
+    """Label channels of the low-channel indexer, uncalibrated (Table 2's
+    indexer is untuned): n distinct channels per KV head drawn uniformly,
+    ascending.  int32 [Hkv, n]."""
+    rng = _rng(0, seed, 0, 0, TAG_CHANNELS)
+    return np.stack([np.sort(rng.choice(HEAD_DIM, size=n, replace=False))
+                     for _ in range(Hkv)]).astype(np.int32)
+
+
+def label_cache(inp: DecodeInputs, channels: np.ndarray) -> np.ndarray:
+    """The label cache of a decode step: each key's label channels (copied
+    bits, so 16-bit for bfloat16 caches), in the key cache's layout with
+    rows of len(channels[g]) elements."""
+    n = channels.shape[1]
+    if inp.layout == "paged":
+        out = np.empty(inp.k.shape[:3] + (n,), dtype=inp.k.dtype)
+        for g in range(inp.Hkv):
+            out[:, :, g, :] = inp.k[:, :, g, :][:, :, channels[g]]
+    else:
+        out = np.empty(inp.k.shape[:3] + (n,), dtype=inp.k.dtype)
+        for g in range(inp.Hkv):
+            out[:, g] = inp.k[:, g][:, :, channels[g]]
+    return out
+
+
+def label_cache_device_layout(inp: DecodeInputs, labels: np.ndarray) -> np.ndarray:
+    """The label cache in the library's layout: unchanged beside a
+    contiguous cache; [pages, Hkv, 16, n] (head-major inside a page) beside a
+    paged one, where label_cache gives the key cache's [pages, 16, Hkv, n]."""
+    if inp.layout == "paged":
+        return np.ascontiguousarray(labels.transpose(0, 2, 1, 3))
+    return labels

@@ -212,6 +212,32 @@ def test_dense_workspace_grows_with_the_cache(sd):
     assert sd.lib.sparse_decode_dense_workspace_size(C.byref(q), C.byref(K), C.byref(n)) == -2
 
 
+def test_label_arguments_are_checked_on_the_host(sd):
+    q, K, V, lens, sp, out, idx = valid_parts(sd)
+
+    def labels(shape, dtype=None, channels=FAKE):
+        lab = sd.SdLabels()
+        lab.t = tensor(sd, shape, dtype)
+        lab.channels = channels
+        return lab
+
+    def call(lab):
+        return sd.lib.sparse_decode_label_attention(C.byref(q), C.byref(K), C.byref(V),
+                                                    C.byref(lab) if lab is not None else None,
+                                                    lens, C.byref(sp), C.byref(out),
+                                                    C.byref(idx), None)
+    assert call(None) == -1
+    assert call(labels((2, 8, 4096, 8), channels=None)) == -1
+    assert call(labels((2, 8, 4095, 8))) == -1                 # capacity differs from K
+    assert call(labels((2, 4, 4096, 8))) == -1                 # KV heads differ
+    assert call(labels((2, 8, 4096, 4))) == -2                 # only 8 label channels
+    assert call(labels((2, 8, 4096, 8), sd.SD_F32)) == -2      # 16-bit labels only
+    scores = tensor(sd, (2, 32, 4096), sd.SD_F32)
+    assert sd.lib.sparse_decode_label_score(C.byref(q), C.byref(K),
+                                            C.byref(labels((2, 8, 4096, 8))), None,
+                                            C.byref(sp), C.byref(scores), None) == -1  # seq_lens
+
+
 def test_empty_batch_is_a_no_op(sd):
     q = tensor(sd, (0, 32, 128))
     K, V = bhnd(sd, 0, 8, 4096), bhnd(sd, 0, 8, 4096)

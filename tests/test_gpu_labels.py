@@ -1,0 +1,171 @@
+"""Parity of the low-channel approximate indexer (a Double Sparsity label
+cache of 8 bf16 channels per key choosing the positions, Table 2) with the
+CPU oracle, through the C ABI."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2605_24168_amd import synth
+from tests import parity as P
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def sd():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2605_24168_amd import sparse_decode
+    sparse_decode.set_debug(0)
+    return sparse_decode
+
+
+SMALL = {
+    "w2": dict(cfg=2, B=2, N=20007),
+    "w3": dict(cfg=3, B=2, N=24003),
+    "w4": dict(cfg=4, B=5, lmin=1000, lmax=30000, N=30000),
+    "w5": dict(cfg=5, N=65536 + 77),
+}
+
+
+def make(name, seed=0, **over):
+    kw = dict(SMALL[name])
+    cfg = kw.pop("cfg")
+    kw.update(over)
+    inp = synth.make_inputs(cfg, seed=seed, **kw)
+    ch = synth.label_channels(inp.Hkv, seed=seed)
+    _INP["last"] = inp
+    return inp, ch, synth.label_cache(inp, ch)
+
+
+# The oracle reads label caches in the key cache's layout; the library's
+# paged label layout is head-major inside a page (a transpose, done here).
+_INP = {}
+
+
+def dev_labels(sd, lab, ch, inp=None):
+    inp = inp if inp is not None else _INP["last"]
+    t = torch.from_numpy(synth.label_cache_device_layout(inp, lab)).view(torch.bfloat16).cuda()
+    return sd.Labels(t=t, channels=torch.from_numpy(ch).cuda())
+
+
+def label_allowance(inp, ch, lab, b, r):
+    """Bound on |float32 label score - exact| for row (b, r): float32 sums of
+    8 exact bf16 products per head (group rows: G heads), doubled."""
+    u = 2.0 ** -24
+    n = 8 * (inp.G if inp.group_shared else 1)
+    gamma = n * u / (1 - n * u)
+    g = r if inp.group_shared else r // inp.G
+    heads = range(g * inp.G, (g + 1) * inp.G) if inp.group_shared else [r]
+    L = int(inp.seq_lens[b])
+    if inp.layout == "paged":
+        pages = inp.block_table[b, :(L + 15) // 16]
+        rows = lab[pages][:, :, g, :].reshape(-1, 8)[:L]
+    else:
+        rows = lab[b, g, :L]
+    lf = np.abs(synth.bf16_to_f32(rows).astype(np.float64))
+    tot = np.zeros(L)
+    for h in heads:
+        qc = np.abs(synth.bf16_to_f32(inp.q[b, h, ch[g]]).astype(np.float64))
+        tot += lf @ qc
+    return 2.0 * gamma * tot + 1e-30
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_label_scores_within_float32_bound(sd, name):
+    inp, ch, lab = make(name)
+    q, cache, lens = sd.cache_from_inputs(inp)
+    sp = sd.sparsity_from_inputs(inp)
+    got = sd.sparse_decode_label_score(q, cache, dev_labels(sd, lab, ch), lens, sp).cpu().numpy()
+    ref = O.label_scores(inp, lab, ch)
+    worst = 0.0
+    for b in range(inp.B):
+        L = int(inp.seq_lens[b])
+        assert np.isneginf(got[b, :, L:]).all()
+        for r in range(0, inp.rows, 3):
+            err = np.abs(got[b, r, :L].astype(np.float64) - ref[b, r, :L])
+            ratio = (err / label_allowance(inp, ch, lab, b, r)).max() if L else 0.0
+            worst = max(worst, ratio)
+    P.log(f"  {name}: label score worst/allow={worst:.3g}")
+    assert worst <= 1.0
+
+
+def run(sd, inp, ch, lab, k_override=None):
+    q, cache, lens = sd.cache_from_inputs(inp)
+    ko = None if k_override is None else torch.tensor(k_override, dtype=torch.int32).cuda()
+    sp = sd.sparsity_from_inputs(inp, k_override=ko)
+    out, idx = sd.sparse_decode_label_attention(q, cache, dev_labels(sd, lab, ch), lens, sp,
+                                                k_max=O.k_max_for(inp))
+    torch.cuda.synchronize()
+    return P.to_host(out), idx.cpu().numpy(), (q, cache, lens, sp)
+
+
+def check(inp, ch, lab, out, idx, label):
+    ora = O.label_attention(inp, lab, ch, k_max=idx.shape[2])
+    ks = []
+    for L in inp.seq_lens:
+        L = int(L)
+        ns = min(inp.n_sink, L)
+        nl = min(inp.n_local, L - ns)
+        ks.append(ns + nl + min(O.budget(L, inp.ratio, inp.rounding), L - ns - nl))
+    rep = P.check_idx_rows(idx, ora["idx"], O.label_scores(inp, lab, ch), ora["tau"],
+                           inp.seq_lens, np.array(ks))
+    assert rep.strict_mismatch_rows == 0, f"{label}: {rep.first_failure}"
+    ref = ora["out"] if rep.band_swaps == 0 else O.attend(inp, idx)[0]
+    ok, ratio, rel = P.out_errors(out, ref, inp.dtype)
+    P.log(f"  {label}: rows={rep.rows} band_swaps={rep.band_swaps} worst/allow={ratio:.3g} "
+          f"relL2={rel:.2e}")
+    assert ok, f"{label}: output error {ratio:.3g} x allowance"
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_label_indexer_matches_oracle(sd, name):
+    inp, ch, lab = make(name)
+    out, idx, _ = run(sd, inp, ch, lab)
+    check(inp, ch, lab, out, idx, f"{name} labels")
+
+
+def test_label_selection_equals_topk_over_label_scores(sd):
+    inp, ch, lab = make("w4", seed=1)
+    out, idx, (q, cache, lens, sp) = run(sd, inp, ch, lab)
+    scores = sd.sparse_decode_label_score(q, cache, dev_labels(sd, lab, ch), lens, sp)
+    idx2 = sd.sparse_decode_topk(scores, lens, sp, k_max=idx.shape[2]).cpu().numpy()
+    np.testing.assert_array_equal(idx, idx2)
+
+
+def test_label_indexer_with_forced_positions_and_fallback(sd):
+    inp, ch, lab = make("w3", seed=2, n_sink=64, n_local=64)
+    out, idx, _ = run(sd, inp, ch, lab)
+    check(inp, ch, lab, out, idx, "labels + sink 64 + local 64")
+    sd.set_debug(1)
+    try:
+        out2, idx2, _ = run(sd, inp, ch, lab)
+    finally:
+        sd.set_debug(0)
+    np.testing.assert_array_equal(idx, idx2)
+    np.testing.assert_array_equal(out, out2)
+
+
+def test_label_indexer_ragged_and_mha(sd):
+    inp, ch, lab = make("w4", seed=3, Hq=16, Hkv=16, seq_lens=[0, 1, 17, 300, 4097, 20000],
+                        N=20000)
+    out, idx, _ = run(sd, inp, ch, lab)
+    assert (idx[0] == -1).all() and (out[0] == 0).all()
+    check(inp, ch, lab, out, idx, "labels MHA ragged")
+
+
+def test_label_arguments_are_checked(sd):
+    inp, ch, lab = make("w2")
+    q, cache, lens = sd.cache_from_inputs(inp)
+    sp = sd.sparsity_from_inputs(inp)
+    bad = sd.Labels(t=torch.from_numpy(lab[..., :4].copy()).view(torch.bfloat16).cuda(),
+                    channels=torch.from_numpy(ch[:, :4].copy()).cuda())   # 4 channels
+    with pytest.raises(sd.SparseDecodeError) as e:
+        sd.sparse_decode_label_attention(q, cache, bad, lens, sp, k_max=O.k_max_for(inp))
+    assert e.value.status == sd.SD_ERR_UNSUPPORTED
+    short = sd.Labels(t=torch.from_numpy(lab[:, :, :100].copy()).view(torch.bfloat16).cuda(),
+                      channels=torch.from_numpy(ch).cuda())
+    with pytest.raises(sd.SparseDecodeError) as e:
+        sd.sparse_decode_label_attention(q, cache, short, lens, sp, k_max=O.k_max_for(inp))
+    assert e.value.status == sd.SD_ERR_INVALID_ARG
