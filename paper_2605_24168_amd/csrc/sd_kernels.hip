@@ -357,12 +357,13 @@ struct WaveLds {
 // the vector ALUs instead of key rows; candidates, blocks and directory are
 // the same.
 constexpr int kLabelDepth = 8;  // 64-key label tiles in flight per wave (8 KB)
-// In label waves the key-tile LDS area holds the rows' query sides (at most
-// kMaxGroup * kLabels floats) and, after them, the wave's page ids.
-constexpr int kLabelPageBase = kMaxGroup * kLabels;
+// In label waves the key-tile LDS area holds the wave's page ids.
+constexpr int kLabelPageBase = 0;
 static_assert(kLabelPageBase + kLabelWaveKeysMax / kTile <= 1024, "label page ids fit the tile area");
 
-template <bool PAGED, bool GRP, bool QUAD, bool LABEL>
+// NR: rows per wave held in registers by the label path (a power of two
+// >= the group's rows; 0 for key rows).
+template <bool PAGED, bool GRP, bool QUAD, bool LABEL, int NR>
 __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   static_assert(PAGED || !QUAD, "head quads are for the paged layout");
   __shared__ WaveLds wlds[kWaves];
@@ -477,20 +478,23 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
       // row of the group, kLabelDepth tiles in flight.  A row's keys that
       // pass are appended to its area in position order (ballot + prefix
       // count); a row that no key of the tile passes costs one compare.
-      float *qlw = (float *)wl.tile;  // the rows' query sides [nrows][kLabels]
-      if (l < nrows * kLabels) {
-        float ql[kLabels];
-        q_label_row(p, b, g, GRP ? -1 : l / kLabels, ql);
-        qlw[l] = ql[l % kLabels];
-      }
-      float thr[kMaxGroup];
-      int cnt16[kMaxGroup];
+      // The rows' query sides and thresholds in registers (rows past the
+      // group's never pass).
+      constexpr int NRr = NR > 0 ? NR : 1;
+      float qlr[NRr][kLabels], thr[NRr];
+      int cntr[NRr];
 #pragma unroll
-      for (int h = 0; h < kMaxGroup; ++h) {
-        thr[h] = h < nrows ? w.theta[row0 + h] : __builtin_inff();
-        cnt16[h] = 0;
+      for (int h = 0; h < NRr; ++h) {
+        cntr[h] = 0;
+        if (h < nrows) {
+          q_label_row(p, b, g, GRP ? -1 : h, qlr[h]);
+          thr[h] = w.theta[row0 + h];
+        } else {
+#pragma unroll
+          for (int c = 0; c < kLabels; ++c) qlr[h][c] = 0.f;
+          thr[h] = __builtin_inff();
+        }
       }
-      __builtin_amdgcn_wave_barrier();  // qlw is read by every lane
       const int nt64 = (nvalid + 63) / 64;
       const int64_t lslab = (((int64_t)b * p.K.hkv + g) * p.K.ncap + w0) * kLabels;
       const int64_t page_el = (int64_t)kTile * p.K.hkv * kLabels;
@@ -517,15 +521,14 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
           const int jl = ti * 64 + l;
           const bool live = jl >= jlo && jl < jhi;
 #pragma unroll
-          for (int h = 0; h < kMaxGroup; ++h) {
-            if (h >= nrows) break;  // wave-uniform
-            const float sc = label_dot(qlw + h * kLabels, lab);
+          for (int h = 0; h < NRr; ++h) {
+            const float sc = label_dot(qlr[h], lab);
             const bool pass = live && sc >= thr[h];
             const uint64_t m = __ballot(pass);
             if (m) {  // wave-uniform
-              const int slot = cnt16[h] + __popcll(m & below);
+              const int slot = cntr[h] + __popcll(m & below);
               if (pass && slot < cap) wl.cand[h * cap + slot] = make_uint2(__float_as_uint(sc), (uint32_t)jl);
-              cnt16[h] += __popcll(m);
+              cntr[h] += __popcll(m);
             }
           }
         }
@@ -536,7 +539,7 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
       for (int r = 0; r < 4; ++r) {
 #pragma unroll
         for (int sg = 0; sg < 4; ++sg)
-          if (s == sg) cnt[r] = cnt16[4 * sg + r];
+          if (4 * sg + r < NRr && s == sg) cnt[r] = cntr[4 * sg + r];
       }
     } else {
       const int nsteps = (ntiles + kDepth - 1) / kDepth * kDepth;
@@ -1387,23 +1390,35 @@ static hipError_t launch_with_events(void (*kern)(Params, Work), dim3 grid, cons
 
 bool stream_by_head_quads(const Work &w) { return w.chunk_keys == w.wave_keys; }
 
+// The label stream instance holding `rows` rows per wave in registers.
+template <bool PAGED, bool QUAD>
+static void (*label_stream_kernel(bool group_shared, int rows))(Params, Work) {
+  if (group_shared) return k_score_stream<PAGED, true, QUAD, true, 1>;
+  if (rows <= 1) return k_score_stream<PAGED, false, QUAD, true, 1>;
+  if (rows <= 2) return k_score_stream<PAGED, false, QUAD, true, 2>;
+  if (rows <= 4) return k_score_stream<PAGED, false, QUAD, true, 4>;
+  if (rows <= 8) return k_score_stream<PAGED, false, QUAD, true, 8>;
+  return k_score_stream<PAGED, false, QUAD, true, 16>;
+}
+
 hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st, hipEvent_t t0,
                                hipEvent_t t1) {
   if (w.force_repair) return hipSuccess;  // every row takes the fallback
   void (*kern)(Params, Work);
   int64_t wgs;
   const bool gs = p.group_shared != 0, lab = p.labels != nullptr;
+  const int rows = gs ? 1 : p.G;
   if (stream_by_head_quads(w)) {
-    if (lab) kern = gs ? k_score_stream<true, true, true, true> : k_score_stream<true, false, true, true>;
-    else kern = gs ? k_score_stream<true, true, true, false> : k_score_stream<true, false, true, false>;
+    if (lab) kern = label_stream_kernel<true, true>(gs, rows);
+    else kern = gs ? k_score_stream<true, true, true, false, 0> : k_score_stream<true, false, true, false, 0>;
     wgs = (int64_t)w.nchunk * p.B * (p.Hkv / kWaves);
   } else if (p.K.paged) {
-    if (lab) kern = gs ? k_score_stream<true, true, false, true> : k_score_stream<true, false, false, true>;
-    else kern = gs ? k_score_stream<true, true, false, false> : k_score_stream<true, false, false, false>;
+    if (lab) kern = label_stream_kernel<true, false>(gs, rows);
+    else kern = gs ? k_score_stream<true, true, false, false, 0> : k_score_stream<true, false, false, false, 0>;
     wgs = (int64_t)w.nchunk * p.B * p.Hkv;
   } else {
-    if (lab) kern = gs ? k_score_stream<false, true, false, true> : k_score_stream<false, false, false, true>;
-    else kern = gs ? k_score_stream<false, true, false, false> : k_score_stream<false, false, false, false>;
+    if (lab) kern = label_stream_kernel<false, false>(gs, rows);
+    else kern = gs ? k_score_stream<false, true, false, false, 0> : k_score_stream<false, false, false, false, 0>;
     wgs = (int64_t)w.nchunk * p.B * p.Hkv;
   }
   return launch_with_events(kern, dim3((unsigned)wgs), p, w, st, t0, t1);

@@ -155,6 +155,14 @@ def test_label_indexer_ragged_and_mha(sd):
     check(inp, ch, lab, out, idx, "labels MHA ragged")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(4, 2), (32, 2), (24, 8)])
+def test_label_indexer_group_sizes(sd, Hq, Hkv):
+    # Label waves hold 2, 16 and 3 (in a register set sized 4) rows.
+    inp, ch, lab = make("w4", seed=5, Hq=Hq, Hkv=Hkv, seq_lens=[9000, 20000, 777], N=20000)
+    out, idx, _ = run(sd, inp, ch, lab)
+    check(inp, ch, lab, out, idx, f"labels {Hq}/{Hkv}")
+
+
 def test_label_arguments_are_checked(sd):
     inp, ch, lab = make("w2")
     q, cache, lens = sd.cache_from_inputs(inp)
