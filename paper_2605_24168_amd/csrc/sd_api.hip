@@ -3,6 +3,7 @@
 // ordering of the kernels on the caller's stream.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cmath>
 #include <mutex>
@@ -610,7 +611,10 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   // five deviations of room; rows beyond it select from global memory.
   const int64_t want = 7 * k_max / 2 + 1024;
   const size_t pre_bytes = sd::select_lds_bytes(L.nchunk, 0);
-  const size_t budget = sd::select_lds_budget(p);
+  const int64_t room256 = (int64_t)sd::select_lds_budget(false) - (int64_t)pre_bytes;
+  const bool wide = sd::select_wide(
+      p, pre_bytes + 4 * (size_t)std::max<int64_t>(0, std::min<int64_t>(want, room256 / 4)));
+  const size_t budget = sd::select_lds_budget(wide);
   if (pre_bytes >= budget) return SD_ERR_UNSUPPORTED;
   const int64_t lds_room = (int64_t)((budget - pre_bytes) / 4);
   const int lds_cap = (int)(want < lds_room ? want : lds_room);
@@ -628,7 +632,7 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   if (e == hipSuccess) e = mark(2);
   if (e == hipSuccess && s.ncap > 0) e = sd::launch_repair(p, w, stream_h);
   if (e == hipSuccess) e = mark(3);
-  if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, stream_h);
+  if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, wide, stream_h);
   if (e == hipSuccess) e = mark(4);
   if (e == hipSuccess) e = sd::launch_attend(p, w, idx_ptr, out->data, true, stream_h);
   if (e == hipSuccess) e = mark(5);

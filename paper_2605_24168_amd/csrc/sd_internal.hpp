@@ -24,6 +24,7 @@ constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
 constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the fallback scoring
 constexpr int kSelectWideRows = 256; // fewer rows: 1024-thread selection workgroups
+constexpr size_t kSelectShareLds = 70 * 1024;  // more dynamic LDS: one workgroup per CU
 constexpr int kDenseWaveKeysMax = 8192; // keys per work item of the dense decode kernel
 constexpr int kDenseMaxGroup = 8;     // query heads per KV head of the dense decode kernel
 constexpr int kLabels = 8;            // label channels per key of the low-channel indexer
@@ -491,6 +492,8 @@ __device__ __forceinline__ void hist_add(uint32_t *hist, uint32_t dig, bool act)
 // only the top bits of T are resolved (the rest are zero): T is then a lower
 // bound of the k-th largest key.
 // ---------------------------------------------------------------------------
+constexpr int kSelU = 8;  // item loads in flight per thread in a selection pass
+
 struct SelShared {
   int scan[kMaxBlockWaves];
   uint32_t digit;
@@ -510,15 +513,18 @@ __device__ void radix_select(const Src &src, int n, int k, uint32_t *hist, SelSh
     const uint32_t dmask = (uint32_t)nb - 1u;
     for (int i = tid; i < nb; i += NT) hist[i] = 0;
     __syncthreads();
-    for (int base = 0; base < n; base += NT) {
-      const int p = base + tid;
-      uint32_t key = 0;
-      bool act = false;
-      if (p < n) {
-        key = src.key(p);
-        act = (key & mask) == prefix;
+    for (int base = 0; base < n; base += NT * kSelU) {
+      uint32_t key[kSelU];
+#pragma unroll
+      for (int u = 0; u < kSelU; ++u) {  // the loads in flight together
+        const int p = base + u * NT + tid;
+        key[u] = p < n ? src.key(p) : 0u;
       }
-      hist_add(hist, (key >> shift) & dmask, act);
+#pragma unroll
+      for (int u = 0; u < kSelU; ++u) {
+        const bool act = base + u * NT + tid < n && (key[u] & mask) == prefix;
+        hist_add(hist, (key[u] >> shift) & dmask, act);
+      }
     }
     __syncthreads();
     // Thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top.

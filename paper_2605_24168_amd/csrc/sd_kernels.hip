@@ -167,10 +167,17 @@ __device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, ui
   };
   for (int i = tid; i < kBuckets; i += NT) hist[i] = 0;
   __syncthreads();
-  for (int base = 0; base < n; base += NT) {
-    const int i = base + tid;
-    const uint32_t key = i < n ? keys[i] : kmin;
-    if (i < n) atomicAdd(&hist[bucket(key)], 1u);  // buckets spread the items
+  // keys may sit in global memory: kSelU loads in flight per thread
+  for (int base = 0; base < n; base += NT * kSelU) {
+    uint32_t key[kSelU];
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u) {
+      const int i = base + u * NT + tid;
+      key[u] = i < n ? keys[i] : kmin;
+    }
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u)
+      if (base + u * NT + tid < n) atomicAdd(&hist[bucket(key[u])], 1u);  // buckets spread the items
   }
   __syncthreads();
   // Thread t owns buckets [nb - (t+1)*bpt, nb - t*bpt), counted from the top.
@@ -199,12 +206,17 @@ __device__ bool bucket_kth(const uint32_t *keys, int n, int k, uint32_t kmin, ui
   const int m = (int)hist[bstar];
   bool found = false;
   if (m <= NT) {  // uniform
-    for (int base = 0; base < n; base += NT) {
-      const int i = base + tid;
-      if (i < n) {
-        const uint32_t key = keys[i];
-        if (bucket(key) == bstar) bs->items[atomicAdd(&bs->n, 1)] = key;
+    for (int base = 0; base < n; base += NT * kSelU) {
+      uint32_t key[kSelU];
+#pragma unroll
+      for (int u = 0; u < kSelU; ++u) {
+        const int i = base + u * NT + tid;
+        key[u] = i < n ? keys[i] : kmin;
       }
+#pragma unroll
+      for (int u = 0; u < kSelU; ++u)
+        if (base + u * NT + tid < n && bucket(key[u]) == bstar)
+          bs->items[atomicAdd(&bs->n, 1)] = key[u];
     }
     __syncthreads();
     if (tid < m) {
@@ -787,9 +799,10 @@ struct DenseSrc {
 
 // The candidates of one row, chunk by chunk: chunk c contributes
 // pre[c+1] - pre[c] items stored from offset start[c] of its block.  Keys
-// are read from LDS when they were staged there (lkey), else from the blocks.
+// are read from the flat copy (flat[i] = item i's key, in LDS or global
+// memory) once flatten_cands has made it; positions from the blocks.
 struct ChunkCands {
-  const uint32_t *lkey;
+  const uint32_t *flat;
   const int *pre;        // nch + 1 prefix sums (LDS)
   const int *start;      // nch block offsets (LDS)
   int nch;
@@ -810,10 +823,7 @@ struct ChunkCands {
   __device__ __forceinline__ int64_t slot(int c, int i) const {
     return (int64_t)c * cap + start[c] + (i - pre[c]);
   }
-  __device__ __forceinline__ uint32_t key(int i) const {
-    if (lkey) return lkey[i];
-    return gkey[slot(chunk_of(i), i)];
-  }
+  __device__ __forceinline__ uint32_t key(int i) const { return flat[i]; }
   __device__ __forceinline__ uint32_t pos(int i) const {
     const int c = chunk_of(i);
     return (uint32_t)c * (uint32_t)ck + gpos[slot(c, i)];
@@ -832,13 +842,46 @@ __device__ __forceinline__ void select_and_write(const Src &src, int n, int k, u
   });
 }
 
-// Candidates whose keys are staged in LDS (src.lkey), kmin..kmax their key
-// range: the k-th largest by bucket_kth (radix passes over the key bits
-// when it declines).  The compaction then records each kept item's index in
-// place of the consumed keys (slot <= item index, and a round reads all its
-// keys before its scans) and writes the softmax weights exp(scale * (s -
-// vmax)) (or, group-shared mode, the kept scores); finally every thread
-// fetches the positions of its kept items with the loads in flight together.
+// Copy the candidates' keys into flat[0, n) in item order, one wave per
+// chunk (coalesced reads of the chunk's block, coalesced writes), and widen
+// (mn, mx) by the keys this thread copied.
+template <int NT>
+__device__ __forceinline__ void flatten_cands(const ChunkCands &src, uint32_t *flat,
+                                              uint32_t &mn, uint32_t &mx) {
+  constexpr int kU = 8;  // loads in flight per lane
+  const int lane = lane_id();
+  for (int c = wave_id(); c < src.nch; c += NT / 64) {
+    const int cnt = src.pre[c + 1] - src.pre[c];
+    const uint32_t *from = src.gkey + (int64_t)c * src.cap + src.start[c];
+    uint32_t *to = flat + src.pre[c];
+    for (int j0 = lane; j0 < cnt; j0 += 64 * kU) {
+      uint32_t v[kU];
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int j = j0 + u * 64;
+        v[u] = j < cnt ? from[j] : 0u;
+      }
+#pragma unroll
+      for (int u = 0; u < kU; ++u) {
+        const int j = j0 + u * 64;
+        if (j < cnt) {
+          to[j] = v[u];
+          mn = v[u] < mn ? v[u] : mn;
+          mx = v[u] > mx ? v[u] : mx;
+        }
+      }
+    }
+  }
+}
+
+// Candidates whose keys sit in one flat array (src.flat: LDS, or the row's
+// global scratch when they do not fit), kmin..kmax their key range: the
+// k-th largest by bucket_kth (radix passes over the key bits when it
+// declines).  The compaction then records each kept item's index in place
+// of the consumed keys (slot <= item index, and a round reads all its keys
+// before its scans) and writes the softmax weights exp(scale * (s - vmax))
+// (or, group-shared mode, the kept scores); finally every thread fetches
+// the positions of its kept items with the loads in flight together.
 template <int NT>
 __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, int n, int k,
                                                         uint32_t kmin, uint32_t kmax,
@@ -849,9 +892,9 @@ __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, i
   const float vmax = key2f(kmax);
   uint32_t T;
   int need_eq;
-  if (!bucket_kth<NT>(src.lkey, n, k, kmin, kmax, hist, sh, bs, T, need_eq))
+  if (!bucket_kth<NT>(src.flat, n, k, kmin, kmax, hist, sh, bs, T, need_eq))
     radix_select<NT>(src, n, k, hist, sh, T, need_eq);
-  uint32_t *stage = const_cast<uint32_t *>(src.lkey);
+  uint32_t *stage = const_cast<uint32_t *>(src.flat);
   compact_selected<NT>(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
     stage[slot] = (uint32_t)i;
     const float v = key2f(key);
@@ -860,11 +903,16 @@ __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, i
   __syncthreads();
   constexpr int kP = 8;  // position loads in flight per thread
   for (int s0 = tid; s0 < k; s0 += NT * kP) {
-    uint32_t pos[kP];
+    uint32_t item[kP], pos[kP];
 #pragma unroll
     for (int u = 0; u < kP; ++u) {
       const int s = s0 + u * NT;
-      pos[u] = s < k ? src.pos((int)stage[s]) : 0u;
+      item[u] = s < k ? stage[s] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kP; ++u) {
+      const int s = s0 + u * NT;
+      pos[u] = s < k ? src.pos((int)item[u]) : 0u;
     }
 #pragma unroll
     for (int u = 0; u < kP; ++u) {
@@ -925,7 +973,7 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
       const int g = p.group_shared ? rr : rr / p.G;
       int *pre = (int *)dyn;          // nch + 1
       int *start = pre + (nch + 1);   // nch
-      uint32_t *lkey = (uint32_t *)(start + nch);
+      uint32_t *lkey = (uint32_t *)(start + nch);  // lds_cap keys
       const int2 *drow = w.dir + (int64_t)row * w.nchunk;
       int carry = 0;
       for (int base = 0; base < nch; base += NT) {
@@ -944,34 +992,17 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
       const int total = carry;
       const int64_t gblk = ((int64_t)b * p.Hkv + g) * w.nchunk * w.blk_cap;
       ChunkCands src{nullptr, pre, start, nch, w.ckey + gblk, w.cpos + gblk, ck, w.blk_cap};
-      if (total <= lds_cap) {
-        constexpr int kU = 16;  // loads in flight per thread
-        uint32_t mn = 0xFFFFFFFFu, mx = 0u;
-        for (int i0 = tid; i0 < total; i0 += NT * kU) {
-          uint32_t v[kU];
-#pragma unroll
-          for (int u = 0; u < kU; ++u) {
-            const int i = i0 + u * NT;
-            v[u] = i < total ? src.key(i) : 0u;
-          }
-#pragma unroll
-          for (int u = 0; u < kU; ++u) {
-            const int i = i0 + u * NT;
-            if (i < total) {
-              lkey[i] = v[u];
-              mn = v[u] < mn ? v[u] : mn;
-              mx = v[u] > mx ? v[u] : mx;
-            }
-          }
-        }
-        block_key_range<NT>(mn, mx, range);  // also publishes lkey
-        src.lkey = lkey;
-        select_and_write_staged<NT>(src, total, k, mn, mx, hist, &sh, &bs, irow, vrow, weights,
-                                p.scale);
-        weights_done = true;
-      } else {
-        select_and_write<NT>(src, total, k, hist, &sh, irow, vrow);
-      }
+      // The flat copy goes to LDS when it fits, else to the row's fallback
+      // score row, which an unflagged row does not use (the candidates are
+      // distinct positions of [lo, hi), so total <= ncap).
+      uint32_t *flat = total <= lds_cap ? lkey : (uint32_t *)(w.dense + (int64_t)row * p.ncap);
+      uint32_t mn = 0xFFFFFFFFu, mx = 0u;
+      flatten_cands<NT>(src, flat, mn, mx);
+      block_key_range<NT>(mn, mx, range);  // its barrier publishes the copy
+      src.flat = flat;
+      select_and_write_staged<NT>(src, total, k, mn, mx, hist, &sh, &bs, irow, vrow, weights,
+                                  p.scale);
+      weights_done = true;
     } else {
       select_and_write<NT>(DenseSrc{dense + (int64_t)row * ld + rp.lo, (uint32_t)rp.lo},
                            rp.hi - rp.lo, k, hist, &sh, irow, vrow);
@@ -1428,18 +1459,22 @@ size_t select_lds_bytes(int nchunk, int lds_cap) {
   return (size_t)(2 * nchunk + 1) * 4 + (size_t)lds_cap * 4;
 }
 
-size_t select_lds_budget(const Params &p) {
+bool select_wide(const Params &p, size_t lds_bytes) {
+  return (size_t)(p.B * p.R) < (size_t)kSelectWideRows || lds_bytes > kSelectShareLds;
+}
+
+size_t select_lds_budget(bool wide) {
   // Dynamic LDS left by the selection kernel's static LDS (hist, scan and
   // bucket scratch: about 9.4 KB at 256 threads, 12.6 KB at 1024) under the
   // 160 KB of a workgroup.
-  return (size_t)(p.B * p.R) < (size_t)kSelectWideRows ? 144 * 1024 : 150 * 1024;
+  return wide ? 144 * 1024 : 150 * 1024;
 }
 
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
-                                    hipStream_t st) {
+                                    bool wide, hipStream_t st) {
   const size_t lds = select_lds_bytes(w.nchunk, lds_cap);
   const unsigned rows = (unsigned)(p.B * p.R);
-  if (rows < kSelectWideRows)
+  if (wide)
     k_select<0, 1024><<<rows, 1024, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
   else
     k_select<0, kBlock><<<rows, kBlock, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);

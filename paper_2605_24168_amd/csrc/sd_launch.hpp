@@ -17,10 +17,15 @@ bool stream_by_head_quads(const Work &w);
 hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st,
                                hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 size_t select_lds_bytes(int nchunk, int lds_cap);
-// Dynamic LDS available to the candidate selection for these shapes.
-size_t select_lds_budget(const Params &p);
+// Whether the candidate selection runs 1024-thread workgroups: when the rows
+// are too few to fill the GPU one workgroup each, or when a workgroup's LDS
+// (lds_bytes, at the 256-thread budget) leaves room for no second one on a
+// compute unit, so that more loads are in flight per compute unit.
+bool select_wide(const Params &p, size_t lds_bytes);
+// Dynamic LDS available to the candidate selection at that width.
+size_t select_lds_budget(bool wide);
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
-                                    hipStream_t st);
+                                    bool wide, hipStream_t st);
 hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st);
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st);

@@ -105,6 +105,14 @@ def test_fixed_k_with_64_sinks(sd, K):
     check(inp, out, idx, f"K={K} + 64 sinks", k_override=ko)
 
 
+def test_forced_windows_at_low_sparsity(sd):
+    # Heavy fraction 1/3 of 65K positions: the candidates of a row exceed
+    # what a selection workgroup stages in LDS.
+    inp = make("w3", 64, 200, B=2, N=65536, Hq=8, Hkv=8, ratio=3.0, seq_lens=[65536, 50001])
+    out, idx = run_fused(sd, inp)
+    check(inp, out, idx, "sink 64 + local 200, heavy 1/3")
+
+
 def test_ragged_sequences_shorter_than_the_windows(sd):
     inp = make("w4", 100, 60, seq_lens=[0, 1, 50, 100, 160, 161, 300, 5000, 17001], N=17001)
     out, idx = run_fused(sd, inp)

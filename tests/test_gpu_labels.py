@@ -163,6 +163,13 @@ def test_label_indexer_group_sizes(sd, Hq, Hkv):
     check(inp, ch, lab, out, idx, f"labels {Hq}/{Hkv}")
 
 
+def test_label_indexer_low_sparsity(sd):
+    # 4x: more candidates per row than a selection workgroup stages in LDS.
+    inp, ch, lab = make("w4", seed=6, Hq=8, Hkv=8, seq_lens=[65536, 40000], N=65536, ratio=4.0)
+    out, idx, _ = run(sd, inp, ch, lab)
+    check(inp, ch, lab, out, idx, "labels 4x")
+
+
 def test_label_arguments_are_checked(sd):
     inp, ch, lab = make("w2")
     q, cache, lens = sd.cache_from_inputs(inp)

@@ -288,6 +288,28 @@ def test_long_candidate_lists(sd, name, ratio):
     check_fused(inp, out, idx, label=f"{name} ratio {ratio}")
 
 
+@pytest.mark.parametrize("name,kw", [
+    ("w3", dict(B=1, N=65536, Hq=8, Hkv=8, ratio=4.0)),
+    ("w3", dict(B=2, N=65536, Hq=8, Hkv=8, ratio=3.0, seq_lens=[65536, 50001])),
+    ("w5", dict(N=65536 + 77, ratio=4.0)),
+])
+def test_candidates_beyond_the_lds_select_from_global_scratch(sd, name, kw):
+    # k of 12K-22K: the ~2.5 k candidates of a row exceed the ~36K keys a
+    # selection workgroup stages in LDS, so a row that does not take the
+    # exact fallback copies its candidates into its unused fallback score row
+    # and selects there.
+    inp = make(name, seed=21, **kw)
+    sd.set_profiling(True)
+    try:
+        out, idx, _ = gpu_fused(sd, inp)
+        prof = sd.last_profile()
+    finally:
+        sd.set_profiling(False)
+    rows_with_k = sum(inp.rows for L in inp.seq_lens if L > 0)
+    assert prof["repaired_rows"] < rows_with_k
+    check_fused(inp, out, idx, label=f"{name} ratio {inp.ratio} from global scratch")
+
+
 def test_clustered_candidates_overflow_to_the_exact_fallback(sd):
     # 400 consecutive keys close to head 0's query direction: with 8 heads
     # per group a row's staging area holds 128 keys per scoring wave (of at
