@@ -64,6 +64,60 @@ def path_bytes(inp, ks, labels=False):
     return key_stream, gather, small
 
 
+def union_gather_rows(torch, idx, inp):
+    """Distinct (KV head, position) pairs of a step's index lists: the value
+    rows a group-deduplicated gather would read (per-head mode lists the
+    same position once per query head that keeps it)."""
+    if inp.group_shared or inp.G == 1:
+        return int((idx >= 0).sum().item())
+    s = idx.view(inp.B, inp.Hkv, -1).sort(dim=-1).values
+    first = torch.ones_like(s, dtype=torch.bool)
+    first[..., 1:] = s[..., 1:] != s[..., :-1]
+    return int(((s >= 0) & first).sum().item())
+
+
+def read_peak(torch, sd, gib=4, reps=10):
+    """Median rate of a plain streaming read of a gib-GiB device buffer
+    (the library's read probe), GB/s."""
+    buf = torch.zeros(gib << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for _ in range(2):
+        sd.read_probe(buf, sink)
+    ms = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        sd.read_probe(buf, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    del buf
+    ms.sort()
+    return (gib << 30) / (ms[len(ms) // 2] * 1e-3) / 1e9
+
+
+def flushed_calls(torch, fn, n, flush_gib=1):
+    """n calls, each timed alone by events around it, with a flush_gib-GiB
+    buffer written before each (outside the events) so that no cache holds
+    the previous call's data.  Returns (median, p10, p90) in ms."""
+    flush = torch.empty(flush_gib << 30, dtype=torch.uint8, device="cuda")
+    ms = []
+    for _ in range(n):
+        flush.zero_()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    del flush
+    ms.sort()
+    pick = lambda f: ms[min(len(ms) - 1, int(round(f * (len(ms) - 1))))]
+    return pick(0.5), pick(0.1), pick(0.9)
+
+
 def counters_traffic():
     """HBM bytes per launch of the scoring kernel from committed rocprofv3
     counters, if they were taken on the current kernel source."""
@@ -353,6 +407,8 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device to device once (a plain "
                          "copy of known size that scales hardware traffic counters)")
+    ap.add_argument("--calls", type=int, default=30,
+                    help="calls timed one by one after a cache flush (median/p10/p90; 0: skip)")
     ap.add_argument("--sink", type=int, default=0,
                     help="forced first positions of every sequence (sink window)")
     ap.add_argument("--local", type=int, default=0,
@@ -472,6 +528,17 @@ def main():
     sd.set_profiling(False)
     prof = sd.profile_mean()
 
+    # Calls one by one, each after a cache flush (events around each call).
+    calls = None
+    if args.calls > 0:
+        log(f"timing {args.calls} calls one by one after a cache flush")
+        med, p10, p90 = flushed_calls(torch, one_step, args.calls)
+        calls = {"n": args.calls, "median_ms": med, "p10_ms": p10, "p90_ms": p90,
+                 "queries_per_s_at_median": inp.B / (med * 1e-3),
+                 "timing": "HIP events around each call on its stream; a 1 GiB device buffer "
+                           "written before each call, outside the events"}
+    union_rows = union_gather_rows(torch, idx, inp)
+
     # Dense decode attention over the same cache: the full-attention baseline.
     dense = None
     if inp.dtype == "bf16" and inp.G <= 8:
@@ -493,6 +560,8 @@ def main():
     score_ms = score_prof["score_ms"]
     score_gbps = score_alg / (score_ms * 1e-3) / 1e9 if score_ms > 0 else None
     traffic = None if args.labels else counters_traffic()  # counters are of the exact stream
+    log("measuring the plain streaming-read rate (read probe, 4 GiB)")
+    peak_read = read_peak(torch, sd)
 
     rec = {
         "metric": METRIC,
@@ -525,6 +594,8 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": score_alg,
             "avg_launch_ms": score_ms,
+            "measured_read_peak_GBps": peak_read,
+            "frac_of_measured_read_peak": score_gbps / peak_read if score_gbps else None,
             "timing": "HIP events attached to every scoring dispatch (call's stream) over K "
                       "steps run right after the uninstrumented timed region",
         },
@@ -534,6 +605,8 @@ def main():
             "algorithmic_bytes": total_b,
             "key_stream_bytes": key_b,
             "value_gather_bytes": gather_b,
+            "value_rows_gathered_per_head": sum(int(k) for k in ks) * inp.rows,
+            "value_rows_union_per_kv_head": union_rows,
             "query_heads_per_s": inp.B * inp.Hq / (ms_step * 1e-3),
             "ms_per_step_events": ms_events,
             "ms_per_step_with_kernel_events": ms_timed_kernel,
@@ -543,6 +616,7 @@ def main():
             "repaired_rows_last_step": prof["repaired_rows"],
         },
         "dense_baseline": dense,
+        "calls_after_flush": calls,
     }
     del q, cache, lens, out, idx, ws
     if args.copy_mib > 0:

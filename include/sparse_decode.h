@@ -272,6 +272,17 @@ sd_status sparse_decode_profile_mean(sd_profile *out, int32_t *n_calls);
  * exact fallback path (used by tests to exercise it).  0 restores normal. */
 sd_status sparse_decode_set_debug(int32_t flags);
 
+/* Measurement helper, not a step of the method: one streaming read of
+ * `bytes` bytes of device memory at `buf` (16-byte aligned, bytes a nonzero
+ * multiple of 16), enqueued on `stream`.  Every byte is read once: one
+ * contiguous 256 KB span per workgroup, nontemporal 16-byte loads, eight in
+ * flight per lane; nothing is written except, with
+ * negligible probability, *sink (one caller-owned device uint32).  Timed by
+ * the caller, it gives this device's plain streaming-read rate, the
+ * reference for the bandwidth-bound kernels.  SD_ERR_INVALID_ARG for a null,
+ * misaligned or empty buffer (checked before any HIP call). */
+sd_status sparse_decode_read_probe(const void *buf, size_t bytes, uint32_t *sink, void *stream);
+
 const char *sparse_decode_status_string(sd_status status);
 
 #ifdef __cplusplus

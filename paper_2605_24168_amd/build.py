@@ -9,7 +9,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsparse_decode.so")
-SOURCES = ["sd_api.hip", "sd_kernels.hip", "sd_dense.hip"]
+SOURCES = ["sd_api.hip", "sd_kernels.hip", "sd_dense.hip", "sd_probe.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -111,6 +111,8 @@ lib.sparse_decode_profile_mean.restype = C.c_int
 lib.sparse_decode_profile_mean.argtypes = [_P(SdProfile), _P(C.c_int32)]
 lib.sparse_decode_set_debug.restype = C.c_int
 lib.sparse_decode_set_debug.argtypes = [C.c_int32]
+lib.sparse_decode_read_probe.restype = C.c_int
+lib.sparse_decode_read_probe.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p]
 lib.sparse_decode_status_string.restype = C.c_char_p
 lib.sparse_decode_status_string.argtypes = [C.c_int]
 
@@ -436,6 +438,19 @@ def profile_mean() -> dict:
     d = {f: getattr(p, f) for f, _ in SdProfile._fields_}
     d["calls"] = int(n.value)
     return d
+
+
+def read_probe(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:
+    """One plain streaming read of buf (device, contiguous, 16-byte aligned):
+    the device's reference read rate when timed.  sink: a device int32/uint32
+    scalar the kernel may write."""
+    _need_device(buf, "buf")
+    _need_device(sink, "sink")
+    if not buf.is_contiguous():
+        raise ValueError("buf must be contiguous")
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib.sparse_decode_read_probe(buf.data_ptr(), nbytes, sink.data_ptr(), _stream(stream)),
+           "sparse_decode_read_probe")
 
 
 def set_debug(flags: int) -> None:

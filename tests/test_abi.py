@@ -298,3 +298,14 @@ def test_binding_refuses_host_tensors(sd):
                        v=torch.zeros((1, 8, 64, 128), dtype=torch.bfloat16))
     with pytest.raises(ValueError):
         sd.sparse_decode_attention(q, cache, torch.zeros(1, dtype=torch.int32), sd.Sparsity(10.0))
+
+
+def test_read_probe_checks_its_buffer_on_the_host(sd):
+    probe = sd.lib.sparse_decode_read_probe
+    sink = FAKE
+    assert probe(None, 1024, sink, None) == -1          # no buffer
+    assert probe(FAKE + 8, 1024, sink, None) == -1      # misaligned
+    assert probe(FAKE, 1000, sink, None) == -1          # not a multiple of 16 bytes
+    assert probe(FAKE, 0, sink, None) == -1             # empty
+    assert probe(FAKE, 1024, None, None) == -1          # no sink
+    assert probe(FAKE, 1024, FAKE + 2, None) == -1      # misaligned sink

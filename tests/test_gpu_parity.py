@@ -462,3 +462,14 @@ def test_full_size_workloads_on_sampled_sequences(sd, cfg, sample):
         assert (row[:, k:] == -1).all() and (row[:, :k] >= 0).all()
         assert (row[:, :k] < inp.seq_lens[b]).all()
         assert (np.diff(row[:, :k], axis=1) > 0).all()
+
+
+def test_read_probe_reads_buffers_of_any_length(sd):
+    # The bandwidth reference the bench reports: any multiple of 16 bytes,
+    # from one 16-byte word to more than the grid covers in one sweep.
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    for n in (16, 16 * 255, 1 << 20, (64 << 20) + 48):
+        buf = torch.zeros(n, dtype=torch.uint8, device="cuda")
+        sd.read_probe(buf, sink)
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 0   # zeros XOR to 0, never the store's value
