@@ -1492,21 +1492,32 @@ hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st) {
 constexpr int kAttendWorkgroups = 1024;   // enough to fill the chip
 constexpr int kAttendLdsMax = 60 * 1024;  // dynamic LDS of one attend workgroup
 constexpr int kAttendMinEntries = 64;     // fewest list entries worth a workgroup of their own
+constexpr int kAttendRowsWhole = 256;     // this many rows fill the chip unsplit
 
-// Positions per attend workgroup: about kAttendWorkgroups workgroups over
-// all rows, at least 64 positions each, within the LDS budget.
+// Positions per attend workgroup: a row is not split when there are enough
+// rows to give every CU a workgroup and the whole list fits one workgroup's
+// LDS (a split then costs the merge launch, more than the extra parallelism
+// saves); otherwise rows are split into about kAttendWorkgroups workgroups
+// in all, at least 64 positions each, within the LDS budget.
 int attend_split(const Params &p, int k_max_positions, bool fused) {
   const int64_t rows = (int64_t)p.B * p.R;
   const int64_t k_max = k_max_positions > 0 ? k_max_positions : 1;
   const int nh = p.group_shared ? p.G : 1;
   const bool rc = attend_recompute(fused, p);
   int64_t nsplit = (kAttendWorkgroups + rows - 1) / rows;
+  if (rows >= kAttendRowsWhole && k_max <= 4096 &&  // (bounded: the LDS sum stays in int)
+      AttLds((int)((k_max + 63) / 64 * 64), nh, rc).total <= kAttendLdsMax)
+    nsplit = 1;
   const int64_t most = (k_max + kAttendMinEntries - 1) / kAttendMinEntries;
   if (nsplit > most) nsplit = most;
   if (nsplit < 1) nsplit = 1;
   int64_t split = (k_max + nsplit - 1) / nsplit;
   split = (split + 63) / 64 * 64;
   while (split > 64 && AttLds((int)split, nh, rc).total > kAttendLdsMax) split -= 64;
+  // As many splits as that takes, the entries spread evenly over them (no
+  // smaller than the LDS-capped size, so still within the budget).
+  nsplit = (k_max + split - 1) / split;
+  split = ((k_max + nsplit - 1) / nsplit + 63) / 64 * 64;
   return (int)split;
 }
 
