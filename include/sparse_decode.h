@@ -268,8 +268,11 @@ sd_status sparse_decode_set_profiling(int32_t enable);
 sd_status sparse_decode_last_profile(sd_profile *out);
 sd_status sparse_decode_profile_mean(sd_profile *out, int32_t *n_calls);
 
-/* Debug switch: with flags & 1 every row of sparse_decode_attention takes the
- * exact fallback path (used by tests to exercise it).  0 restores normal. */
+/* Debug switch (used by tests to exercise paths): with flags & 1 every row of
+ * sparse_decode_attention takes the exact fallback path; flags & 4 / & 8
+ * turn the group-deduplicated attention off / on wherever it applies
+ * (per-head rows with recomputed logits, bf16, 2 or more heads per group),
+ * overriding the cost rule.  0 restores normal. */
 sd_status sparse_decode_set_debug(int32_t flags);
 
 /* Measurement helper, not a step of the method: one streaming read of

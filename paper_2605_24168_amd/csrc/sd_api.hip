@@ -220,9 +220,37 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
 // Workspace layout.  Sizes depend only on the shapes and the sparsity, so
 // the same layout is recomputed on every call.
 struct Layout {
-  size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, total;
+  size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, umask, total;
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
+  int64_t umask_stride;  // bytes per group of the head masks (0: none)
+  int union_chunk;       // positions per union-attention workgroup (0: per-row lists)
 };
+
+// The group-deduplicated attention applies to fused per-head rows whose
+// logits are recomputed (label selection or forced positions), bf16 GQA.
+bool union_eligible(const Shape &s, const sd_sparsity *sp, bool labels) {
+  return !sp->group_shared && s.G >= 2 && s.bf16 && s.ncap > 0 &&
+         (labels || sp->n_sink + sp->n_local > 0);
+}
+
+// Whether it is faster than per-head lists: each head's k_max kept rows
+// (key + value, 512 B) against the expected union of G such sets of an
+// Ncap-position range drawn independently (heads that agree only shrink the
+// union), plus clearing, reading and marking the masks.  The group-row
+// kernel gathers at about 0.7 of the per-head kernel's rate (half the rows
+// in flight per wave, two waves per SIMD against four, measured at 128K),
+// so the union must move under 0.65 of the bytes.  Debug flags 4 / 8 force
+// it off / on.
+bool union_pays(const Shape &s, int64_t k_max) {
+  const int dbg = g_debug.load();
+  if (dbg & 4) return false;
+  if (dbg & 8) return true;
+  const double Lc = (double)s.ncap, G = s.G;
+  const double kt = (double)(k_max < s.ncap ? k_max : s.ncap);
+  const double per_head = G * kt * 512.0;
+  const double uni = Lc * (1.0 - std::pow(1.0 - kt / Lc, G)) * 512.0 + 2.0 * G * Lc + G * kt;
+  return uni < 0.65 * per_head;
+}
 
 Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp,
                   bool labels = false) {
@@ -248,6 +276,12 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
   shape_only.n_sink = sp->n_sink;
   shape_only.n_local = sp->n_local;
   L.nsplit = sd::attend_nsplit(shape_only);
+  const bool uni_ok = fused && union_eligible(s, sp, labels);
+  if (uni_ok && union_pays(s, k_max)) {
+    L.union_chunk = sd::union_chunk(shape_only);
+    const int un = (int)((s.ncap + L.union_chunk - 1) / L.union_chunk);
+    L.nsplit = un > L.nsplit ? un : L.nsplit;
+  }
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t o = off;
@@ -264,6 +298,12 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
     L.flags = take((size_t)rows * 4);
     L.dense = take((size_t)rows * s.ncap * 4);
     L.sigma = take((size_t)rows * k_max * 4);
+    if (uni_ok) {  // present whenever the call could use it (see union_pays)
+      L.umask_stride = (int64_t)((s.ncap * s.G + 15) / 16 * 16);
+      L.umask = take((size_t)s.B * s.Hkv * L.umask_stride);
+      L.nsplit = std::max<int>(L.nsplit, (int)((s.ncap + sd::union_chunk(shape_only) - 1) /
+                                               sd::union_chunk(shape_only)));
+    }
   }
   L.part = take((size_t)s.B * s.Hq * L.nsplit * sd::kPartStride * 4);
   L.stats = take(64);
@@ -324,6 +364,9 @@ sd::Work carve(char *base, const Layout &L, bool fused) {
   }
   w.part = (float *)(base + L.part);
   w.stats = (int32_t *)(base + L.stats);
+  w.umask = L.union_chunk > 0 ? (uint8_t *)(base + L.umask) : nullptr;
+  w.umask_stride = L.umask_stride;
+  w.union_chunk = L.union_chunk;
   w.nchunk = L.nchunk;
   w.wave_keys = L.wave_keys;
   w.chunk_keys = L.chunk_keys;
@@ -376,7 +419,9 @@ sd_status sparse_decode_workspace_size(const sd_tensor *q, const sd_kv *K, const
   int64_t k_max = 0;
   st = check_idx(idx, s, sp, k_max);
   if (st) return st;
-  *bytes = layout_for(s, k_max, true, sp).total;
+  // Enough for the exact-score and the label-indexer calls alike.
+  *bytes = std::max(layout_for(s, k_max, true, sp, false).total,
+                    layout_for(s, k_max, true, sp, true).total);
   return SD_OK;
 }
 

@@ -91,6 +91,15 @@ struct Work {
   int32_t blk_cap;     // entries per packed block: kChunkCap, or kCandBuf
   int32_t nsplit;
   int32_t force_repair;  // every row takes the exact fallback
+  // Group-deduplicated attention (per-head rows whose logits are recomputed,
+  // GQA): umask[(b*Hkv + g) * umask_stride + j*G + h] = 1 when head h of
+  // group g keeps position j (cleared in the call before the selection marks
+  // it); the attention then reads each kept key and value row once for the
+  // whole group, union_chunk positions per workgroup.  Null / 0: per-row
+  // lists.
+  uint8_t *umask;
+  int64_t umask_stride;  // bytes per group, a multiple of 16
+  int32_t union_chunk;
 };
 
 // Scratch of the dense decode kernels.

@@ -755,6 +755,16 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   const int k = row_plan(p, b, L).kh;
   const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
   const int tid = threadIdx.x;
+  if (w.umask) {
+    // The group's head masks (union attention), cleared before the
+    // selection marks the kept positions: part `part` of the 16-byte words.
+    u32x4 *gm = (u32x4 *)(w.umask + (int64_t)bg * w.umask_stride);
+    const int64_t nw = w.umask_stride / 16;
+    const int64_t per = (nw + kRepairParts - 1) / kRepairParts;
+    const int64_t w1 = (part + 1) * per < nw ? (part + 1) * per : nw;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    for (int64_t i = part * per + tid; i < w1; i += kBlock) gm[i] = z;
+  }
   if (tid < kMaxGroup) {
     cnt[tid] = 0;
     bad[tid] = 0;
@@ -1021,6 +1031,13 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
     lrow[i] = -1;
     if (lvals) lvals[i] = -__builtin_inff();
   }
+  if (MODE == 0 && w.umask) {
+    // Union attention: mark this head's kept positions in its group's mask.
+    __syncthreads();  // the list was written by every thread of the block
+    const int rr = row % p.R;
+    uint8_t *gm = w.umask + ((int64_t)b * p.Hkv + rr / p.G) * w.umask_stride + rr % p.G;
+    for (int i = tid; i < rp.total; i += NT) gm[(int64_t)lrow[i] * p.G] = 1;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1041,6 +1058,8 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
 // red[kWaves][nhb][128] f32, lred[kWaves][nhb] f32, nhb = min(nh, kAttHeads).
 // ---------------------------------------------------------------------------
 constexpr int kAttHeads = 8;  // heads accumulated per pass over the value rows
+constexpr int kUnionPerThread = 4;  // union attention: mask positions per thread
+constexpr int kUnionChunkMax = kBlock * kUnionPerThread;  // positions per workgroup
 
 template <bool BF16>
 struct RowRaw {
@@ -1101,14 +1120,15 @@ __host__ __device__ inline bool attend_recompute(bool fused, const Params &p) {
 
 // Byte offsets of the dynamic LDS areas of k_attend (host and device agree).
 struct AttLds {
-  int voff, koff, e, pos, q, red, lred, total;
-  __host__ __device__ AttLds(int split, int nh, bool recompute) {
+  int voff, koff, e, pos, hm, q, red, lred, total;
+  __host__ __device__ AttLds(int split, int nh, bool recompute, bool uni = false) {
     const int nhb = nh < kAttHeads ? nh : kAttHeads;
     int o = 0;
     voff = o; o += 8 * split;
     koff = o; o += recompute ? 8 * split : 0;
     e = o; o += 4 * nh * split;
     pos = o; o += 4 * split;
+    hm = o; o += uni ? 4 * split : 0;
     q = o; o += recompute ? 4 * nh * kHeadDim : 0;
     red = o; o += 4 * kWaves * nhb * kHeadDim;
     lred = o; o += 4 * kWaves * nhb;
@@ -1116,9 +1136,14 @@ struct AttLds {
   }
 };
 
-template <bool BF16, bool FUSED, bool GRP>
+// UNI (union attention, with FUSED and GRP): the workgroup of (chunk s,
+// group (b, g)) takes the positions [s*split, +split) that any head of the
+// group keeps (the group's head masks), in order, and serves every head,
+// each over its own positions only.
+template <bool BF16, bool FUSED, bool GRP, bool UNI = false>
 __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32_t *idx, void *out,
                                                    int split) {
+  static_assert(!UNI || (BF16 && FUSED && GRP), "union attention: fused bf16 group rows");
   extern __shared__ int64_t att_dyn[];
   __shared__ float mh[kMaxGroup];
   __shared__ float hmax[kWaves][kMaxGroup];
@@ -1126,23 +1151,25 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   constexpr int HB = GRP ? kAttHeads : 1;  // heads accumulated per pass
 
   const int s = blockIdx.x, row = blockIdx.y;
-  const int b = row / p.R, r = row % p.R;
+  const int rows_per_b = UNI ? p.Hkv : p.R;  // union rows are the groups
+  const int b = row / rows_per_b, r = row % rows_per_b;
   constexpr bool grp = GRP;
   const int nh = grp ? p.G : 1;
   const int nhb = nh < kAttHeads ? nh : kAttHeads;
   const int h0 = grp ? r * p.G : r;
   const int g = grp ? r : r / p.G;
   const int L = seq_len(p, b);
-  const int n_list = attend_list_len(p, b, L, FUSED);
+  const int n_list = UNI ? L : attend_list_len(p, b, L, FUSED);
   const int nsp = (n_list + split - 1) / split;
   const int tid = threadIdx.x, l = lane_id(), col = l & 15, sub = l >> 4, wv = wave_id();
-  const bool recompute = attend_recompute(FUSED, p);
-  const AttLds lay(split, nh, recompute);
+  const bool recompute = UNI || attend_recompute(FUSED, p);
+  const AttLds lay(split, nh, recompute, UNI);
   char *dyn = (char *)att_dyn;
   int64_t *voff_l = (int64_t *)(dyn + lay.voff);
   int64_t *koff_l = (int64_t *)(dyn + lay.koff);
   float *e_l = (float *)(dyn + lay.e);
   int32_t *pos_l = (int32_t *)(dyn + lay.pos);
+  uint32_t *hm_l = (uint32_t *)(dyn + lay.hm);  // UNI: each entry's head bits
   float *q_l = (float *)(dyn + lay.q);        // [nh][128]
   float *red = (float *)(dyn + lay.red);      // [kWaves][nhb][128]
   float *lred = (float *)(dyn + lay.lred);    // [kWaves][nhb]
@@ -1155,18 +1182,77 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   }
   if (s >= nsp) return;
   const int e0 = s * split;
-  const int n = (n_list - e0) < split ? (n_list - e0) : split;
+  int n = (n_list - e0) < split ? (n_list - e0) : split;
   const int32_t *irow = idx + (int64_t)row * p.k_max + e0;
 
-  // Resolve every entry to its row offsets once (page-table reads in
-  // parallel); skipped entries point at position 0 and get weight 0.
-  for (int t = tid; t < n; t += kBlock) {
-    int32_t j = irow[t];
-    if (j < 0 || j >= L) j = -1;
-    pos_l[t] = j;
-    const int64_t jc = j >= 0 ? j : 0;
-    voff_l[t] = kv_offset(p.V, b, g, jc);
-    if (recompute) koff_l[t] = kv_offset(p.K, b, g, jc);
+  if constexpr (UNI) {
+    // The chunk's positions that some head keeps, in order, with their head
+    // bits: each thread packs the G mask bytes of kU consecutive positions,
+    // then one block scan places the kept ones.
+    __shared__ int scan_tmp[kWaves];
+    const uint8_t *gm = w.umask + ((int64_t)b * p.Hkv + g) * w.umask_stride + (int64_t)e0 * p.G;
+    uint32_t bits[kUnionPerThread];
+    int cnt = 0;
+    const int t0u = tid * kUnionPerThread;  // n <= split <= kUnionChunkMax
+    if (nh % 4 == 0 && t0u + kUnionPerThread <= n) {
+      // This thread's 4 G mask bytes in 16-byte loads (the group's masks
+      // start 16-byte aligned, and so does every 4 positions' span here).
+      const u32x4 *src = (const u32x4 *)(gm + (int64_t)t0u * nh);
+#pragma unroll
+      for (int u = 0; u < kUnionPerThread; ++u) bits[u] = 0u;
+      for (int v = 0; v < nh / 4; ++v) {  // the bytes in order: position u * nh + head h
+        const u32x4 x = src[v];
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+          const int byte = 16 * v + c;  // = position u * nh + head h
+          const uint32_t nz = ((x[c >> 2] >> (8 * (c & 3))) & 0xFFu) != 0u ? 1u : 0u;
+          const int u = byte / nh, h = byte % nh;
+#pragma unroll
+          for (int uu = 0; uu < kUnionPerThread; ++uu)
+            if (uu == u) bits[uu] |= nz << h;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnionPerThread; ++u) cnt += bits[u] != 0u ? 1 : 0;
+    } else {
+#pragma unroll
+      for (int u = 0; u < kUnionPerThread; ++u) {
+        const int t = t0u + u;
+        uint32_t m = 0u;
+        if (t < n)
+          for (int h = 0; h < nh; ++h) m |= (uint32_t)(gm[(int64_t)t * nh + h] != 0) << h;
+        bits[u] = m;
+        cnt += m != 0u ? 1 : 0;
+      }
+    }
+    int tot;
+    int slot = block_excl_scan<kBlock>(cnt, scan_tmp, &tot);
+#pragma unroll
+    for (int u = 0; u < kUnionPerThread; ++u) {
+      if (bits[u]) {
+        pos_l[slot] = e0 + tid * kUnionPerThread + u;
+        hm_l[slot] = bits[u];
+        ++slot;
+      }
+    }
+    n = tot;
+    __syncthreads();
+    for (int t = tid; t < n; t += kBlock) {
+      const int64_t j = pos_l[t];
+      voff_l[t] = kv_offset(p.V, b, g, j);
+      koff_l[t] = kv_offset(p.K, b, g, j);
+    }
+  } else {
+    // Resolve every entry to its row offsets once (page-table reads in
+    // parallel); skipped entries point at position 0 and get weight 0.
+    for (int t = tid; t < n; t += kBlock) {
+      int32_t j = irow[t];
+      if (j < 0 || j >= L) j = -1;
+      pos_l[t] = j;
+      const int64_t jc = j >= 0 ? j : 0;
+      voff_l[t] = kv_offset(p.V, b, g, jc);
+      if (recompute) koff_l[t] = kv_offset(p.K, b, g, jc);
+    }
   }
   if (recompute && !BF16) {  // float32 queries for the vector-ALU logits
     for (int e = tid; e < nh * kHeadDim; e += kBlock) {
@@ -1209,10 +1295,12 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
         const int t = tt * kTile + kcol;
         if (t < n) {
           const bool skip = pos_l[t] < 0;
+          const uint32_t hb = UNI ? hm_l[t] : 0xFFFFFFFFu;  // heads that keep it
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int h = 4 * quad + r;
-            if (h < nh) e_l[h * split + t] = skip ? -__builtin_inff() : p.scale * acc[r];
+            if (h < nh)
+              e_l[h * split + t] = (skip || !((hb >> h) & 1u)) ? -__builtin_inff() : p.scale * acc[r];
           }
         }
       }
@@ -1382,7 +1470,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(Params p, Work w, void 
   __shared__ MergeShared sh;
   const int bh = blockIdx.x, b = bh / p.Hq;
   const int L = seq_len(p, b);
-  const int n_list = attend_list_len(p, b, L, FUSED);
+  const int n_list = w.union_chunk ? L : attend_list_len(p, b, L, FUSED);
   const int nsp = (n_list + split - 1) / split;
   if (nsp <= 1 || L == 0) return;  // written directly by k_attend
   const float v = merge_partials(w.part + (int64_t)bh * w.nsplit * kPartStride, nsp, sh);
@@ -1534,8 +1622,25 @@ int attend_nsplit(const Params &p) {
   return most;
 }
 
+int union_chunk(const Params &p) {
+  int c = kUnionChunkMax;
+  while (c > 64 && AttLds(c, p.G, true, true).total > kAttendLdsMax) c -= 64;
+  return c;
+}
+
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st) {
+  if (fused && w.union_chunk > 0) {  // group-deduplicated attention
+    if (!p.bf16 || p.group_shared || w.union_chunk > kUnionChunkMax || !w.umask)
+      return hipErrorInvalidValue;
+    const int split = w.union_chunk;
+    const size_t lds = (size_t)AttLds(split, p.G, true, true).total;
+    const int nsplit = (int)((p.ncap + split - 1) / split);
+    k_attend<true, true, true, true><<<dim3(nsplit, p.B * p.Hkv), kBlock, lds, st>>>(p, w, idx, out,
+                                                                                      split);
+    if (nsplit > 1) k_merge<true, true><<<(unsigned)(p.B * p.Hq), kMergeThreads, 0, st>>>(p, w, out, split);
+    return hipGetLastError();
+  }
   const int split = attend_split(p, p.k_max, fused);
   const size_t lds = (size_t)AttLds(split, p.group_shared ? p.G : 1,
                                     attend_recompute(fused, p)).total;

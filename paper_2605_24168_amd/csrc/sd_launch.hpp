@@ -30,6 +30,8 @@ hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st);
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st);
 int attend_nsplit(const Params &p);
+// Positions per workgroup of the group-deduplicated attention (fits the LDS).
+int union_chunk(const Params &p);
 hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st);
 hipError_t launch_topk(const Params &p, const float *scores, int32_t *idx, float *vals,
                        hipStream_t st);

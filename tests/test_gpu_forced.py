@@ -149,3 +149,21 @@ def test_stage_topk_with_forced_positions_is_bit_exact(sd):
         for r in range(0, inp.rows, 7):
             n = int((gi[b, r] >= 0).sum())
             np.testing.assert_array_equal(v[b, r, :n], s_host[b, r, gi[b, r, :n]])
+
+
+@pytest.mark.parametrize("Hq,Hkv,flags", [(32, 8, 0), (32, 2, 8), (16, 4, 8)])
+def test_forced_windows_union_attention(sd, Hq, Hkv, flags):
+    # Sink and local windows beside a heavy 1/3 (the cost rule picks the
+    # group-deduplicated attention), or forced on (flag 8) at the workload's
+    # sparsity; a 16-head group takes two passes over the heads.
+    ratio = 3.0 if flags == 0 else None
+    kw = dict(B=3, N=40000, Hq=Hq, Hkv=Hkv, seq_lens=[40000, 333, 25000])
+    if ratio:
+        kw["ratio"] = ratio
+    inp = make("w4", 64, 200, **kw)
+    sd.set_debug(flags)
+    try:
+        out, idx = run_fused(sd, inp)
+    finally:
+        sd.set_debug(0)
+    check(inp, out, idx, f"union {Hq}/{Hkv} flags {flags}")

@@ -184,3 +184,37 @@ def test_label_arguments_are_checked(sd):
     with pytest.raises(sd.SparseDecodeError) as e:
         sd.sparse_decode_label_attention(q, cache, short, lens, sp, k_max=O.k_max_for(inp))
     assert e.value.status == sd.SD_ERR_INVALID_ARG
+
+
+def _with_debug(sd, flags, fn):
+    sd.set_debug(flags)
+    try:
+        return fn()
+    finally:
+        sd.set_debug(0)
+
+
+@pytest.mark.parametrize("Hq,Hkv,ratio", [(32, 8, 3.0), (16, 8, 2.0), (32, 2, 4.0)])
+def test_label_union_attention_at_low_sparsity(sd, Hq, Hkv, ratio):
+    # GQA at low sparsity: the heads of a group keep overlapping positions,
+    # and the attention reads each kept key and value row once per group
+    # (debug flag 8 forces it; the cost rule picks it for 4 and 16 heads
+    # here).  Checked against the oracle and against per-head lists (flag 4
+    # turns the union off).
+    inp, ch, lab = make("w4", seed=7, Hq=Hq, Hkv=Hkv, seq_lens=[65536, 40001, 0, 1000],
+                        N=65536, ratio=ratio)
+    out, idx, _ = _with_debug(sd, 8, lambda: run(sd, inp, ch, lab))
+    assert (idx[2] == -1).all() and (out[2] == 0).all()
+    check(inp, ch, lab, out, idx, f"labels union {Hq}/{Hkv} {ratio}x")
+    out2, idx2, _ = _with_debug(sd, 4, lambda: run(sd, inp, ch, lab))
+    np.testing.assert_array_equal(idx, idx2)
+    ok, ratio_err, _ = P.out_errors(out2, out, inp.dtype)
+    assert ok, f"union vs per-head lists: {ratio_err:.3g} x allowance"
+
+
+def test_label_union_attention_forced_on_at_high_sparsity(sd):
+    # Debug flag 8 forces the union where the cost rule would not: most
+    # position chunks then hold few kept positions, many none at all.
+    inp, ch, lab = make("w4", seed=8, Hq=32, Hkv=8, seq_lens=[30000, 1, 17, 20000], N=30000)
+    out, idx, _ = _with_debug(sd, 8, lambda: run(sd, inp, ch, lab))
+    check(inp, ch, lab, out, idx, "labels union forced, 50x")
