@@ -238,8 +238,9 @@ sd_status sparse_decode_label_score(const sd_tensor *q, const sd_kv *K, const sd
                                     const int32_t *seq_lens, const sd_sparsity *sparsity,
                                     sd_tensor *scores, void *stream);
 
-/* Bytes of device workspace sparse_decode_attention and sparse_decode_attend
- * need for these shapes (idx gives k_max). */
+/* Bytes of device workspace sparse_decode_attention,
+ * sparse_decode_label_attention and sparse_decode_attend need for these
+ * shapes (idx gives k_max): the largest of their layouts. */
 sd_status sparse_decode_workspace_size(const sd_tensor *q, const sd_kv *K,
                                        const sd_sparsity *sparsity, const sd_tensor *idx,
                                        size_t *bytes);

@@ -1183,12 +1183,11 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   if (s >= nsp) return;
   const int e0 = s * split;
   int n = (n_list - e0) < split ? (n_list - e0) : split;
-  const int32_t *irow = idx + (int64_t)row * p.k_max + e0;
 
   if constexpr (UNI) {
     // The chunk's positions that some head keeps, in order, with their head
-    // bits: each thread packs the G mask bytes of kU consecutive positions,
-    // then one block scan places the kept ones.
+    // bits: each thread packs the G mask bytes of kUnionPerThread consecutive
+    // positions, then one block scan places the kept ones.
     __shared__ int scan_tmp[kWaves];
     const uint8_t *gm = w.umask + ((int64_t)b * p.Hkv + g) * w.umask_stride + (int64_t)e0 * p.G;
     uint32_t bits[kUnionPerThread];
@@ -1245,6 +1244,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   } else {
     // Resolve every entry to its row offsets once (page-table reads in
     // parallel); skipped entries point at position 0 and get weight 0.
+    const int32_t *irow = idx + (int64_t)row * p.k_max + e0;
     for (int t = tid; t < n; t += kBlock) {
       int32_t j = irow[t];
       if (j < 0 || j >= L) j = -1;
