@@ -356,3 +356,61 @@ def label_attention(inp, labels: np.ndarray, channels: np.ndarray, k_max: int | 
 
 def default_scale(d: int) -> float:
     return 1.0 / math.sqrt(d)
+
+
+# ---------------------------------------------------------------------------
+# Stochastic index selection with importance weights (the paper's vAttention
+# runs, Section 4 and the RULER-HARD figure).  The paper names the method
+# but does not define it; this is the reading built here: the exact top-k
+# set S of a row (with its forced positions), plus s positions drawn
+# uniformly, with replacement, from the rest C = [0, L) \ S, each drawn
+# entry weighted |C| / s, so that the weighted sums over the draws estimate
+# the sums over C without bias; the attention is the self-normalised
+# weighted softmax over S and the draws.  The random numbers are inputs:
+# draw i of a row is a uint32 u, and it picks the floor(u |C| / 2^32)-th
+# position of C in ascending order.
+# ---------------------------------------------------------------------------
+def complement_position(kept: np.ndarray, L: int, rank: int) -> int:
+    """The rank-th (0-based) position of [0, L) outside the ascending set
+    ``kept``: by enumeration."""
+    rest = np.setdiff1d(np.arange(L, dtype=np.int64), np.asarray(kept, dtype=np.int64))
+    return int(rest[rank])
+
+
+def sampled_lists(idx: np.ndarray, seq_lens, draws: np.ndarray):
+    """Index lists and weights of the sampled selection, from the exact
+    selection's lists idx [B, R, k_max] (ascending, -1 padded) and the draws
+    [B, R, s] (uint32): per row its kept positions (weight 1), then its s
+    drawn positions (weight |C| / s, float32), then -1 (weight 0).  Rows
+    whose kept set is the whole sequence draw nothing."""
+    B, R, k_max = idx.shape
+    s = draws.shape[2]
+    out_idx = np.full((B, R, k_max + s), -1, dtype=np.int32)
+    out_w = np.zeros((B, R, k_max + s), dtype=np.float32)
+    for b in range(B):
+        L = int(seq_lens[b])
+        for r in range(R):
+            kept = idx[b, r][idx[b, r] >= 0]
+            n = len(kept)
+            out_idx[b, r, :n] = kept
+            out_w[b, r, :n] = 1.0
+            c = L - n
+            if c <= 0 or s == 0:
+                continue
+            rest = np.setdiff1d(np.arange(L, dtype=np.int64), kept.astype(np.int64))
+            ranks = (draws[b, r].astype(np.uint64) * np.uint64(c)) >> np.uint64(32)
+            out_idx[b, r, n:n + s] = rest[ranks.astype(np.int64)]
+            out_w[b, r, n:n + s] = np.float32(c) / np.float32(s)
+    return out_idx, out_w
+
+
+def sampled_attention(inp, draws: np.ndarray, k_max: int | None = None, k_override=None,
+                      scale: float = 0.0, nthreads: int = 0) -> dict:
+    """The sampled selection's attention: exact top-k (sparse_attention's
+    selection), the draws of the rest, weighted softmax.  Returns dict(idx,
+    weights, out, absw, topk_idx)."""
+    base = sparse_attention(inp, k_max=k_max, k_override=k_override, scale=scale,
+                            nthreads=nthreads)
+    idx, w = sampled_lists(base["idx"], inp.seq_lens, np.asarray(draws, dtype=np.uint32))
+    out, absw = attend_weighted(inp, idx, w, scale=scale, nthreads=nthreads)
+    return {"idx": idx, "weights": w, "out": out, "absw": absw, "topk_idx": base["idx"]}

@@ -18,6 +18,7 @@ import pytest
 import torch
 
 from oracle import oracle as O
+from paper_2605_24168_amd import synth
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
 
@@ -634,3 +635,69 @@ def test_stage_functions_compose_to_the_fused_oracle():
                 assert tau == fused["tau"][b, r]
         out, _ = O.attend(p, fused["idx"])
         np.testing.assert_array_equal(out, fused["out"])
+
+
+# ---------------------------------------------------------------------------
+# Sampled selection (the stochastic index selection reading): pinned to dense
+# attention, which the oracle computes separately over every position.
+# ---------------------------------------------------------------------------
+
+def _enumerating_draws(c: int, rows: int) -> np.ndarray:
+    """Draws whose ranks are 0, 1, ..., c-1: draw i = ceil(i 2^32 / c)."""
+    i = np.arange(c, dtype=np.uint64)
+    d = ((i << np.uint64(32)) + np.uint64(c - 1)) // np.uint64(c)
+    return np.broadcast_to(d.astype(np.uint32), (1, rows, c)).copy()
+
+
+def test_sampled_selection_enumerating_the_rest_is_dense_attention():
+    # s = |C| draws of ranks 0..|C|-1 list every position outside the top-k
+    # once, with weight |C| / s = 1: the attention is dense attention.
+    inp = synth.make_inputs(2, seed=3, B=1, N=2000, Hq=8, Hkv=2)
+    k = O.budget(2000, inp.ratio, inp.rounding)
+    r = O.sampled_attention(inp, _enumerating_draws(2000 - k, inp.rows))
+    for row in range(inp.rows):
+        got = np.sort(r["idx"][0, row][r["idx"][0, row] >= 0])
+        np.testing.assert_array_equal(got, np.arange(2000))
+    assert (r["weights"][0][r["idx"][0] >= 0] == 1.0).all()
+    dense = O.dense_attention(inp)
+    np.testing.assert_allclose(r["out"], dense, rtol=0, atol=1e-12)
+
+
+def test_sampled_selection_enumerating_the_rest_twice_is_dense_attention():
+    # s = 2 |C| draws listing every position outside the top-k twice, each
+    # with weight |C| / s = 1/2: again exactly dense attention (a weight of 1,
+    # or s / |C|, would count the rest twice or four times).
+    inp = synth.make_inputs(2, seed=7, B=1, N=900, Hq=4, Hkv=1, ratio=10.0)
+    c = 900 - O.budget(900, inp.ratio, inp.rounding)
+    d = _enumerating_draws(c, inp.rows)
+    r = O.sampled_attention(inp, np.concatenate([d, d], axis=2), scale=1.0)
+    assert (r["weights"][0][:, -2 * c:] == np.float32(0.5)).all()
+    np.testing.assert_allclose(r["out"], O.dense_attention(inp, scale=1.0), rtol=0, atol=1e-12)
+
+
+def test_sampled_selection_converges_to_dense_attention():
+    # Many random draws with weight |C| / s: the weighted sums over the draws
+    # estimate the sums over the rest without bias, so the output nears dense
+    # attention, while the top-k part alone stays far from it (softmax scale
+    # 1, so the attention is peaked enough to tell weights apart: with a
+    # weight of 1 or s / |C| the error is as large as the top-k part's).
+    inp = synth.make_inputs(2, seed=4, B=1, N=1500, Hq=4, Hkv=1, ratio=20.0)
+    rng = np.random.default_rng(5)
+    draws = rng.integers(0, 2**32, size=(1, inp.rows, 60000), dtype=np.uint64).astype(np.uint32)
+    r = O.sampled_attention(inp, draws, scale=1.0)
+    dense = O.dense_attention(inp, scale=1.0)
+    topk_only = O.sparse_attention(inp, scale=1.0)["out"]
+    err_s = np.abs(r["out"] - dense).max()
+    err_k = np.abs(topk_only - dense).max()
+    assert err_s < 0.05 * err_k, (err_s, err_k)
+
+
+def test_sampled_selection_zero_draws_pick_the_first_position_outside_the_set():
+    inp = synth.make_inputs(2, seed=6, B=1, N=700, Hq=4, Hkv=1, ratio=10.0)
+    r = O.sampled_attention(inp, np.zeros((1, inp.rows, 5), np.uint32))
+    for row in range(inp.rows):
+        kept = r["topk_idx"][0, row][r["topk_idx"][0, row] >= 0]
+        first = min(set(range(700)) - set(kept.tolist()))
+        n = len(kept)
+        assert (r["idx"][0, row, n:n + 5] == first).all()
+        assert r["weights"][0, row, n] == np.float32(700 - n) / np.float32(5)
