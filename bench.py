@@ -43,7 +43,7 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def path_bytes(inp, ks, labels=False):
+def path_bytes(inp, ks, labels=False, samples=0):
     """Algorithmic HBM bytes of one step: every key (or, with the label
     indexer, every 16-byte label row) once, the kept value rows, q, out and
     idx.  (Per-head mode gathers one value row per query head and kept
@@ -56,10 +56,10 @@ def path_bytes(inp, ks, labels=False):
     if inp.group_shared:
         gather = sum(int(k) for k in ks) * inp.Hkv * 2 * row
     else:
-        recompute = labels or inp.n_sink + inp.n_local > 0
+        recompute = labels or inp.n_sink + inp.n_local > 0 or samples > 0
         per_entry = 2 * row if recompute else row
-        gather = sum(int(k) for k in ks) * inp.Hq * per_entry
-    k_max = max(int(k) for k in ks)
+        gather = sum(int(k) + samples for k in ks) * inp.Hq * per_entry
+    k_max = max(int(k) for k in ks) + samples
     small = 2 * inp.B * inp.Hq * row + inp.B * inp.rows * k_max * 4
     return key_stream, gather, small
 
@@ -131,7 +131,7 @@ def counters_traffic():
     return c.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(inp, n_seq, k_max, fixed_k=None, labels=None, min_s=10.0):
+def cpu_baseline(inp, n_seq, k_max, fixed_k=None, labels=None, min_s=10.0, draws=None):
     import dataclasses
     from oracle import oracle as O
     bs = list(range(min(n_seq, inp.B)))
@@ -151,7 +151,9 @@ def cpu_baseline(inp, n_seq, k_max, fixed_k=None, labels=None, min_s=10.0):
     ko = None if fixed_k is None else np.full(len(bs), fixed_k, np.int32)
 
     def once():
-        if labels is None:
+        if draws is not None:
+            O.sampled_attention(sub, draws[bs], k_max=k_max, k_override=ko, nthreads=threads)
+        elif labels is None:
             O.sparse_attention(sub, k_max=k_max, k_override=ko, nthreads=threads)
         else:  # (label cache in the key cache's layout, channels)
             lab, ch = labels
@@ -427,6 +429,9 @@ def main():
                     help="sparsity S (top-k budget round(L/S)) instead of the workload's")
     ap.add_argument("--fixed-k", type=int, default=None,
                     help="top-k budget K for every sequence instead of the ratio rule")
+    ap.add_argument("--samples", type=int, default=0,
+                    help="stochastic index selection: this many importance-weighted uniform "
+                         "draws of the rest of each row beside its exact top-k")
     ap.add_argument("--labels", action="store_true",
                     help="select with the 8-channel label indexer (bf16 workloads) instead of "
                          "exact scores")
@@ -451,6 +456,7 @@ def main():
         indexer_table(args)
         return
 
+    import numpy as np
     import torch
     from oracle import oracle as O
     from paper_2605_24168_amd import sparse_decode as sd
@@ -478,7 +484,15 @@ def main():
         ks.append(ns + nl + min(kh, L - ns - nl))
     k_max = O.k_max_for(inp) if args.fixed_k is None else max(ks)
     out = torch.empty_like(q)
-    idx = torch.empty((inp.B, inp.rows, k_max), dtype=torch.int32, device="cuda")
+    idx = torch.empty((inp.B, inp.rows, k_max + args.samples), dtype=torch.int32, device="cuda")
+    draws = wts = None
+    if args.samples > 0:
+        if args.labels:
+            raise SystemExit("--samples and --labels do not combine")
+        g = torch.Generator(device="cuda").manual_seed(args.seed)
+        draws = torch.randint(-2**31, 2**31 - 1, (inp.B, inp.rows, args.samples),
+                              dtype=torch.int32, device="cuda", generator=g)
+        wts = torch.empty(idx.shape, dtype=torch.float32, device="cuda")
     ws = torch.empty(sd.workspace_size(q, cache, sp, idx), dtype=torch.uint8, device="cuda")
     sd.set_workspace(ws)
     labels = host_labels = None
@@ -491,7 +505,10 @@ def main():
     torch.cuda.synchronize()
 
     def one_step():
-        if labels is None:
+        if draws is not None:
+            sd.sparse_decode_sampled_attention(q, cache, lens, sp, draws, out=out, idx=idx,
+                                               weights=wts)
+        elif labels is None:
             sd.sparse_decode_attention(q, cache, lens, sp, out=out, idx=idx)
         else:
             sd.sparse_decode_label_attention(q, cache, labels, lens, sp, out=out, idx=idx)
@@ -562,7 +579,7 @@ def main():
                  "frac_of_peak": dense_b / (dense_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                  "sparse_speedup": dense_ms / ms_step}
 
-    key_b, gather_b, small_b = path_bytes(inp, ks, labels=args.labels)
+    key_b, gather_b, small_b = path_bytes(inp, ks, labels=args.labels, samples=args.samples)
     total_b = key_b + gather_b + small_b
     path_gbps = total_b / (ms_step * 1e-3) / 1e9
     q_bytes = inp.B * inp.Hq * inp.d * (2 if inp.dtype == "bf16" else 4)
@@ -593,7 +610,8 @@ def main():
                    **({"n_sink": inp.n_sink, "n_local": inp.n_local}
                       if inp.n_sink or inp.n_local else {}),
                    **({"fixed_k": args.fixed_k} if args.fixed_k is not None else {}),
-                   **({"indexer": "8-channel bf16 labels"} if args.labels else {})},
+                   **({"indexer": "8-channel bf16 labels"} if args.labels else {}),
+                   **({"samples": args.samples} if args.samples else {})},
         "roofline": {
             "bound": "hbm",
             "kernel": "k_score_stream" + (" (label rows)" if args.labels else ""),
@@ -640,8 +658,9 @@ def main():
         del src, dst
     if args.cpu_sample > 0:
         log(f"timing the CPU oracle on {args.cpu_sample} sequences")
-        rec["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample, k_max, args.fixed_k,
-                                           host_labels)
+        rec["cpu_baseline"] = cpu_baseline(
+            inp, args.cpu_sample, k_max, args.fixed_k, host_labels,
+            draws=None if draws is None else draws.cpu().numpy().view(np.uint32))
     else:
         rec["cpu_baseline"] = None
     print(json.dumps(rec), flush=True)

@@ -238,6 +238,28 @@ sd_status sparse_decode_label_score(const sd_tensor *q, const sd_kv *K, const sd
                                     const int32_t *seq_lens, const sd_sparsity *sparsity,
                                     sd_tensor *scores, void *stream);
 
+/* Stochastic index selection with importance weights (the vAttention runs
+ * of Section 4; the paper does not define the method, and this is the
+ * standard importance-weighted reading): per query head (row), the exact
+ * top-k set S of sparse_decode_attention (with any forced positions), plus
+ * s positions drawn uniformly with replacement from the rest
+ * C = [0, L_b) \ S, each drawn entry weighted |C| / s; out is the weighted
+ * softmax attention over S and the draws (as sparse_decode_attend_weighted).
+ *   draws    int32 [B, R, s]: the random numbers, one per draw, read as
+ *            uint32 bits u; draw i picks the floor(u |C| / 2^32)-th position
+ *            of C in ascending order.
+ *   idx      int32 [B, R, k_max + s], written: S ascending, then the s drawn
+ *            positions, then -1; k_max >= the k of a full-capacity sequence
+ *            (plus the forced positions), as for sparse_decode_attention.
+ *   weights  float32 [B, R, k_max + s], written: 1 for S, |C| / s for a
+ *            draw, 0 for padding.  A row with |C| = 0 draws nothing.
+ * Per-head rows only (group_shared returns SD_ERR_UNSUPPORTED).  Uses the
+ * same workspace as sparse_decode_attention for this idx. */
+sd_status sparse_decode_sampled_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                          const int32_t *seq_lens, const sd_sparsity *sparsity,
+                                          const sd_tensor *draws, sd_tensor *out, sd_tensor *idx,
+                                          sd_tensor *weights, void *stream);
+
 /* Bytes of device workspace sparse_decode_attention,
  * sparse_decode_label_attention and sparse_decode_attend need for these
  * shapes (idx gives k_max): the largest of their layouts. */

@@ -253,7 +253,7 @@ bool union_pays(const Shape &s, int64_t k_max) {
 }
 
 Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp,
-                  bool labels = false) {
+                  bool labels = false, bool allow_union = true) {
   Layout L{};
   const int group_shared = sp->group_shared ? 1 : 0;
   const int64_t rows = (int64_t)s.B * s.R;
@@ -276,7 +276,7 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
   shape_only.n_sink = sp->n_sink;
   shape_only.n_local = sp->n_local;
   L.nsplit = sd::attend_nsplit(shape_only);
-  const bool uni_ok = fused && union_eligible(s, sp, labels);
+  const bool uni_ok = fused && allow_union && union_eligible(s, sp, labels);
   if (uni_ok && union_pays(s, k_max)) {
     L.union_chunk = sd::union_chunk(shape_only);
     const int un = (int)((s.ncap + L.union_chunk - 1) / L.union_chunk);
@@ -601,9 +601,18 @@ namespace {
 
 // The fused call, with exact scores (labels null) or the low-channel
 // indexer's label scores choosing the positions.
+// The sampled selection's extra inputs and outputs (see
+// sparse_decode_sampled_attention); null for the plain fused call.
+struct Sampled {
+  const uint32_t *draws;  // [B, R, n] device
+  int n;
+  float *weights;         // [B, R, k_max + n] device
+};
+
 sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
                          const sd_labels *labels, const int32_t *seq_lens,
-                         const sd_sparsity *sp, sd_tensor *out, sd_tensor *idx, void *stream) {
+                         const sd_sparsity *sp, sd_tensor *out, sd_tensor *idx, void *stream,
+                         const Sampled *smp = nullptr) {
   Shape s{};
   sd_status st = check_problem(q, K, V, sp, s);
   if (st) return st;
@@ -612,16 +621,22 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
     st = check_labels(labels, K, s);
     if (st) return st;
   }
-  int64_t k_max = 0;
-  st = check_idx(idx, s, sp, k_max);
+  int64_t k_max = 0;  // the selection's list capacity
+  int64_t k_list = 0;  // the index list's row length (k_max + draws)
+  st = check_idx(idx, s, sp, k_list);
   if (st) return st;
+  k_max = k_list - (smp ? smp->n : 0);
+  if (k_max < 0 || (!sp->k_override && k_max < list_budget(s.ncap, sp)))
+    return SD_ERR_INVALID_ARG;
   st = check_out(out, s, q->dtype);
   if (st) return st;
   if (s.B == 0) return SD_OK;
   if (!seq_lens) return SD_ERR_INVALID_ARG;
   const hipStream_t stream_h = (hipStream_t)stream;
   std::lock_guard<std::mutex> lk(g_mu);
-  const Layout L = layout_for(s, k_max, true, sp, labels != nullptr);
+  // (the sampled call's unfused weighted attention needs partials for the
+  // whole list, and no union attention)
+  const Layout L = layout_for(s, smp ? k_list : k_max, true, sp, labels != nullptr, !smp);
   // One scoring workgroup per (chunk, sequence, KV head) on a 1-D grid.
   if ((int64_t)L.nchunk * s.B * s.Hkv > INT32_MAX) return SD_ERR_UNSUPPORTED;
   DevState *ds = nullptr;
@@ -636,6 +651,7 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
     p.labels = (const uint16_t *)labels->t.data;
     p.channels = labels->channels;
   }
+  if (smp) p.idx_stride = (int32_t)k_list;
   int32_t *idx_ptr = (int32_t *)idx->data;
 
   const int prof_level = g_profiling.load();
@@ -678,8 +694,19 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   if (e == hipSuccess && s.ncap > 0) e = sd::launch_repair(p, w, stream_h);
   if (e == hipSuccess) e = mark(3);
   if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, wide, stream_h);
+  if (e == hipSuccess && smp)
+    e = sd::launch_sample_rest(p, idx_ptr, smp->draws, smp->n, smp->weights, stream_h);
   if (e == hipSuccess) e = mark(4);
-  if (e == hipSuccess) e = sd::launch_attend(p, w, idx_ptr, out->data, true, stream_h);
+  if (e == hipSuccess && !smp) e = sd::launch_attend(p, w, idx_ptr, out->data, true, stream_h);
+  if (e == hipSuccess && smp) {
+    // Weighted attention over the kept entries and the draws, logits
+    // recomputed from the key rows.
+    sd::Params pa = p;
+    pa.k_max = (int32_t)k_list;
+    pa.idx_stride = 0;
+    pa.weights = smp->weights;
+    e = sd::launch_attend(pa, w, idx_ptr, out->data, false, stream_h);
+  }
   if (e == hipSuccess) e = mark(5);
   if (prof && e == hipSuccess) {
     ds->level[ds->n_calls % kRing] = prof_level;
@@ -705,6 +732,26 @@ sd_status sparse_decode_label_attention(const sd_tensor *q, const sd_kv *K, cons
                                         void *stream) {
   if (!labels) return SD_ERR_INVALID_ARG;
   return attention_impl(q, K, V, labels, seq_lens, sp, out, idx, stream);
+}
+
+sd_status sparse_decode_sampled_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                          const int32_t *seq_lens, const sd_sparsity *sparsity,
+                                          const sd_tensor *draws, sd_tensor *out, sd_tensor *idx,
+                                          sd_tensor *weights, void *stream) {
+  if (!q || !draws || !idx || !weights) return SD_ERR_INVALID_ARG;
+  if (draws->ndim != 3 || draws->dtype != SD_I32 || idx->ndim != 3 || weights->ndim != 3 ||
+      weights->dtype != SD_F32)
+    return SD_ERR_INVALID_ARG;
+  const int64_t n = draws->shape[2];
+  if (n < 0 || n > INT32_MAX / 4 || (n > 0 && !draws->data)) return SD_ERR_INVALID_ARG;
+  for (int i = 0; i < 2; ++i)
+    if (draws->shape[i] != idx->shape[i]) return SD_ERR_INVALID_ARG;
+  for (int i = 0; i < 3; ++i)
+    if (weights->shape[i] != idx->shape[i]) return SD_ERR_INVALID_ARG;
+  if (idx->shape[2] > 0 && !weights->data) return SD_ERR_INVALID_ARG;
+  if (sparsity && sparsity->group_shared) return SD_ERR_UNSUPPORTED;  // per-head rows only
+  const Sampled smp{(const uint32_t *)draws->data, (int)n, (float *)weights->data};
+  return attention_impl(q, K, V, nullptr, seq_lens, sparsity, out, idx, stream, &smp);
 }
 
 sd_status sparse_decode_label_score(const sd_tensor *q, const sd_kv *K, const sd_labels *labels,

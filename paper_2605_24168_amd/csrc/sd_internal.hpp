@@ -68,6 +68,9 @@ struct Params {
   // channel channels[g * kLabels + c].
   const uint16_t *labels;
   const int32_t *channels;     // [Hkv][kLabels]
+  // Row stride of the index list the selection writes, when it is longer
+  // than k_max (the sampled selection appends its draws); 0: k_max.
+  int32_t idx_stride;
 };
 
 // Scratch carved from the library workspace (see the host orchestration).

@@ -965,7 +965,8 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
   const bool forced = rp.ns + rp.nl > 0;
   const bool weights = MODE != 1 && !p.group_shared && !forced;
   const int k = rp.kh;
-  int32_t *lrow = idx + (int64_t)row * p.k_max;
+  const int64_t ist = p.idx_stride > 0 ? p.idx_stride : p.k_max;  // list row stride
+  int32_t *lrow = idx + (int64_t)row * ist;
   float *lvals = vals ? vals + (int64_t)row * p.k_max : nullptr;
   int32_t *irow = lrow + rp.ns;
   float *vrow = lvals ? lvals + rp.ns : nullptr;
@@ -1027,16 +1028,57 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
     lrow[slot] = pos;
     if (lvals) lvals[slot] = MODE == 1 ? dense[(int64_t)row * ld + pos] : 0.f;
   }
-  for (int i = rp.total + tid; i < p.k_max; i += NT) {
-    lrow[i] = -1;
-    if (lvals) lvals[i] = -__builtin_inff();
-  }
+  for (int i = rp.total + tid; i < ist; i += NT) lrow[i] = -1;
+  if (lvals)
+    for (int i = rp.total + tid; i < p.k_max; i += NT) lvals[i] = -__builtin_inff();
   if (MODE == 0 && w.umask) {
     // Union attention: mark this head's kept positions in its group's mask.
     __syncthreads();  // the list was written by every thread of the block
     const int rr = row % p.R;
     uint8_t *gm = w.umask + ((int64_t)b * p.Hkv + rr / p.G) * w.umask_stride + rr % p.G;
     for (int i = tid; i < rp.total; i += NT) gm[(int64_t)lrow[i] * p.G] = 1;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Sampled selection: after the exact selection has written each row's kept
+// list S (ascending, total = |S| entries, row stride p.idx_stride), append
+// the row's s draws from the rest C = [0, L) \ S and write every entry's
+// weight: 1 for S, |C| / s for a draw (float32), 0 for the padding.  Draw i
+// (a uint32 u) is the floor(u |C| / 2^32)-th position of C in ascending
+// order: the rank rho plus the number of kept positions at or below the
+// result, which is #{t : S[t] - t <= rho} (S[t] - t is non-decreasing), found
+// by binary search.  grid = B*R rows.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlock) void k_sample_rest(Params p, int32_t *list,
+                                                        const uint32_t *draws, int s,
+                                                        float *weights) {
+  const int row = blockIdx.x, b = row / p.R;
+  const int L = seq_len(p, b);
+  const RowPlan rp = row_plan(p, b, L);
+  const int64_t ist = p.idx_stride;  // = k_max + s
+  int32_t *lrow = list + (int64_t)row * ist;
+  float *wrow = weights + (int64_t)row * ist;
+  const uint32_t *drow = draws + (int64_t)row * s;
+  const int total = rp.total;
+  const int64_t c = (int64_t)L - total;  // positions outside the kept set
+  const float wd = c > 0 && s > 0 ? (float)c / (float)s : 0.f;
+  for (int t = threadIdx.x; t < ist; t += kBlock) {
+    if (t < total) {
+      wrow[t] = 1.f;
+    } else if (t < total + s && c > 0) {
+      const uint64_t rho = ((uint64_t)drow[t - total] * (uint64_t)c) >> 32;  // < c
+      int lo = 0, hi = total;  // count of t' with S[t'] - t' <= rho, in [0, total]
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if ((int64_t)lrow[mid] - mid <= (int64_t)rho) lo = mid + 1;
+        else hi = mid;
+      }
+      lrow[t] = (int32_t)((int64_t)rho + lo);
+      wrow[t] = wd;
+    } else {
+      wrow[t] = 0.f;  // padding (the selection wrote -1)
+    }
   }
 }
 
@@ -1620,6 +1662,13 @@ int attend_nsplit(const Params &p) {
     most = ns > most ? ns : most;
   }
   return most;
+}
+
+hipError_t launch_sample_rest(const Params &p, int32_t *list, const uint32_t *draws, int s,
+                              float *weights, hipStream_t st) {
+  if (p.idx_stride != p.k_max + s) return hipErrorInvalidValue;
+  k_sample_rest<<<p.B * p.R, kBlock, 0, st>>>(p, list, draws, s, weights);
+  return hipGetLastError();
 }
 
 int union_chunk(const Params &p) {

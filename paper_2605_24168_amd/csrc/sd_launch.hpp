@@ -30,6 +30,10 @@ hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st);
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st);
 int attend_nsplit(const Params &p);
+// The sampled selection's draws and weights after the exact selection wrote
+// the kept lists (p: the selection's parameters, idx_stride = k_max + s).
+hipError_t launch_sample_rest(const Params &p, int32_t *list, const uint32_t *draws, int s,
+                              float *weights, hipStream_t st);
 // Positions per workgroup of the group-deduplicated attention (fits the LDS).
 int union_chunk(const Params &p);
 hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st);

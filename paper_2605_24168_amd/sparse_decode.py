@@ -111,6 +111,10 @@ lib.sparse_decode_profile_mean.restype = C.c_int
 lib.sparse_decode_profile_mean.argtypes = [_P(SdProfile), _P(C.c_int32)]
 lib.sparse_decode_set_debug.restype = C.c_int
 lib.sparse_decode_set_debug.argtypes = [C.c_int32]
+lib.sparse_decode_sampled_attention.restype = C.c_int
+lib.sparse_decode_sampled_attention.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p,
+                                                _P(SdSparsity), _P(SdTensor), _P(SdTensor),
+                                                _P(SdTensor), _P(SdTensor), C.c_void_p]
 lib.sparse_decode_read_probe.restype = C.c_int
 lib.sparse_decode_read_probe.argtypes = [C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p]
 lib.sparse_decode_status_string.restype = C.c_char_p
@@ -438,6 +442,35 @@ def profile_mean() -> dict:
     d = {f: getattr(p, f) for f, _ in SdProfile._fields_}
     d["calls"] = int(n.value)
     return d
+
+
+def sparse_decode_sampled_attention(q, cache: KVCache, seq_lens, sparsity: Sparsity, draws,
+                                    out=None, idx=None, weights=None, k_max: Optional[int] = None,
+                                    stream=None):
+    """Exact top-k plus s importance-weighted uniform draws of the rest of
+    each row (draws: int32 [B, R, s], read as uint32 bits).  Returns (out,
+    idx [B, R, k_max + s], weights, same shape)."""
+    _need_device(seq_lens, "seq_lens", torch.int32)
+    _need_device(draws, "draws", torch.int32)
+    s = int(draws.shape[2])
+    if idx is None:
+        km = k_max_of(cache, sparsity) if k_max is None else k_max
+        idx = torch.empty((q.shape[0], rows_of(q, cache, sparsity), km + s), dtype=torch.int32,
+                          device=q.device)
+    if weights is None:
+        weights = torch.empty(idx.shape, dtype=torch.float32, device=q.device)
+    if out is None:
+        out = torch.empty_like(q)
+    sp = sparsity.c()
+    cq, kk, kv = _tensor(q, "q"), cache.c("k"), cache.c("v")
+    cd, co, ci, cw = _tensor(draws, "draws"), _tensor(out, "out"), _tensor(idx, "idx"), \
+        _tensor(weights, "weights")
+    _check(lib.sparse_decode_sampled_attention(C.byref(cq), C.byref(kk), C.byref(kv),
+                                               seq_lens.data_ptr(), C.byref(sp), C.byref(cd),
+                                               C.byref(co), C.byref(ci), C.byref(cw),
+                                               _stream(stream)),
+           "sparse_decode_sampled_attention")
+    return out, idx, weights
 
 
 def read_probe(buf: torch.Tensor, sink: torch.Tensor, stream=None) -> None:

@@ -309,3 +309,35 @@ def test_read_probe_checks_its_buffer_on_the_host(sd):
     assert probe(FAKE, 0, sink, None) == -1             # empty
     assert probe(FAKE, 1024, None, None) == -1          # no sink
     assert probe(FAKE, 1024, FAKE + 2, None) == -1      # misaligned sink
+
+
+@pytest.mark.parametrize("defect,code", [
+    ("draws_null", -1), ("draws_dtype", -1), ("draws_rows", -1), ("weights_shape", -1),
+    ("weights_dtype", -1), ("idx_short_of_draws", -1), ("group_shared", -2),
+])
+def test_sampled_attention_rejects_invalid_arguments(sd, defect, code):
+    q, K, V, lens, sp, out, idx = valid_parts(sd)
+    s = 16
+    idx.shape[2] = 205 + s
+    draws = tensor(sd, (2, 32, s), sd.SD_I32)
+    w = tensor(sd, (2, 32, 205 + s), sd.SD_F32)
+    if defect == "draws_null":
+        draws = None
+    elif defect == "draws_dtype":
+        draws.dtype = sd.SD_F32
+    elif defect == "draws_rows":
+        draws.shape[1] = 31
+    elif defect == "weights_shape":
+        w.shape[2] = 205
+    elif defect == "weights_dtype":
+        w.dtype = sd.SD_BF16
+    elif defect == "idx_short_of_draws":
+        idx.shape[2] = 205 + s - 1   # the top-k part must still hold 205
+    elif defect == "group_shared":
+        sp.group_shared = 1
+        idx.shape[1] = draws.shape[1] = w.shape[1] = 8
+    rc = sd.lib.sparse_decode_sampled_attention(
+        C.byref(q), C.byref(K), C.byref(V), lens, C.byref(sp),
+        C.byref(draws) if draws is not None else None, C.byref(out), C.byref(idx), C.byref(w),
+        None)
+    assert rc == code
