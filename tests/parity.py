@@ -121,3 +121,15 @@ def to_host(t) -> np.ndarray:
 
 def fmt_s(x: float) -> str:
     return "nan" if math.isnan(x) else f"{x:.3g}"
+
+
+def slice_batch(inp, bs):
+    """Sequences bs of a decode step as a smaller step (views of the cache;
+    a paged step keeps its page pool and slices its block table)."""
+    import dataclasses
+    bs = list(bs)
+    if inp.layout == "paged":
+        return dataclasses.replace(inp, B=len(bs), q=inp.q[bs], seq_lens=inp.seq_lens[bs],
+                                   block_table=inp.block_table[bs])
+    return dataclasses.replace(inp, B=len(bs), q=inp.q[bs], k=inp.k[bs], v=inp.v[bs],
+                               seq_lens=inp.seq_lens[bs])

@@ -218,3 +218,20 @@ def test_label_union_attention_forced_on_at_high_sparsity(sd):
     inp, ch, lab = make("w4", seed=8, Hq=32, Hkv=8, seq_lens=[30000, 1, 17, 20000], N=30000)
     out, idx, _ = _with_debug(sd, 8, lambda: run(sd, inp, ch, lab))
     check(inp, ch, lab, out, idx, "labels union forced, 50x")
+
+
+@pytest.mark.parametrize("cfg,ratio,sample", [(3, None, [0, 15]), (4, 3.0, [3, 17])])
+def test_label_indexer_full_size_on_sampled_sequences(sd, cfg, ratio, sample):
+    # Workload 3 with labels (the bench's --labels line: per-head lists), and
+    # workload 4 (paged, ragged, 4 heads per group) at 3x, where the cost
+    # rule picks the group-deduplicated attention; the oracle checks two
+    # sequences of each.
+    P.log(f"  generating workload {cfg} at full size")
+    inp = synth.make_inputs(cfg, seed=0, **({"ratio": ratio} if ratio else {}))
+    ch = synth.label_channels(inp.Hkv, seed=0)
+    lab = synth.label_cache(inp, ch)
+    _INP["last"] = inp  # the device label layout follows this step's page table
+    out, idx, _ = run(sd, inp, ch, lab)
+    sub = P.slice_batch(inp, sample)
+    sub_lab = lab if inp.layout == "paged" else lab[sample]
+    check(sub, ch, sub_lab, out[sample], idx[sample], f"labels full workload {cfg}")

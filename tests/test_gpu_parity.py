@@ -427,13 +427,7 @@ def test_invalid_arguments_are_rejected_before_launch(sd):
 # Full-size workloads, as the benchmark runs them, on sampled sequences.
 # ---------------------------------------------------------------------------
 
-def slice_batch(inp, bs):
-    bs = list(bs)
-    if inp.layout == "paged":
-        return dataclasses.replace(inp, B=len(bs), q=inp.q[bs], seq_lens=inp.seq_lens[bs],
-                                   block_table=inp.block_table[bs])
-    return dataclasses.replace(inp, B=len(bs), q=inp.q[bs], k=inp.k[bs], v=inp.v[bs],
-                               seq_lens=inp.seq_lens[bs])
+slice_batch = P.slice_batch
 
 
 @pytest.mark.parametrize("cfg,sample", [(1, [0]), (2, [1]), (3, [0, 15]), (4, [3, 17]), (5, [0])])

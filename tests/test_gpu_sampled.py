@@ -132,3 +132,15 @@ def test_sampled_without_draws_is_the_top_k_attention(sd):
     assert ((w == 1.0) == (idx >= 0)).all()
     ok, ratio, _ = P.out_errors(out, P.to_host(out2), inp.dtype)
     assert ok, f"{ratio:.3g} x allowance"
+
+
+def test_sampled_full_size_on_sampled_sequences(sd):
+    # Workload 3 at full size with the bench's first sampled line (top-k
+    # 1/200 plus 1311 draws per row), two sequences checked by the oracle.
+    P.log("  generating workload 3 at full size")
+    inp = synth.make_inputs(3, seed=0, ratio=200.0)
+    draws = random_draws(inp, 1311, seed=9)
+    out, idx, w = run(sd, inp, draws)
+    sample = [0, 15]
+    check(P.slice_batch(inp, sample), draws[sample], out[sample], idx[sample], w[sample],
+          "sampled full workload 3")
