@@ -237,10 +237,10 @@ bool union_eligible(const Shape &s, const sd_sparsity *sp, bool labels) {
 // (key + value, 512 B) against the expected union of G such sets of an
 // Ncap-position range drawn independently (heads that agree only shrink the
 // union), plus clearing, reading and marking the masks.  The group-row
-// kernel gathers at about 0.7 of the per-head kernel's rate (half the rows
-// in flight per wave, two waves per SIMD against four, measured at 128K),
-// so the union must move under 0.65 of the bytes.  Debug flags 4 / 8 force
-// it off / on.
+// kernel gathers at about 0.87 of the per-head kernel's rate for up to 4
+// heads (three waves per SIMD) and 0.7 for more (8 heads per pass: two
+// waves), measured at 128K, so the union must move under 0.83 or 0.65 of
+// the bytes.  Debug flags 4 / 8 force it off / on.
 bool union_pays(const Shape &s, int64_t k_max) {
   const int dbg = g_debug.load();
   if (dbg & 4) return false;
@@ -249,7 +249,7 @@ bool union_pays(const Shape &s, int64_t k_max) {
   const double kt = (double)(k_max < s.ncap ? k_max : s.ncap);
   const double per_head = G * kt * 512.0;
   const double uni = Lc * (1.0 - std::pow(1.0 - kt / Lc, G)) * 512.0 + 2.0 * G * Lc + G * kt;
-  return uni < 0.65 * per_head;
+  return uni < (s.G <= 4 ? 0.83 : 0.65) * per_head;
 }
 
 Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp,

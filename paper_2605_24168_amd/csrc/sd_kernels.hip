@@ -1181,8 +1181,10 @@ struct AttLds {
 // UNI (union attention, with FUSED and GRP): the workgroup of (chunk s,
 // group (b, g)) takes the positions [s*split, +split) that any head of the
 // group keeps (the group's head masks), in order, and serves every head,
-// each over its own positions only.
-template <bool BF16, bool FUSED, bool GRP, bool UNI = false>
+// each over its own positions only.  HBU: heads accumulated per pass over
+// the value rows in group mode (4 for groups of at most 4 heads: fewer
+// registers, three waves per SIMD instead of two).
+template <bool BF16, bool FUSED, bool GRP, bool UNI = false, int HBU = kAttHeads>
 __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32_t *idx, void *out,
                                                    int split) {
   static_assert(!UNI || (BF16 && FUSED && GRP), "union attention: fused bf16 group rows");
@@ -1190,7 +1192,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   __shared__ float mh[kMaxGroup];
   __shared__ float hmax[kWaves][kMaxGroup];
   constexpr int U = (BF16 && !GRP) ? 8 : 4;  // positions per 16-lane group per step
-  constexpr int HB = GRP ? kAttHeads : 1;  // heads accumulated per pass
+  constexpr int HB = GRP ? HBU : 1;  // heads accumulated per pass
 
   const int s = blockIdx.x, row = blockIdx.y;
   const int rows_per_b = UNI ? p.Hkv : p.R;  // union rows are the groups
@@ -1685,8 +1687,9 @@ hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, voi
     const int split = w.union_chunk;
     const size_t lds = (size_t)AttLds(split, p.G, true, true).total;
     const int nsplit = (int)((p.ncap + split - 1) / split);
-    k_attend<true, true, true, true><<<dim3(nsplit, p.B * p.Hkv), kBlock, lds, st>>>(p, w, idx, out,
-                                                                                      split);
+    const dim3 grid(nsplit, p.B * p.Hkv);
+    if (p.G <= 4) k_attend<true, true, true, true, 4><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
+    else k_attend<true, true, true, true><<<grid, kBlock, lds, st>>>(p, w, idx, out, split);
     if (nsplit > 1) k_merge<true, true><<<(unsigned)(p.B * p.Hq), kMergeThreads, 0, st>>>(p, w, out, split);
     return hipGetLastError();
   }
