@@ -210,8 +210,15 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
   if (sp->k_override) return sd::kWaveKeysMax;
   const int rows = group_shared ? 1 : s.G;
   const double area = (double)(sd::kCandBuf / rows);
+  // Candidates per key the pilot aims at (about f k of n keys, f between 1
+  // and 2.5: pilot_rank over a full-capacity sequence); a wave's expected
+  // candidates must fill at most half of a row's staging area.
+  double f = 2.5;
+  const int64_t n = s.ncap, m = n < sd::kSampleMax ? n : sd::kSampleMax;
+  const int64_t k = sd::budget_rule(n, sp->ratio, sp->k_rounding);
+  if (n > 0 && k > 0 && m < n) f = (double)sd::pilot_rank(k, m, n) * n / ((double)k * m);
   int wk = labels ? sd::kLabelWaveKeysMax : sd::kWaveKeysMax;
-  while (wk > 256 && 5.0 * wk / sp->ratio > area) wk /= 2;
+  while (wk > 256 && 2.0 * f * wk / sp->ratio > area) wk /= 2;
   if (labels)
     while (wk > sd::kWaveKeysMax && (int64_t)s.B * s.Hkv * ((s.ncap + wk - 1) / wk) < 2048) wk /= 2;
   return wk;

@@ -118,6 +118,20 @@ struct DenseWork {
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
 
+// Pilot threshold rank (see the pilot kernel): of m samples of n
+// positions, for a top-k of k, the smallest r with r - z sqrt(r) >= e,
+// e = k m / n, capped at ceil(2.5 e) (and at m).  z: the margin in
+// standard deviations of the count above the r-th sample.
+constexpr double kPilotZ = 4.3;
+__host__ __device__ inline int64_t pilot_rank(int64_t k, int64_t m, int64_t n) {
+  const int64_t rr = (5 * k * m + 2 * n - 1) / (2 * n);
+  const double e = (double)k * m / n;
+  const double sq = 0.5 * (kPilotZ + sqrt(kPilotZ * kPilotZ + 4.0 * e));
+  const int64_t rz = (int64_t)ceil(sq * sq);
+  const int64_t r = rz < rr ? rz : rr;
+  return r < m ? r : m;
+}
+
 // k for a sequence of L positions (Table 1 caption: 1/S of the tokens).
 __host__ __device__ inline int64_t budget_rule(int64_t L, double ratio, int rounding) {
   if (L <= 0) return 0;

@@ -141,7 +141,6 @@ __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
 // ---------------------------------------------------------------------------
 constexpr int kBuckets = 2048;
 constexpr int kPilotMinRank = 48;  // fewest sample ranks above the threshold
-constexpr double kPilotZ = 4.3;    // sample-rank margin, in standard deviations
 
 template <int NT = kBlock>
 struct BucketShared {
@@ -297,14 +296,8 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
     // About 2.5 k candidates where the expected sample rank of the k-th key,
     // e = k m / n, is small; where it is large the count above the r-th
     // sample varies by about sqrt(r) ranks only, so r need only clear e by
-    // kPilotZ of them: the smallest r with r - kPilotZ sqrt(r) >= e (at
-    // e of about 20 the two agree).
-    const int64_t rr = (5LL * k * m + 2LL * mid - 1) / (2LL * mid);
-    const double e = (double)k * m / mid;
-    const double sq = 0.5 * (kPilotZ + sqrt(kPilotZ * kPilotZ + 4.0 * e));
-    const int64_t rz = (int64_t)ceil(sq * sq);
-    r = (int)(rz < rr ? rz : rr);
-    r = r < m ? r : m;
+    // kPilotZ of them (pilot_rank; at e of about 20 the two agree).
+    r = (int)pilot_rank(k, m, mid);
     // A small rank leaves the candidate count a relative spread of about
     // 1/sqrt(r): with k of a few dozen, one row in five would come up short
     // of k.  Take at least kPilotMinRank (as far as the staging areas hold
