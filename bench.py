@@ -131,7 +131,8 @@ def counters_traffic():
     return c.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(inp, n_seq, k_max, fixed_k=None, labels=None, min_s=10.0, draws=None):
+def cpu_baseline(inp, n_seq, k_max, fixed_k=None, labels=None, min_s=10.0, draws=None,
+                 threads=None):
     import dataclasses
     from oracle import oracle as O
     bs = list(range(min(n_seq, inp.B)))
@@ -141,11 +142,12 @@ def cpu_baseline(inp, n_seq, k_max, fixed_k=None, labels=None, min_s=10.0, draws
     else:
         sub = dataclasses.replace(inp, B=len(bs), q=inp.q[bs], k=inp.k[bs], v=inp.v[bs],
                                   seq_lens=inp.seq_lens[bs])
-    try:
-        threads = len(os.sched_getaffinity(0))
-    except AttributeError:
-        threads = os.cpu_count() or 1
-    threads = max(1, min(threads, 16))
+    if threads is None:
+        try:
+            threads = len(os.sched_getaffinity(0))
+        except AttributeError:
+            threads = os.cpu_count() or 1
+        threads = max(1, min(threads, 16))
     used = O.max_threads(threads)
     import numpy as np
     ko = None if fixed_k is None else np.full(len(bs), fixed_k, np.int32)
@@ -407,6 +409,24 @@ def indexer_table(args):
     print(json.dumps(rec), flush=True)
 
 
+def oracle_table(args):
+    """The CPU oracle alone on workloads 1 and 2 (whole batches), on one core
+    and on every core it may use: one JSON line.  No GPU is touched."""
+    from oracle import oracle as O
+    from paper_2605_24168_amd import synth
+    rows = []
+    for cfg in (1, 2):
+        inp = synth.make_inputs(cfg, seed=args.seed)
+        for threads in (1, None):
+            r = cpu_baseline(inp, inp.B, O.k_max_for(inp), min_s=3.0, threads=threads)
+            r.update(workload=cfg, name=synth.NAMES[cfg],
+                     ms_per_call=1e3 * inp.B / r["value"])
+            log(f"oracle workload {cfg}, {r['cores']} core(s): {r['ms_per_call']:.1f} ms/call")
+            rows.append(r)
+    print(json.dumps({"table": "CPU oracle (score + select + attend, float64) per call",
+                      "rows": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -443,12 +463,18 @@ def main():
                     help="instead of the default line, sweep dense decode against the "
                          "weighted sparse backend in Table 1's shape (batch 1/4/8/16, "
                          "2x-500x, 128K, GQA 32/8, paged)")
+    ap.add_argument("--oracle-cores", action="store_true",
+                    help="instead of the default line, time the CPU oracle on workloads 1 and "
+                         "2 on one core and on all cores (no GPU)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU: the method's data-parallel shards (sequences or KV "
               "heads) need no exchange, so only --gpus 1 is supported", file=sys.stderr)
         sys.exit(2)
+    if args.oracle_cores:
+        oracle_table(args)
+        return
     if args.table1:
         backend_table(args)
         return

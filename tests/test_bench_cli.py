@@ -34,6 +34,8 @@ def test_cpu_baseline_repeats_the_oracle_sample_for_a_bounded_time():
     assert rec["kind"] == "oracle" and rec["unit"] == "queries/s"
     assert rec["value"] > 0 and rec["cores"] >= 1
     assert "passes in" in rec["sample"]
+    one = bench.cpu_baseline(inp, 1, O.k_max_for(inp), min_s=0.1, threads=1)
+    assert one["cores"] == 1
 
 
 def test_union_gather_rows_counts_distinct_positions_per_kv_head():
