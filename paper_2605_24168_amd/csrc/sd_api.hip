@@ -228,7 +228,9 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
 // the same layout is recomputed on every call.
 struct Layout {
   size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, umask, total;
+  size_t dsel_hist, dsel_state, dsel_cnt;
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
+  int dsel_parts;        // pieces per row of the multi-workgroup fallback selection (0: none)
   int64_t umask_stride;  // bytes per group of the head masks (0: none)
   int union_chunk;       // positions per union-attention workgroup (0: per-row lists)
 };
@@ -257,6 +259,36 @@ bool union_pays(const Shape &s, int64_t k_max) {
   const double per_head = G * kt * 512.0;
   const double uni = Lc * (1.0 - std::pow(1.0 - kt / Lc, G)) * 512.0 + 2.0 * G * Lc + G * kt;
   return uni < (s.G <= 4 ? 0.83 : 0.65) * per_head;
+}
+
+// Pieces per row for the fallback selection over several workgroups: about
+// 2048 workgroups in all, pieces of at least 2048 positions, rows of at
+// least 16K positions (shorter ones select fast enough in one workgroup);
+// 0 when that leaves fewer than two pieces.
+int dsel_parts_for(const Shape &s) {
+  const int64_t rows = (int64_t)s.B * s.R;
+  if (rows <= 0 || s.ncap < 16384) return 0;
+  int64_t parts = (2048 + rows - 1) / rows;
+  parts = std::min<int64_t>(parts, s.ncap / 2048);
+  parts = std::min<int64_t>(parts, sd::kDselPartsMax);
+  return parts >= 2 ? (int)parts : 0;
+}
+
+// Whether the pilot would send a row of the full capacity to the exact
+// fallback (its rule: the expected candidates of a scoring wave would fill
+// more than half of a row's staging area), so that the call can take the
+// fallback for every row without sampling or streaming first.  Forced
+// windows and per-sequence budgets are left to the pilot.
+bool all_rows_fall_back(const Shape &s, const sd_sparsity *sp, int wave_keys) {
+  if (sp->k_override || sp->n_sink > 0 || sp->n_local > 0 || s.ncap <= 0) return false;
+  const int64_t n = s.ncap;
+  const int64_t m = n < sd::kSampleMax ? n : sd::kSampleMax;
+  const int64_t k = sd::budget_rule(n, sp->ratio, sp->k_rounding);
+  if (k <= 0) return false;
+  const int64_t r = m < n ? sd::pilot_rank(k, m, n) : k;
+  const int64_t cap = sd::kCandBuf / (sp->group_shared ? 1 : s.G);
+  const int64_t span = n < wave_keys ? n : wave_keys;
+  return 2 * (r - 1) * span > cap * m;
 }
 
 Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *sp,
@@ -305,6 +337,12 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
     L.flags = take((size_t)rows * 4);
     L.dense = take((size_t)rows * s.ncap * 4);
     L.sigma = take((size_t)rows * k_max * 4);
+    L.dsel_parts = dsel_parts_for(s);
+    if (L.dsel_parts) {
+      L.dsel_hist = take((size_t)rows * 2048 * 4);
+      L.dsel_state = take((size_t)rows * 4 * 4);
+      L.dsel_cnt = take((size_t)rows * sd::kDselPartsMax * 8);
+    }
     if (uni_ok) {  // present whenever the call could use it (see union_pays)
       L.umask_stride = (int64_t)((s.ncap * s.G + 15) / 16 * 16);
       L.umask = take((size_t)s.B * s.Hkv * L.umask_stride);
@@ -368,6 +406,11 @@ sd::Work carve(char *base, const Layout &L, bool fused) {
     w.flags = (int32_t *)(base + L.flags);
     w.dense = (float *)(base + L.dense);
     w.sigma = (float *)(base + L.sigma);
+    if (L.dsel_parts) {
+      w.dsel_hist = (uint32_t *)(base + L.dsel_hist);
+      w.dsel_state = (int32_t *)(base + L.dsel_state);
+      w.dsel_cnt = (int2 *)(base + L.dsel_cnt);
+    }
   }
   w.part = (float *)(base + L.part);
   w.stats = (int32_t *)(base + L.stats);
@@ -651,8 +694,11 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   st = get_workspace(L.total, ds, base);
   if (st) return st;
   sd::Work w = carve(base, L, true);
-  // float32 caches (small problems) take the full-score path for every row.
-  if (!s.bf16) w.force_repair = 1;
+  // float32 caches (small problems) take the full-score path for every row,
+  // and so do calls whose rows the pilot would all send there.
+  if (!s.bf16 || all_rows_fall_back(s, sp, L.wave_keys)) w.force_repair = 1;
+  // Those rows select over several workgroups each when they are few.
+  if (w.force_repair && L.dsel_parts) w.dsel_parts = L.dsel_parts;
   sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   if (labels) {
     p.labels = (const uint16_t *)labels->t.data;
@@ -687,7 +733,8 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   const int64_t lds_room = (int64_t)((budget - pre_bytes) / 4);
   const int lds_cap = (int)(want < lds_room ? want : lds_room);
   hipError_t e = mark(0);
-  if (e == hipSuccess) e = sd::launch_pilot(p, w, stream_h);
+  // (the pilot's thresholds and flags serve only the scoring stream)
+  if (e == hipSuccess && !w.force_repair) e = sd::launch_pilot(p, w, stream_h);
   if (e == hipSuccess) e = mark(1);
   // Level 2 times the scoring kernel alone, with events attached to its
   // dispatch (recorded back to back when the kernel does not run).
@@ -700,6 +747,7 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   if (e == hipSuccess) e = mark(2);
   if (e == hipSuccess && s.ncap > 0) e = sd::launch_repair(p, w, stream_h);
   if (e == hipSuccess) e = mark(3);
+  if (e == hipSuccess) e = sd::launch_dense_select(p, w, idx_ptr, stream_h);
   if (e == hipSuccess) e = sd::launch_select_candidates(p, w, idx_ptr, lds_cap, wide, stream_h);
   if (e == hipSuccess && smp)
     e = sd::launch_sample_rest(p, idx_ptr, smp->draws, smp->n, smp->weights, stream_h);

@@ -22,6 +22,7 @@ constexpr int kChunkCap = kWaves * kCandBuf;  // entries of one workgroup's pack
 constexpr int kDenseChunk = 8192;  // keys per workgroup of the full-score kernels
 constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
+constexpr int kDselPartsMax = 64;  // pieces of a row in the multi-workgroup fallback selection
 constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the fallback scoring
 constexpr int kSelectWideRows = 256; // fewer rows: 1024-thread selection workgroups
 constexpr size_t kSelectShareLds = 70 * 1024;  // more dynamic LDS: one workgroup per CU
@@ -103,6 +104,13 @@ struct Work {
   uint8_t *umask;
   int64_t umask_stride;  // bytes per group, a multiple of 16
   int32_t union_chunk;
+  // Exact fallback selection over several workgroups per row (calls whose
+  // every row takes the fallback): dsel_parts pieces per row, 0 = each
+  // row's selection runs in one workgroup of k_select.
+  uint32_t *dsel_hist;  // [rows][2048] key-digit histograms (cleared by the repair)
+  int32_t *dsel_state;  // [rows][4]: key prefix, its mask, rank still to place
+  int2 *dsel_cnt;       // [rows][kDselPartsMax] (keys above, keys equal to) the threshold
+  int32_t dsel_parts;
 };
 
 // Scratch of the dense decode kernels.
@@ -642,13 +650,15 @@ __device__ __forceinline__ float merge_partials(const float *pp, int nsp, MergeS
 // is called for every kept item i with its output slot (0..k-1 in item
 // order).  Only keys are read here; the caller fetches whatever else a kept
 // item carries.  Each thread handles kIpt consecutive items per round.
+// compact_selected_from continues a compaction begun elsewhere: eq_before
+// items equal to T and sel_before kept items precede item 0 (slots start at
+// sel_before).
 // ---------------------------------------------------------------------------
 constexpr int kIpt = 8;
 
 template <int NT = kBlock, class Src, class Emit>
-__device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int need_eq, int *scan,
-                                 Emit emit) {
-  int eq_before = 0, sel_before = 0;
+__device__ void compact_selected_from(const Src &src, int n, int k, uint32_t T, int need_eq,
+                                      int *scan, int eq_before, int sel_before, Emit emit) {
   const int tid = threadIdx.x;
 #pragma unroll 1
   for (int base = 0; base < n && sel_before < k; base += NT * kIpt) {
@@ -688,6 +698,13 @@ __device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int n
     eq_before += eq_tot;
     sel_before += sel_tot;
   }
+}
+
+// The same over a whole row: no items before it.
+template <int NT = kBlock, class Src, class Emit>
+__device__ void compact_selected(const Src &src, int n, int k, uint32_t T, int need_eq, int *scan,
+                                 Emit emit) {
+  compact_selected_from<NT>(src, n, k, T, need_eq, scan, 0, 0, emit);
 }
 
 }  // namespace sd

@@ -740,7 +740,8 @@ __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, in
                             q_lds);
 }
 
-// Exact fallback, scoring.  grid = (kRepairParts, B*Hkv).  A row takes the
+// Exact fallback, scoring.  grid = (parts, B*Hkv), parts at least
+// kRepairParts (repair_parts).  A row takes the
 // fallback when every row is forced to, or when its candidates cannot prove
 // exactness: fewer than k passed, or a staging area overflowed (a per-chunk
 // count of -1).  Each workgroup derives its group's flags from the rows'
@@ -763,7 +764,7 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
     // selection marks the kept positions: part `part` of the 16-byte words.
     u32x4 *gm = (u32x4 *)(w.umask + (int64_t)bg * w.umask_stride);
     const int64_t nw = w.umask_stride / 16;
-    const int64_t per = (nw + kRepairParts - 1) / kRepairParts;
+    const int64_t per = (nw + gridDim.x - 1) / gridDim.x;
     const int64_t w1 = (part + 1) * per < nw ? (part + 1) * per : nw;
     const u32x4 z = {0u, 0u, 0u, 0u};
     for (int64_t i = part * per + tid; i < w1; i += kBlock) gm[i] = z;
@@ -773,6 +774,13 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
     bad[tid] = 0;
   }
   if (tid == 0) any = 0;
+  // The multi-workgroup fallback selection's histograms start at zero; with
+  // the pilot skipped (every row forced), the repaired-row count too.
+  if (w.dsel_parts) {
+    uint32_t *gh = w.dsel_hist + row0 * 2048;
+    for (int e = part * kBlock + tid; e < nrows * 2048; e += gridDim.x * kBlock) gh[e] = 0u;
+  }
+  if (w.force_repair && part == 0 && bg == 0 && tid == 0) w.stats[0] = 0;
   __syncthreads();
   if (k > 0 && !w.force_repair) {
     const int ck = w.chunk_keys;
@@ -791,7 +799,7 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
     if (part == 0) w.flags[row0 + tid] = flag ? 1 : 0;
   }
   __syncthreads();
-  if (any) dense_scores<BF16, LABEL>(p, w.dense, p.ncap, b, g, part, kRepairParts, false, q_lds);
+  if (any) dense_scores<BF16, LABEL>(p, w.dense, p.ncap, b, g, part, (int)gridDim.x, false, q_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -977,8 +985,9 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
   if (k > 0) {
     if (MODE == 0 && w.flags[row]) {  // the exact fallback: full scores
       if (tid == 0) atomicAdd(&w.stats[0], 1);
-      select_and_write<NT>(DenseSrc{w.dense + (int64_t)row * p.ncap + rp.lo, (uint32_t)rp.lo},
-                           rp.hi - rp.lo, k, hist, &sh, irow, vrow);
+      if (!w.dsel_parts)  // (else the k_dsel kernels wrote the selection)
+        select_and_write<NT>(DenseSrc{w.dense + (int64_t)row * p.ncap + rp.lo, (uint32_t)rp.lo},
+                             rp.hi - rp.lo, k, hist, &sh, irow, vrow);
     } else if (MODE == 0) {
       // Candidates: at least k of them and no overflow (else flagged).
       const int ck = w.chunk_keys;
@@ -1041,6 +1050,206 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
     uint8_t *gm = w.umask + ((int64_t)b * p.Hkv + rr / p.G) * w.umask_stride + rr % p.G;
     for (int i = tid; i < rp.total; i += NT) gm[(int64_t)lrow[i] * p.G] = 1;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Exact fallback selection over several workgroups per row, for calls whose
+// every row takes the fallback while the rows are too few to fill the GPU
+// one workgroup each.  A row's full scores (w.dense over its top-k range
+// [lo, hi)) are cut into gridDim.x consecutive pieces.  Three rounds fix the
+// k-th largest key 11, 11 and 10 bits at a time (the digits of
+// radix_select): in each, every piece adds the histogram of its keys that
+// match the bits fixed so far into the row's global histogram
+// (k_dsel_hist), and one workgroup per row picks the digit holding the
+// remaining rank and clears the histogram for the next round
+// (k_dsel_digit).  Each piece then counts its keys above and equal to the
+// threshold T (k_dsel_count) and writes its kept positions and scores, in
+// position order, at the offset the pieces before it leave (k_dsel_write);
+// keys equal to T are kept in position order up to the rank left over, so
+// the list is the one a single workgroup would write.  k_select then adds
+// the rest of each row's list (weights, forced positions, padding).
+// grid = (pieces, B*R) for the piece kernels, B*R for k_dsel_digit.
+// ---------------------------------------------------------------------------
+struct DselPiece {
+  const float *src;  // the row's scores from position lo
+  int i0, i1;        // the piece: items [i0, i1) of the top-k range
+  int k;             // the row's top-k budget (0: nothing to select)
+};
+
+__device__ __forceinline__ DselPiece dsel_piece(const Params &p, const Work &w, int row, int q,
+                                                int parts) {
+  const int b = row / p.R;
+  const RowPlan rp = row_plan(p, b, seq_len(p, b));
+  const int64_t n = rp.hi - rp.lo;
+  DselPiece d;
+  d.src = w.dense + (int64_t)row * p.ncap + rp.lo;
+  d.i0 = (int)(n * q / parts);
+  d.i1 = (int)(n * (q + 1) / parts);
+  d.k = w.flags[row] ? rp.kh : 0;
+  return d;
+}
+
+template <int PASS>
+__global__ __launch_bounds__(kBlock) void k_dsel_hist(Params p, Work w) {
+  __shared__ uint32_t hist[2048];
+  const int row = blockIdx.y;
+  const DselPiece d = dsel_piece(p, w, row, blockIdx.x, gridDim.x);
+  if (d.k == 0) return;  // whole workgroup
+  constexpr int shift = PASS == 0 ? 21 : (PASS == 1 ? 10 : 0);
+  constexpr int nb = PASS == 2 ? 1024 : 2048;
+  constexpr uint32_t dmask = (uint32_t)nb - 1u;
+  const uint32_t prefix = PASS == 0 ? 0u : (uint32_t)w.dsel_state[row * 4 + 0];
+  const uint32_t mask = PASS == 0 ? 0u : (uint32_t)w.dsel_state[row * 4 + 1];
+  const int tid = threadIdx.x;
+  for (int i = tid; i < nb; i += kBlock) hist[i] = 0;
+  __syncthreads();
+  for (int base = d.i0; base < d.i1; base += kBlock * kSelU) {
+    uint32_t key[kSelU];
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u) {  // the loads in flight together
+      const int i = base + u * kBlock + tid;
+      key[u] = i < d.i1 ? f2key(d.src[i]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u) {
+      const bool act = base + u * kBlock + tid < d.i1 && (key[u] & mask) == prefix;
+      hist_add(hist, (key[u] >> shift) & dmask, act);
+    }
+  }
+  __syncthreads();
+  uint32_t *g = w.dsel_hist + (int64_t)row * 2048;
+  for (int i = tid; i < nb; i += kBlock)
+    if (hist[i]) atomicAdd(&g[i], hist[i]);
+}
+
+template <int PASS>
+__global__ __launch_bounds__(kBlock) void k_dsel_digit(Params p, Work w) {
+  __shared__ uint32_t hist[2048];
+  __shared__ SelShared sh;
+  const int row = blockIdx.x;
+  const DselPiece d = dsel_piece(p, w, row, 0, 1);
+  if (d.k == 0) return;
+  constexpr int shift = PASS == 0 ? 21 : (PASS == 1 ? 10 : 0);
+  constexpr int nb = PASS == 2 ? 1024 : 2048;
+  constexpr uint32_t dmask = (uint32_t)nb - 1u;
+  int32_t *st = w.dsel_state + row * 4;
+  const uint32_t prefix = PASS == 0 ? 0u : (uint32_t)st[0];
+  const uint32_t mask = PASS == 0 ? 0u : (uint32_t)st[1];
+  const int krem = PASS == 0 ? d.k : st[2];
+  const int tid = threadIdx.x;
+  uint32_t *g = w.dsel_hist + (int64_t)row * 2048;
+  for (int i = tid; i < 2048; i += kBlock) {
+    hist[i] = i < nb ? g[i] : 0u;
+    g[i] = 0u;
+  }
+  if (tid == 0) {
+    sh.digit = 0;
+    sh.above = 0;
+  }
+  __syncthreads();
+  // Thread t owns bins [nb - (t+1)*bpt, nb - t*bpt): counting from the top.
+  constexpr int bpt = nb / kBlock;
+  const int hi = nb - tid * bpt;
+  int mine = 0;
+  for (int i = 1; i <= bpt; ++i) mine += (int)hist[hi - i];
+  int tot;
+  const int before = block_excl_scan<kBlock>(mine, sh.scan, &tot);
+  if (before < krem && krem <= before + mine) {
+    int cum = before;
+    for (int i = 1; i <= bpt; ++i) {
+      const int c = (int)hist[hi - i];
+      if (cum + c >= krem) {
+        sh.digit = (uint32_t)(hi - i);
+        sh.above = cum;
+        break;
+      }
+      cum += c;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    st[0] = (int32_t)(prefix | (sh.digit << shift));
+    st[1] = (int32_t)(mask | (dmask << shift));
+    st[2] = krem - sh.above;
+  }
+}
+
+__global__ __launch_bounds__(kBlock) void k_dsel_count(Params p, Work w) {
+  __shared__ int red[kWaves][2];
+  const int row = blockIdx.y;
+  const DselPiece d = dsel_piece(p, w, row, blockIdx.x, gridDim.x);
+  if (d.k == 0) return;
+  const uint32_t T = (uint32_t)w.dsel_state[row * 4 + 0];
+  const int tid = threadIdx.x;
+  int gt = 0, eq = 0;
+  for (int base = d.i0; base < d.i1; base += kBlock * kSelU) {
+    uint32_t key[kSelU];
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u) {
+      const int i = base + u * kBlock + tid;
+      key[u] = i < d.i1 ? f2key(d.src[i]) : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u) {
+      const bool in = base + u * kBlock + tid < d.i1;
+      gt += (in && key[u] > T) ? 1 : 0;
+      eq += (in && key[u] == T) ? 1 : 0;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    gt += __shfl_xor(gt, o);
+    eq += __shfl_xor(eq, o);
+  }
+  if (lane_id() == 0) {
+    red[wave_id()][0] = gt;
+    red[wave_id()][1] = eq;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int a = 0, e = 0;
+#pragma unroll
+    for (int v = 0; v < kWaves; ++v) {
+      a += red[v][0];
+      e += red[v][1];
+    }
+    w.dsel_cnt[(int64_t)row * kDselPartsMax + blockIdx.x] = make_int2(a, e);
+  }
+}
+
+struct PieceSrc {
+  const float *row;  // the piece's first score
+  __device__ __forceinline__ uint32_t key(int i) const { return f2key(row[i]); }
+};
+
+__global__ __launch_bounds__(kBlock) void k_dsel_write(Params p, Work w, int32_t *idx,
+                                                       float *vals) {
+  __shared__ int scan[kWaves];
+  const int row = blockIdx.y, q = blockIdx.x;
+  const DselPiece d = dsel_piece(p, w, row, q, gridDim.x);
+  if (d.k == 0) return;
+  const int b = row / p.R;
+  const RowPlan rp = row_plan(p, b, seq_len(p, b));
+  const uint32_t T = (uint32_t)w.dsel_state[row * 4 + 0];
+  const int need_eq = w.dsel_state[row * 4 + 2];
+  const int tid = threadIdx.x;
+  // Keys above and equal to T in the pieces before this one.
+  int2 c = make_int2(0, 0);
+  if (tid < q) c = w.dsel_cnt[(int64_t)row * kDselPartsMax + tid];
+  int gt_before, eq_before;
+  block_excl_scan<kBlock>(c.x, scan, &gt_before);
+  block_excl_scan<kBlock>(c.y, scan, &eq_before);
+  const int sel_before = gt_before + (eq_before < need_eq ? eq_before : need_eq);
+  const int64_t ist = p.idx_stride > 0 ? p.idx_stride : p.k_max;
+  int32_t *irow = idx + (int64_t)row * ist + rp.ns;
+  float *vrow = vals ? vals + (int64_t)row * p.k_max + rp.ns : nullptr;
+  const uint32_t base = (uint32_t)(rp.lo + d.i0);
+  compact_selected_from<kBlock>(PieceSrc{d.src + d.i0}, d.i1 - d.i0, d.k, T, need_eq, scan,
+                                eq_before, sel_before, [&](int slot, int i, uint32_t key) {
+                                  if (slot >= d.k) return;  // (never: exactly k are kept)
+                                  irow[slot] = (int32_t)(base + (uint32_t)i);
+                                  if (vrow) vrow[slot] = key2f(key);
+                                });
 }
 
 // ---------------------------------------------------------------------------
@@ -1616,8 +1825,37 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
   return hipGetLastError();
 }
 
+// Workgroups per (sequence, KV head) of the fallback scoring: kRepairParts,
+// or, when every row is forced onto the fallback and the groups are few,
+// enough for about 2048 in all (with one sequence each wave would otherwise
+// score a long run of tiles one after another, each waiting for its loads;
+// without forcing, flagged rows are rare and the extra workgroups would only
+// cost their launch).
+int repair_parts(const Params &p, const Work &w) {
+  if (!w.force_repair) return kRepairParts;
+  const int groups = p.B * p.Hkv;
+  int parts = (2048 + groups - 1) / groups;
+  parts = parts < kRepairParts ? kRepairParts : parts;
+  return parts > 256 ? 256 : parts;
+}
+
+hipError_t launch_dense_select(const Params &p, const Work &w, int32_t *idx, hipStream_t st) {
+  if (!w.dsel_parts) return hipSuccess;
+  const int rows = p.B * p.R;
+  const dim3 grid(w.dsel_parts, rows);
+  k_dsel_hist<0><<<grid, kBlock, 0, st>>>(p, w);
+  k_dsel_digit<0><<<rows, kBlock, 0, st>>>(p, w);
+  k_dsel_hist<1><<<grid, kBlock, 0, st>>>(p, w);
+  k_dsel_digit<1><<<rows, kBlock, 0, st>>>(p, w);
+  k_dsel_hist<2><<<grid, kBlock, 0, st>>>(p, w);
+  k_dsel_digit<2><<<rows, kBlock, 0, st>>>(p, w);
+  k_dsel_count<<<grid, kBlock, 0, st>>>(p, w);
+  k_dsel_write<<<grid, kBlock, 0, st>>>(p, w, idx, w.sigma);
+  return hipGetLastError();
+}
+
 hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st) {
-  const dim3 grid(kRepairParts, p.B * p.Hkv);
+  const dim3 grid(repair_parts(p, w), p.B * p.Hkv);
   if (p.labels) k_repair_score<true, true><<<grid, kBlock, 0, st>>>(p, w);
   else if (p.bf16) k_repair_score<true, false><<<grid, kBlock, 0, st>>>(p, w);
   else k_repair_score<false, false><<<grid, kBlock, 0, st>>>(p, w);

@@ -27,6 +27,9 @@ size_t select_lds_budget(bool wide);
 hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx, int lds_cap,
                                     bool wide, hipStream_t st);
 hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st);
+// The fallback rows' selection over w.dsel_parts workgroups per row (after
+// the repair, before launch_select_candidates); nothing when dsel_parts is 0.
+hipError_t launch_dense_select(const Params &p, const Work &w, int32_t *idx, hipStream_t st);
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st);
 int attend_nsplit(const Params &p);

@@ -186,6 +186,48 @@ def test_fused_exact_fallback_path_gives_identical_results(sd, name):
     np.testing.assert_array_equal(out_a, out_b)
 
 
+@pytest.mark.parametrize("debug", [0, 1])
+def test_fused_ties_at_the_threshold_go_to_the_lower_position(sd, debug):
+    # Keys repeat with period 50, so each head's scores take 50 values and
+    # the k-th is shared by about 400 positions: both the candidate path and
+    # the fallback (its selection cut into pieces over several workgroups,
+    # whose tied keys straddle the pieces) must keep the lowest positions
+    # among the tied ones, exactly as the oracle does.
+    inp = make("w2", seed=12)
+    period = np.arange(inp.ncap) % 50
+    inp = dataclasses.replace(inp, k=np.ascontiguousarray(inp.k[:, :, period]),
+                              v=np.ascontiguousarray(inp.v[:, :, period]))
+    sd.set_debug(debug)
+    try:
+        sd.set_profiling(True)
+        out, idx, _ = gpu_fused(sd, inp)
+        prof = sd.last_profile()
+    finally:
+        sd.set_debug(0)
+        sd.set_profiling(False)
+    if debug:
+        assert prof["repaired_rows"] == inp.B * inp.rows
+    ora = O.sparse_attention(inp)
+    np.testing.assert_array_equal(idx, ora["idx"])
+    ok, ratio, _ = P.out_errors(out, ora["out"], inp.dtype)
+    assert ok, f"output error {ratio:.3g} x allowance"
+
+
+def test_fused_low_sparsity_takes_the_fallback_for_every_row(sd):
+    # At 2x with 4 heads per KV head a scoring wave's expected candidates
+    # would overfill the staging areas, so the call scores every row in full
+    # and selects over several workgroups per row.
+    inp = make("w2", seed=13, ratio=2.0)
+    sd.set_profiling(True)
+    try:
+        out, idx, _ = gpu_fused(sd, inp)
+        prof = sd.last_profile()
+    finally:
+        sd.set_profiling(False)
+    assert prof["repaired_rows"] == inp.B * inp.rows
+    check_fused(inp, out, idx, label="2x, every row on the fallback")
+
+
 def test_fused_is_deterministic(sd):
     inp = make("w3", seed=4)
     a = gpu_fused(sd, inp)
