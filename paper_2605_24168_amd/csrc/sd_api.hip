@@ -227,11 +227,11 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
 // Workspace layout.  Sizes depend only on the shapes and the sparsity, so
 // the same layout is recomputed on every call.
 struct Layout {
-  size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, umask, total;
+  size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, ustart, total;
   size_t dsel_hist, dsel_state, dsel_cnt;
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
   int dsel_parts;        // pieces per row of the multi-workgroup fallback selection (0: none)
-  int64_t umask_stride;  // bytes per group of the head masks (0: none)
+  int ustride;           // chunk starts per row of the union attention (0: none)
   int union_chunk;       // positions per union-attention workgroup (0: per-row lists)
 };
 
@@ -245,7 +245,7 @@ bool union_eligible(const Shape &s, const sd_sparsity *sp, bool labels) {
 // Whether it is faster than per-head lists: each head's k_max kept rows
 // (key + value, 512 B) against the expected union of G such sets of an
 // Ncap-position range drawn independently (heads that agree only shrink the
-// union), plus clearing, reading and marking the masks.  The group-row
+// union), plus reading the heads' lists once more.  The group-row
 // kernel gathers at about 0.87 of the per-head kernel's rate for up to 4
 // heads (three waves per SIMD) and 0.7 for more (8 heads per pass: two
 // waves), measured at 128K, so the union must move under 0.83 or 0.65 of
@@ -257,7 +257,7 @@ bool union_pays(const Shape &s, int64_t k_max) {
   const double Lc = (double)s.ncap, G = s.G;
   const double kt = (double)(k_max < s.ncap ? k_max : s.ncap);
   const double per_head = G * kt * 512.0;
-  const double uni = Lc * (1.0 - std::pow(1.0 - kt / Lc, G)) * 512.0 + 2.0 * G * Lc + G * kt;
+  const double uni = Lc * (1.0 - std::pow(1.0 - kt / Lc, G)) * 512.0 + 4.0 * G * kt;
   return uni < (s.G <= 4 ? 0.83 : 0.65) * per_head;
 }
 
@@ -344,8 +344,9 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
       L.dsel_cnt = take((size_t)rows * sd::kDselPartsMax * 8);
     }
     if (uni_ok) {  // present whenever the call could use it (see union_pays)
-      L.umask_stride = (int64_t)((s.ncap * s.G + 15) / 16 * 16);
-      L.umask = take((size_t)s.B * s.Hkv * L.umask_stride);
+      const int uc = sd::union_chunk(shape_only);
+      L.ustride = (int)((s.ncap + uc - 1) / uc) + 1;
+      L.ustart = take((size_t)rows * L.ustride * 4);
       L.nsplit = std::max<int>(L.nsplit, (int)((s.ncap + sd::union_chunk(shape_only) - 1) /
                                                sd::union_chunk(shape_only)));
     }
@@ -414,8 +415,8 @@ sd::Work carve(char *base, const Layout &L, bool fused) {
   }
   w.part = (float *)(base + L.part);
   w.stats = (int32_t *)(base + L.stats);
-  w.umask = L.union_chunk > 0 ? (uint8_t *)(base + L.umask) : nullptr;
-  w.umask_stride = L.umask_stride;
+  w.ustart = L.union_chunk > 0 ? (int32_t *)(base + L.ustart) : nullptr;
+  w.ustride = L.ustride;
   w.union_chunk = L.union_chunk;
   w.nchunk = L.nchunk;
   w.wave_keys = L.wave_keys;

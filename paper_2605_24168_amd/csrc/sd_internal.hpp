@@ -84,8 +84,9 @@ struct Work {
   uint16_t *cpos;    // [B*Hkv][nchunk][blk_cap] positions within the chunk
   int32_t *flags;    // [rows] 1 = the row needs the exact fallback
   float *dense;      // [rows][ncap] fallback scores
-  float *sigma;      // [rows][k_max] kept scores (group-shared mode) or softmax
-                     // weights exp(scale*(s - max s)) (per-head mode), aligned with idx
+  float *sigma;      // [rows][k_max] softmax weights exp(scale*(s - max s)) of the
+                     // kept entries, aligned with idx (per-head rows whose attention
+                     // does not recompute its logits; otherwise unused)
   float *part;       // [B*Hq][nsplit][kPartStride] attend partials
   int32_t *stats;    // [4]: [0] rows repaired in the last call
   int32_t nchunk;      // chunks per sequence (of chunk_keys keys)
@@ -96,13 +97,13 @@ struct Work {
   int32_t nsplit;
   int32_t force_repair;  // every row takes the exact fallback
   // Group-deduplicated attention (per-head rows whose logits are recomputed,
-  // GQA): umask[(b*Hkv + g) * umask_stride + j*G + h] = 1 when head h of
-  // group g keeps position j (cleared in the call before the selection marks
-  // it); the attention then reads each kept key and value row once for the
-  // whole group, union_chunk positions per workgroup.  Null / 0: per-row
-  // lists.
-  uint8_t *umask;
-  int64_t umask_stride;  // bytes per group, a multiple of 16
+  // GQA): ustart[row * ustride + c] is the first entry of the row's list at
+  // or past position c * union_chunk (c = 0 .. ceil(L / union_chunk); the
+  // selection writes it after the list); the attention then takes, chunk by
+  // chunk, the positions any head of a group keeps and reads each kept key
+  // and value row once for the whole group.  Null / 0: per-row lists.
+  int32_t *ustart;
+  int32_t ustride;
   int32_t union_chunk;
   // Exact fallback selection over several workgroups per row (calls whose
   // every row takes the fallback): dsel_parts pieces per row, 0 = each

@@ -759,16 +759,6 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   const int k = row_plan(p, b, L).kh;
   const int64_t row0 = p.group_shared ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
   const int tid = threadIdx.x;
-  if (w.umask) {
-    // The group's head masks (union attention), cleared before the
-    // selection marks the kept positions: part `part` of the 16-byte words.
-    u32x4 *gm = (u32x4 *)(w.umask + (int64_t)bg * w.umask_stride);
-    const int64_t nw = w.umask_stride / 16;
-    const int64_t per = (nw + gridDim.x - 1) / gridDim.x;
-    const int64_t w1 = (part + 1) * per < nw ? (part + 1) * per : nw;
-    const u32x4 z = {0u, 0u, 0u, 0u};
-    for (int64_t i = part * per + tid; i < w1; i += kBlock) gm[i] = z;
-  }
   if (tid < kMaxGroup) {
     cnt[tid] = 0;
     bad[tid] = 0;
@@ -900,8 +890,8 @@ __device__ __forceinline__ void flatten_cands(const ChunkCands &src, uint32_t *f
 // k-th largest by bucket_kth (radix passes over the key bits when it
 // declines).  The compaction then records each kept item's index in place
 // of the consumed keys (slot <= item index, and a round reads all its keys
-// before its scans) and writes the softmax weights exp(scale * (s - vmax))
-// (or, group-shared mode, the kept scores); finally every thread fetches
+// before its scans) and, when vrow is given, writes the softmax weights
+// exp(scale * (s - vmax)) (weights set) or the kept scores; finally every thread fetches
 // the positions of its kept items with the loads in flight together.
 template <int NT>
 __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, int n, int k,
@@ -918,8 +908,10 @@ __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, i
   uint32_t *stage = const_cast<uint32_t *>(src.flat);
   compact_selected<NT>(src, n, k, T, need_eq, sh->scan, [&](int slot, int i, uint32_t key) {
     stage[slot] = (uint32_t)i;
-    const float v = key2f(key);
-    vrow[slot] = weights ? expf(scale * (v - vmax)) : v;
+    if (vrow) {
+      const float v = key2f(key);
+      vrow[slot] = weights ? expf(scale * (v - vmax)) : v;
+    }
   });
   __syncthreads();
   constexpr int kP = 8;  // position loads in flight per thread
@@ -974,7 +966,7 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
   // forced local window.
   const RowPlan rp = row_plan(p, b, L);
   const bool forced = rp.ns + rp.nl > 0;
-  const bool weights = MODE != 1 && !p.group_shared && !forced;
+  const bool weights = MODE != 1 && !p.group_shared && !forced && vals != nullptr;
   const int k = rp.kh;
   const int64_t ist = p.idx_stride > 0 ? p.idx_stride : p.k_max;  // list row stride
   int32_t *lrow = idx + (int64_t)row * ist;
@@ -1043,12 +1035,18 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
   for (int i = rp.total + tid; i < ist; i += NT) lrow[i] = -1;
   if (lvals)
     for (int i = rp.total + tid; i < p.k_max; i += NT) lvals[i] = -__builtin_inff();
-  if (MODE == 0 && w.umask) {
-    // Union attention: mark this head's kept positions in its group's mask.
+  if (MODE == 0 && w.ustart) {
+    // Union attention: where each chunk of union_chunk positions begins in
+    // this row's (ascending) list; entry `total` closes the last chunk.
     __syncthreads();  // the list was written by every thread of the block
-    const int rr = row % p.R;
-    uint8_t *gm = w.umask + ((int64_t)b * p.Hkv + rr / p.G) * w.umask_stride + rr % p.G;
-    for (int i = tid; i < rp.total; i += NT) gm[(int64_t)lrow[i] * p.G] = 1;
+    const int uc = w.union_chunk;
+    const int nck = (L + uc - 1) / uc;
+    int32_t *us = w.ustart + (int64_t)row * w.ustride;
+    for (int i = tid; i <= rp.total; i += NT) {
+      const int cur = i < rp.total ? lrow[i] / uc : nck;
+      const int prev = i > 0 ? lrow[i - 1] / uc : -1;
+      for (int c = prev + 1; c <= cur; ++c) us[c] = i;
+    }
   }
 }
 
@@ -1392,7 +1390,7 @@ struct AttLds {
 
 // UNI (union attention, with FUSED and GRP): the workgroup of (chunk s,
 // group (b, g)) takes the positions [s*split, +split) that any head of the
-// group keeps (the group's head masks), in order, and serves every head,
+// group keeps (from the heads' lists and chunk starts), in order, and serves every head,
 // each over its own positions only.  HBU: heads accumulated per pass over
 // the value rows in group mode (4 for groups of at most 4 heads: fewer
 // registers, three waves per SIMD instead of two).
@@ -1442,43 +1440,58 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
 
   if constexpr (UNI) {
     // The chunk's positions that some head keeps, in order, with their head
-    // bits: each thread packs the G mask bytes of kUnionPerThread consecutive
-    // positions, then one block scan places the kept ones.
+    // bits: each head's entries in the chunk (the span its chunk starts give)
+    // set the head's bit of their positions in an LDS bitmap (the key
+    // offset area, free until the offsets are resolved); then each thread
+    // takes kUnionPerThread consecutive positions and one block scan places
+    // the kept ones.
     __shared__ int scan_tmp[kWaves];
-    const uint8_t *gm = w.umask + ((int64_t)b * p.Hkv + g) * w.umask_stride + (int64_t)e0 * p.G;
-    uint32_t bits[kUnionPerThread];
-    int cnt = 0;
-    const int t0u = tid * kUnionPerThread;  // n <= split <= kUnionChunkMax
-    if (nh % 4 == 0 && t0u + kUnionPerThread <= n) {
-      // This thread's 4 G mask bytes in 16-byte loads (the group's masks
-      // start 16-byte aligned, and so does every 4 positions' span here).
-      const u32x4 *src = (const u32x4 *)(gm + (int64_t)t0u * nh);
+    __shared__ int hspan[kMaxGroup][2];
+    uint32_t *hb = (uint32_t *)koff_l;  // n <= split <= kUnionChunkMax words
+    for (int t = tid; t < n; t += kBlock) hb[t] = 0u;
+    if (tid < nh) {
+      const int32_t *us = w.ustart + ((int64_t)b * p.R + h0 + tid) * w.ustride;
+      hspan[tid][0] = us[s];
+      hspan[tid][1] = us[s + 1];
+    }
+    __syncthreads();
+    // The heads' entries as one flat range (head by head), four per thread
+    // per round with their loads in flight together.
+    int tot_e = 0;
+    for (int h = 0; h < nh; ++h) tot_e += hspan[h][1] - hspan[h][0];
+    const int32_t *lists = idx + ((int64_t)b * p.R + h0) * p.k_max;
+    for (int ebase = tid; ebase < tot_e; ebase += 4 * kBlock) {
+      int pos[4], hh[4];
 #pragma unroll
-      for (int u = 0; u < kUnionPerThread; ++u) bits[u] = 0u;
-      for (int v = 0; v < nh / 4; ++v) {  // the bytes in order: position u * nh + head h
-        const u32x4 x = src[v];
-#pragma unroll
-        for (int c = 0; c < 16; ++c) {
-          const int byte = 16 * v + c;  // = position u * nh + head h
-          const uint32_t nz = ((x[c >> 2] >> (8 * (c & 3))) & 0xFFu) != 0u ? 1u : 0u;
-          const int u = byte / nh, h = byte % nh;
-#pragma unroll
-          for (int uu = 0; uu < kUnionPerThread; ++uu)
-            if (uu == u) bits[uu] |= nz << h;
+      for (int u = 0; u < 4; ++u) {
+        const int e = ebase + u * kBlock;
+        hh[u] = -1;
+        pos[u] = 0;
+        if (e < tot_e) {
+          int h = 0, before = 0;
+          while (h < nh - 1 && e >= before + hspan[h][1] - hspan[h][0]) {
+            before += hspan[h][1] - hspan[h][0];
+            ++h;
+          }
+          hh[u] = h;
+          pos[u] = lists[(int64_t)h * p.k_max + hspan[h][0] + (e - before)];
         }
       }
 #pragma unroll
-      for (int u = 0; u < kUnionPerThread; ++u) cnt += bits[u] != 0u ? 1 : 0;
-    } else {
-#pragma unroll
-      for (int u = 0; u < kUnionPerThread; ++u) {
-        const int t = t0u + u;
-        uint32_t m = 0u;
-        if (t < n)
-          for (int h = 0; h < nh; ++h) m |= (uint32_t)(gm[(int64_t)t * nh + h] != 0) << h;
-        bits[u] = m;
-        cnt += m != 0u ? 1 : 0;
+      for (int u = 0; u < 4; ++u) {
+        const int off = pos[u] - e0;
+        if (hh[u] >= 0 && (unsigned)off < (unsigned)n) atomicOr(&hb[off], 1u << hh[u]);
       }
+    }
+    __syncthreads();
+    uint32_t bits[kUnionPerThread];
+    int cnt = 0;
+    const int t0u = tid * kUnionPerThread;  // n <= split <= kUnionChunkMax
+#pragma unroll
+    for (int u = 0; u < kUnionPerThread; ++u) {
+      const int t = t0u + u;
+      bits[u] = t < n ? hb[t] : 0u;
+      cnt += bits[u] != 0u ? 1 : 0;
     }
     int tot;
     int slot = block_excl_scan<kBlock>(cnt, scan_tmp, &tot);
@@ -1818,10 +1831,13 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
                                     bool wide, hipStream_t st) {
   const size_t lds = select_lds_bytes(w.nchunk, lds_cap);
   const unsigned rows = (unsigned)(p.B * p.R);
+  // The kept scores / weights only serve an attention that does not
+  // recompute its logits.
+  float *vals = attend_recompute(true, p) ? nullptr : w.sigma;
   if (wide)
-    k_select<0, 1024><<<rows, 1024, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
+    k_select<0, 1024><<<rows, 1024, lds, st>>>(p, w, nullptr, 0, idx, vals, lds_cap);
   else
-    k_select<0, kBlock><<<rows, kBlock, lds, st>>>(p, w, nullptr, 0, idx, w.sigma, lds_cap);
+    k_select<0, kBlock><<<rows, kBlock, lds, st>>>(p, w, nullptr, 0, idx, vals, lds_cap);
   return hipGetLastError();
 }
 
@@ -1850,7 +1866,7 @@ hipError_t launch_dense_select(const Params &p, const Work &w, int32_t *idx, hip
   k_dsel_hist<2><<<grid, kBlock, 0, st>>>(p, w);
   k_dsel_digit<2><<<rows, kBlock, 0, st>>>(p, w);
   k_dsel_count<<<grid, kBlock, 0, st>>>(p, w);
-  k_dsel_write<<<grid, kBlock, 0, st>>>(p, w, idx, w.sigma);
+  k_dsel_write<<<grid, kBlock, 0, st>>>(p, w, idx, attend_recompute(true, p) ? nullptr : w.sigma);
   return hipGetLastError();
 }
 
@@ -1923,7 +1939,7 @@ int union_chunk(const Params &p) {
 hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, void *out, bool fused,
                          hipStream_t st) {
   if (fused && w.union_chunk > 0) {  // group-deduplicated attention
-    if (!p.bf16 || p.group_shared || w.union_chunk > kUnionChunkMax || !w.umask)
+    if (!p.bf16 || p.group_shared || w.union_chunk > kUnionChunkMax || !w.ustart)
       return hipErrorInvalidValue;
     const int split = w.union_chunk;
     const size_t lds = (size_t)AttLds(split, p.G, true, true).total;
