@@ -415,6 +415,14 @@ def test_float32_gqa_and_paged(sd):
     check_fused(inp, out, idx, label="f32 paged")
 
 
+def test_float32_rows_selected_in_pieces(sd):
+    # float32 caches take the full-score path for every row; rows of 16K
+    # positions and more are selected over several workgroups each.
+    inp = make("w4", seed=14, B=3, lmin=16000, lmax=24000, N=24000, dtype="f32")
+    out, idx, _ = gpu_fused(sd, inp)
+    check_fused(inp, out, idx, label="f32 paged, pieces")
+
+
 def test_k_override(sd):
     inp = make("w2", seed=11, B=4, N=3000)
     ko = np.array([0, 1, 3000, 77], np.int32)

@@ -134,6 +134,16 @@ def test_sampled_without_draws_is_the_top_k_attention(sd):
     assert ok, f"{ratio:.3g} x allowance"
 
 
+def test_sampled_at_low_sparsity_through_the_fallback(sd):
+    # At 2x with 4 heads per KV head every row takes the exact fallback, its
+    # selection cut into pieces over several workgroups, with the draws'
+    # slots after each kept list.
+    inp = make("w2", seed=7, ratio=2.0)
+    draws = random_draws(inp, 96, seed=8)
+    out, idx, w = run(sd, inp, draws)
+    check(inp, draws, out, idx, w, "sampled 2x")
+
+
 def test_sampled_full_size_on_sampled_sequences(sd):
     # Workload 3 at full size with the bench's first sampled line (top-k
     # 1/200 plus 1311 draws per row), two sequences checked by the oracle.
