@@ -274,12 +274,17 @@ int dsel_parts_for(const Shape &s) {
   return parts >= 2 ? (int)parts : 0;
 }
 
+constexpr int64_t kManyCandidates = 48 * 1024;
+
 // Whether the pilot would send a row of the full capacity to the exact
 // fallback (its rule: the expected candidates of a scoring wave would fill
 // more than half of a row's staging area), so that the call can take the
 // fallback for every row without sampling or streaming first.  Per-sequence
 // budgets are left to the pilot.
-bool all_rows_fall_back(const Shape &s, const sd_sparsity *sp, int wave_keys, int64_t k_max) {
+// cands: the candidates the pilot would pass in such a row (r n / m).
+bool all_rows_fall_back(const Shape &s, const sd_sparsity *sp, int wave_keys, int64_t k_max,
+                        int64_t *cands = nullptr) {
+  if (cands) *cands = 0;
   if (sp->k_override || s.ncap <= 0 || s.ncap > INT32_MAX) return false;
   const sd::RowPlan rp = sd::row_plan((int)s.ncap, sp->n_sink, sp->n_local,
                                       sd::budget_rule(s.ncap, sp->ratio, sp->k_rounding),
@@ -288,6 +293,7 @@ bool all_rows_fall_back(const Shape &s, const sd_sparsity *sp, int wave_keys, in
   if (k <= 0 || n <= 0) return false;
   const int64_t m = n < sd::kSampleMax ? n : sd::kSampleMax;
   const int64_t r = m < n ? sd::pilot_rank(k, m, n) : k;
+  if (cands) *cands = r * n / m;
   const int64_t cap = sd::kCandBuf / (sp->group_shared ? 1 : s.G);
   const int64_t span = n < wave_keys ? n : wave_keys;
   return 2 * (r - 1) * span > cap * m;
@@ -699,7 +705,12 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   sd::Work w = carve(base, L, true);
   // float32 caches (small problems) take the full-score path for every row,
   // and so do calls whose rows the pilot would all send there.
-  if (!s.bf16 || all_rows_fall_back(s, sp, L.wave_keys, k_max)) w.force_repair = 1;
+  int64_t cands = 0;
+  if (!s.bf16 || all_rows_fall_back(s, sp, L.wave_keys, k_max, &cands)) w.force_repair = 1;
+  // So do few rows with very many candidates each (low sparsity): selecting
+  // tens of thousands of candidates in one workgroup per row costs more than
+  // selecting full rows over 16 or more workgroups each.
+  if (L.dsel_parts >= 16 && cands >= kManyCandidates) w.force_repair = 1;
   // Those rows select over several workgroups each when they are few.
   if (w.force_repair && L.dsel_parts) w.dsel_parts = L.dsel_parts;
   sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
