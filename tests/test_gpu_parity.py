@@ -440,6 +440,32 @@ def test_k_override(sd):
     assert (idx.cpu().numpy()[0] == -1).all()
 
 
+def test_fallback_pieces_at_extreme_budgets(sd):
+    # Every row forced onto the fallback with rows long enough to be cut
+    # into pieces: budgets of 0, 1, the whole row and one in between, so
+    # that the kept positions sit in one piece, in all pieces, or in none.
+    N = 20007
+    inp = make("w2", seed=16, B=4, N=N)
+    ko = np.array([0, 1, N, 4099], np.int32)
+    q, cache, lens = sd.cache_from_inputs(inp)
+    sp = sd.sparsity_from_inputs(inp, k_override=torch.from_numpy(ko).cuda())
+    sd.set_debug(1)
+    try:
+        out, idx = sd.sparse_decode_attention(q, cache, lens, sp, k_max=N)
+        torch.cuda.synchronize()
+    finally:
+        sd.set_debug(0)
+    idx = idx.cpu().numpy()
+    ora = O.sparse_attention(inp, k_max=N, k_override=ko)
+    rep = P.check_idx_rows(idx, ora["idx"], O.scores(inp), ora["tau"], inp.seq_lens, ko)
+    assert rep.strict_mismatch_rows == 0, rep.first_failure
+    assert (idx[0] == -1).all()
+    np.testing.assert_array_equal(idx[2], np.broadcast_to(np.arange(N), idx[2].shape))
+    ok, ratio, _ = P.out_errors(P.to_host(out), ora["out"] if not rep.band_swaps
+                                else O.attend(inp, idx)[0], "bf16")
+    assert ok, f"{ratio:.3g} x allowance"
+
+
 def test_workspace_from_caller(sd):
     inp = make("w2", seed=12, B=2, N=7000)
     q, cache, lens = sd.cache_from_inputs(inp)
