@@ -32,6 +32,7 @@ struct DevState {
   int level[kRing] = {};  // profiling level each ring slot was recorded with
   int64_t n_calls = 0;  // profiled calls in the current series
   int32_t *stats = nullptr;
+  int n_cu = 0;         // compute units (0: not queried yet)
 };
 
 std::mutex g_mu;
@@ -228,6 +229,7 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
 // the same layout is recomputed on every call.
 struct Layout {
   size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, ustart, total;
+  size_t queue, unit_pre;
   size_t dsel_hist, dsel_state, dsel_cnt;
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
   int dsel_parts;        // pieces per row of the multi-workgroup fallback selection (0: none)
@@ -345,6 +347,8 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
     L.flags = take((size_t)rows * 4);
     L.dense = take((size_t)rows * s.ncap * 4);
     L.sigma = take((size_t)rows * k_max * 4);
+    L.queue = take(4);
+    L.unit_pre = take((size_t)(s.B + 1) * 4);
     L.dsel_parts = dsel_parts_for(s);
     if (L.dsel_parts) {
       L.dsel_hist = take((size_t)rows * 2048 * 4);
@@ -401,10 +405,16 @@ sd_status get_workspace(size_t bytes, DevState *&ds, char *&base) {
     ds->ws_bytes = bytes;
   }
   base = (char *)ds->ws;
+  if (ds->n_cu == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return SD_ERR_HIP;
+    ds->n_cu = n > 0 ? n : 1;
+  }
   return SD_OK;
 }
 
-sd::Work carve(char *base, const Layout &L, bool fused) {
+sd::Work carve(char *base, const Layout &L, bool fused, const Shape &s) {
   sd::Work w{};
   if (fused) {
     w.sample = (float *)(base + L.sample);
@@ -415,6 +425,9 @@ sd::Work carve(char *base, const Layout &L, bool fused) {
     w.flags = (int32_t *)(base + L.flags);
     w.dense = (float *)(base + L.dense);
     w.sigma = (float *)(base + L.sigma);
+    w.queue = (int32_t *)(base + L.queue);
+    w.unit_pre = (int32_t *)(base + L.unit_pre);
+    w.unit_heads = L.chunk_keys == L.wave_keys ? s.Hkv / sd::kWaves : s.Hkv;
     if (L.dsel_parts) {
       w.dsel_hist = (uint32_t *)(base + L.dsel_hist);
       w.dsel_state = (int32_t *)(base + L.dsel_state);
@@ -576,7 +589,7 @@ sd_status sparse_decode_attend(const sd_tensor *q, const sd_kv *K, const sd_kv *
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
   if (st) return st;
-  const sd::Work w = carve(base, L, false);
+  const sd::Work w = carve(base, L, false, s);
   const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   return hip_status(sd::launch_attend(p, w, (const int32_t *)idx->data, out->data, false,
                                       (hipStream_t)stream));
@@ -609,7 +622,7 @@ sd_status sparse_decode_attend_weighted(const sd_tensor *q, const sd_kv *K, cons
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
   if (st) return st;
-  const sd::Work w = carve(base, L, false);
+  const sd::Work w = carve(base, L, false, s);
   sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   p.weights = (const float *)weights->data;
   return hip_status(sd::launch_attend(p, w, (const int32_t *)idx->data, out->data, false,
@@ -702,7 +715,7 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
   if (st) return st;
-  sd::Work w = carve(base, L, true);
+  sd::Work w = carve(base, L, true, s);
   // float32 caches (small problems) take the full-score path for every row,
   // and so do calls whose rows the pilot would all send there.
   int64_t cands = 0;
@@ -719,6 +732,11 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
     p.channels = labels->channels;
   }
   if (smp) p.idx_stride = (int32_t)k_list;
+  // Exact key scores stream on one persistent workgroup per compute unit;
+  // the label stream (bound by the vector ALUs) keeps one workgroup per
+  // chunk, several per compute unit.
+  w.persistent = labels ? 0 : 1;
+  w.stream_wgs = ds->n_cu;
   int32_t *idx_ptr = (int32_t *)idx->data;
 
   const int prof_level = g_profiling.load();

@@ -29,6 +29,8 @@ constexpr size_t kSelectShareLds = 70 * 1024;  // more dynamic LDS: one workgrou
 constexpr int kDenseWaveKeysMax = 8192; // keys per work item of the dense decode kernel
 constexpr int kDenseMaxGroup = 8;     // query heads per KV head of the dense decode kernel
 constexpr int kLabels = 8;            // label channels per key of the low-channel indexer
+constexpr int kOutboxCap = 16384;     // candidates a persistent stream workgroup holds in LDS
+constexpr int kOutboxBlocks = 64;     // blocks it holds at once
 
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -112,6 +114,16 @@ struct Work {
   int32_t *dsel_state;  // [rows][4]: key prefix, its mask, rank still to place
   int2 *dsel_cnt;       // [rows][kDselPartsMax] (keys above, keys equal to) the threshold
   int32_t dsel_parts;
+  // Persistent scoring stream: one workgroup per compute unit takes units
+  // (chunks) from a queue; k_pilot_select writes the work list and resets
+  // the queue.  unit_pre[b] = units of the sequences before b (B + 1
+  // entries); unit_heads = units per chunk of a sequence (Hkv, or Hkv / 4
+  // when each wave of a workgroup scores its own KV head).
+  int32_t persistent;
+  int32_t stream_wgs;   // workgroups of the persistent launch (compute units)
+  int32_t unit_heads;
+  int32_t *queue;
+  int32_t *unit_pre;
 };
 
 // Scratch of the dense decode kernels.

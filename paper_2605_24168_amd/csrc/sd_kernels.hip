@@ -283,6 +283,23 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __shared__ BucketShared<> bs;
   __shared__ uint32_t range[kWaves][2];
   const int row = blockIdx.x, b = row / p.R;
+  if (row == 0 && w.persistent) {
+    // The persistent stream's work list: ceil(L_b / chunk_keys) chunks of
+    // every sequence, unit_heads units each, and an empty queue.
+    int carry = 0;
+    for (int base = 0; base < p.B; base += kBlock) {
+      const int bb = base + (int)threadIdx.x;
+      const int units = bb < p.B ? (seq_len(p, bb) + w.chunk_keys - 1) / w.chunk_keys * w.unit_heads : 0;
+      int tot;
+      const int e = block_excl_scan(units, sh.scan, &tot);
+      if (bb < p.B) w.unit_pre[bb] = carry + e;
+      carry += tot;
+    }
+    if (threadIdx.x == 0) {
+      w.unit_pre[p.B] = carry;
+      w.queue[0] = 0;
+    }
+  }
   const int L = seq_len(p, b);
   const RowPlan rp = row_plan(p, b, L);
   const int k = rp.kh;
@@ -337,29 +354,127 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
 }
 
 // ---------------------------------------------------------------------------
-// The scoring stream.  grid = nchunk * B * Hkv workgroups, one per (chunk,
-// sequence, KV head); a chunk is kWaves * wk keys (wk = w.wave_keys).  Wave
-// v of the workgroup of chunk c streams keys
-// [c*4wk + v*wk, +wk) of one (sequence, KV head) in 16-key MFMA tiles,
-// kDepth tiles in flight, and stages the keys at or above each row's
-// threshold in LDS, in position order, one area of kCandBuf / rows entries
-// per row of the group.  At the end the workgroup writes one packed block:
-// for every row its candidates (keys, then chunk-relative positions), in
-// position order, rows one after another; dir[row][c] gets the row's
-// (start, count) in the block, count -1 if one of its areas overflowed.
-// The streaming loop issues no global stores, so its load waits stay exact;
-// the block goes out in a few fully coalesced nontemporal stores.
+// The scoring stream.  Its unit of work is one chunk of one (sequence, KV
+// head): kWaves * wk keys (wk = w.wave_keys), wave v streaming keys
+// [c*4wk + v*wk, +wk) in 16-key MFMA tiles, kDepth tiles in flight, and
+// staging the keys at or above each row's threshold in LDS, in position
+// order, one area of kCandBuf / rows entries per row of the group.  Each
+// unit leaves one packed block: for every row its candidates (keys, then
+// chunk-relative positions), in position order, rows one after another;
+// dir[row][c] gets the row's (start, count) in the block, count -1 if one
+// of its areas overflowed.  (QUAD: the unit is one chunk of wk keys of four
+// KV heads, one per wave, and each wave's head gets its own block.)
+//
+// Persistent launch (w.persistent): one workgroup per compute unit takes
+// units from a device-side queue until none is left.  The units are those
+// of k_pilot_select's work list (unit_pre: units of the sequences before
+// each one, so that chunks past a sequence's end are never handed out),
+// hence a ragged batch stays balanced.  The blocks a workgroup produces are
+// kept in an LDS outbox and written to HBM when it is full and when the
+// workgroup runs out of work: HBM writes interleaved with the key stream
+// cost far more than their bytes on this memory system (about 1.7 us per
+// MB of candidates measured at the 128K batch-16 workload), while one burst
+// at the end, after the reads, costs little.
+// Otherwise (label rows: that stream is bound by the vector ALUs and wants
+// several workgroups per compute unit) one workgroup per unit, on a static
+// grid that includes empty chunks, writes its block directly.
+// The streaming loop issues no global stores, so its load waits stay exact.
 // ---------------------------------------------------------------------------
 constexpr int kDepth = 3;        // tiles in flight per wave
 constexpr int kWavePages = kWaveKeysMax / kTile;
 static_assert(kCandBuf / kMaxGroup >= kTile, "every row must hold a tile's keys");
 static_assert(kChunkCap % 4 == 0 && kWaves * kMaxGroup == 64, "block layout");
+static_assert(kOutboxCap >= kChunkCap && kOutboxCap % 4 == 0, "a unit's blocks fit an empty outbox");
 
 struct WaveLds {
   u32x4 tile[256];
   uint2 cand[kCandBuf + 64];   // per-row areas of (score bits, position in wave), +64 discard slots
   int32_t page[kWavePages];
 };
+
+// The LDS outbox of a persistent stream workgroup: nb blocks of n entries
+// in all (keys in obk, positions in obp, each block starting at a multiple
+// of 4 entries), block j going to entry dst[j] of the candidate blocks.
+// The key and position arrays follow the struct in dynamic LDS (16-byte
+// aligned for the 16-byte accesses).
+struct alignas(16) Outbox {
+  uint32_t *obk;
+  uint16_t *obp;
+  int n, nb;
+  int64_t dst[kOutboxBlocks];
+  int off[kOutboxBlocks], cnt[kOutboxBlocks];
+};
+
+struct StreamLds {
+  WaveLds wave[kWaves];
+  int seg_n[kWaves * kMaxGroup];          // [row][wave] candidates found
+  int seg_off[kWaves * (kMaxGroup + 1)];  // their offsets in the block(s)
+  int wave_tot[kWaves];                   // QUAD: entries of each wave's block
+  int unit;                               // the unit taken from the queue
+  Outbox ob;
+};
+
+// Write the outbox's blocks to the candidate blocks (16- and 8-byte
+// nontemporal stores) and empty it.  Every thread of the block must call it.
+__device__ __forceinline__ void outbox_flush(const Work &w, Outbox &ob) {
+  __syncthreads();
+  for (int j = 0; j < ob.nb; ++j) {
+    const int off = ob.off[j], cnt = ob.cnt[j];
+    const int64_t dst = ob.dst[j];
+    for (int i0 = 4 * (int)threadIdx.x; i0 < cnt; i0 += 4 * kBlock) {
+      __builtin_nontemporal_store(*(const u32x4 *)(ob.obk + off + i0), (u32x4 *)(w.ckey + dst + i0));
+      __builtin_nontemporal_store(*(const unsigned long long *)(ob.obp + off + i0),
+                                  (unsigned long long *)(w.cpos + dst + i0));
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    ob.n = 0;
+    ob.nb = 0;
+  }
+  __syncthreads();
+}
+
+// Room in the outbox for `need` entries in `blocks` more blocks: returns
+// where they start, after flushing it if they do not fit.  Every thread of
+// the block must call it; it ends with a barrier, so that no thread reads
+// the outbox state after thread 0 advances it.
+__device__ __forceinline__ int outbox_reserve(const Work &w, Outbox &ob, int need, int blocks) {
+  if (ob.n + need > kOutboxCap || ob.nb + blocks > kOutboxBlocks) outbox_flush(w, ob);
+  const int base = ob.n;
+  __syncthreads();
+  return base;
+}
+
+// Pack entries [i0, i0 + 4) of a block (item i: entry i of the staged
+// candidates, found by cand_of) into 16 + 8 bytes and store them at kdst /
+// pdst + i0, in LDS (outbox) or in HBM (nontemporal).
+template <class CandOf>
+__device__ __forceinline__ void pack4(int i0, int ntot, CandOf cand_of, uint32_t *kdst,
+                                      uint16_t *pdst, bool to_lds) {
+  u32x4 kv;
+  uint32_t pv[2] = {0u, 0u};
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = i0 + u;
+    uint32_t key = 0u, pos = 0u;
+    if (i < ntot) {
+      const uint2 it = cand_of(i);
+      key = f2key(__uint_as_float(it.x));
+      pos = it.y;
+    }
+    kv[u] = key;
+    pv[u >> 1] |= pos << (16 * (u & 1));
+  }
+  const unsigned long long pp = (unsigned long long)pv[0] | ((unsigned long long)pv[1] << 32);
+  if (to_lds) {
+    *(u32x4 *)(kdst + i0) = kv;
+    *(unsigned long long *)(pdst + i0) = pp;
+  } else {
+    __builtin_nontemporal_store(kv, (u32x4 *)(kdst + i0));
+    __builtin_nontemporal_store(pp, (unsigned long long *)(pdst + i0));
+  }
+}
 
 // bfloat16 caches.  The loop body issues a fixed set of loads every step
 // (tile indices past the end are clamped to the last tile, whose keys the
@@ -376,35 +491,18 @@ constexpr int kLabelDepth = 8;  // 64-key label tiles in flight per wave (8 KB)
 constexpr int kLabelPageBase = 0;
 static_assert(kLabelPageBase + kLabelWaveKeysMax / kTile <= 1024, "label page ids fit the tile area");
 
+// One unit: sequence b, chunk `chunk`, KV head g0 (QUAD: heads g0 .. g0+3,
+// one per wave).  ob: the outbox, or null to store the blocks in HBM.
+// Every thread of the block must call it (it has barriers).
 // NR: rows per wave held in registers by the label path (a power of two
 // >= the group's rows; 0 for key rows).
 template <bool PAGED, bool GRP, bool QUAD, bool LABEL, int NR>
-__global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
+__device__ __forceinline__ void stream_unit(const Params &p, const Work &w, int b, int g0,
+                                            int chunk, StreamLds &sl, Outbox *ob) {
   static_assert(PAGED || !QUAD, "head quads are for the paged layout");
-  __shared__ WaveLds wlds[kWaves];
-  __shared__ int seg_n[kWaves * kMaxGroup];            // [row][wave] candidates found
-  __shared__ int seg_off[kWaves * (kMaxGroup + 1)];    // their offsets in the block(s)
   const int wk = w.wave_keys;
   const int wv = wave_id();
-  // Dispatch order (consecutive workgroups run together): in the paged
-  // layout the KV heads of a page block are adjacent in memory, so heads go
-  // fastest; in the contiguous layout a head's slab is swept chunk by chunk.
-  const int wid = (int)blockIdx.x;
-  int chunk, g, b;
-  if (QUAD) {
-    const int nq = p.Hkv / kWaves;
-    chunk = (wid / nq) % w.nchunk;
-    b = wid / (nq * w.nchunk);
-    g = kWaves * (wid % nq) + wv;
-  } else if (PAGED) {
-    g = wid % p.Hkv;
-    chunk = (wid / p.Hkv) % w.nchunk;
-    b = wid / (p.Hkv * w.nchunk);
-  } else {
-    chunk = wid % w.nchunk;
-    g = (wid / w.nchunk) % p.Hkv;
-    b = wid / (w.nchunk * p.Hkv);
-  }
+  const int g = QUAD ? g0 + wv : g0;
   const int bg = b * p.Hkv + g;
   const int L = seq_len(p, b);
   const int64_t c0 = (int64_t)chunk * w.chunk_keys;
@@ -420,11 +518,10 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   const int64_t row0 = GRP ? (int64_t)b * p.R + g : (int64_t)b * p.R + (int64_t)g * p.G;
   const int nrows = GRP ? 1 : p.G;
   const int cap = kCandBuf / nrows;  // staging slots per row
-  WaveLds &wl = wlds[wv];
+  WaveLds &wl = sl.wave[wv];
   // Candidates found per row: lane group s counts rows 4s+r (wave-uniform
   // within the group); counting continues past cap to detect overflow.
   int cnt[4] = {0, 0, 0, 0};
-
   if (nvalid > 0) {  // wave-uniform
     QFrag qf;
     if constexpr (!LABEL) load_q_bf16(p, b, g, qf);
@@ -590,50 +687,63 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   }
   if constexpr (QUAD) {
     // This wave's block: its rows one after another, each in position order.
-    int *off = seg_off + wv * (kMaxGroup + 1);
+    int *off = sl.seg_off + wv * (kMaxGroup + 1);
     if (col == 0) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int h = 4 * s + r;
-        if (h < nrows) seg_n[wv * kMaxGroup + h] = cnt[r];
+        if (h < nrows) sl.seg_n[wv * kMaxGroup + h] = cnt[r];
       }
     }
     __builtin_amdgcn_wave_barrier();  // counts were written by other lanes
-    const int n = l < nrows ? seg_n[wv * kMaxGroup + l] : 0;
+    const int n = l < nrows ? sl.seg_n[wv * kMaxGroup + l] : 0;
     const int nc = n < cap ? n : cap;
     const int inc = wave_incl_scan(nc);
     if (l < nrows)
       w.dir[(row0 + l) * w.nchunk + chunk] = make_int2(inc - nc, n > cap ? -1 : nc);
     if (l <= kMaxGroup) off[l] = inc - nc;  // rows >= nrows: the total
     const int ntot = __shfl(inc, 63);
-    __builtin_amdgcn_wave_barrier();  // offsets are read by every lane
+    if (l == 0) sl.wave_tot[wv] = ntot;
     const int64_t blk = ((int64_t)bg * w.nchunk + chunk) * w.blk_cap;
     uint32_t *kdst = w.ckey + blk;
     uint16_t *pdst = w.cpos + blk;
+    int base = 0, before = 0, all = 0;
+    if (ob) {
+      __syncthreads();  // every wave's block size
+#pragma unroll
+      for (int v = 0; v < kWaves; ++v) {
+        const int t = (sl.wave_tot[v] + 3) & ~3;
+        before += v < wv ? t : 0;
+        all += t;
+      }
+      base = outbox_reserve(w, *ob, all, kWaves);
+      kdst = ob->obk + base + before;
+      pdst = ob->obp + base + before;
+    } else {
+      __builtin_amdgcn_wave_barrier();  // offsets are read by every lane
+    }
     for (int i0 = 4 * l; i0 < ntot; i0 += 4 * 64) {
       // Row of item i0: the last t with off[t] <= i0.
       int t = 0;
 #pragma unroll
       for (int step = 8; step > 0; step >>= 1)
         if (off[t + step] <= i0) t += step;
-      u32x4 kv;
-      uint32_t pv[2] = {0u, 0u};
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = i0 + u;
-        uint32_t key = 0u, pos = 0u;
-        if (i < ntot) {
-          while (off[t + 1] <= i) ++t;  // stops at t = 15: off[16] = ntot > i
-          const uint2 it = wl.cand[t * cap + (i - off[t])];
-          key = f2key(__uint_as_float(it.x));
-          pos = it.y;
-        }
-        kv[u] = key;
-        pv[u >> 1] |= pos << (16 * (u & 1));
+      pack4(i0, ntot, [&](int i) {
+        while (off[t + 1] <= i) ++t;  // stops at t = 15: off[16] = ntot > i
+        return wl.cand[t * cap + (i - off[t])];
+      }, kdst, pdst, ob != nullptr);
+    }
+    if (ob) {
+      if (l == 0) {
+        ob->dst[ob->nb + wv] = blk;
+        ob->off[ob->nb + wv] = base + before;
+        ob->cnt[ob->nb + wv] = ntot;
       }
-      __builtin_nontemporal_store(kv, (u32x4 *)(kdst + i0));
-      __builtin_nontemporal_store((unsigned long long)pv[0] | ((unsigned long long)pv[1] << 32),
-                                  (unsigned long long *)(pdst + i0));
+      __syncthreads();  // every wave has read nb
+      if (threadIdx.x == 0) {
+        ob->nb += kWaves;
+        ob->n = base + all;
+      }
     }
     return;
   }
@@ -641,7 +751,7 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int h = 4 * s + r;
-      if (h < nrows) seg_n[h * kWaves + wv] = cnt[r];
+      if (h < nrows) sl.seg_n[h * kWaves + wv] = cnt[r];
     }
   }
   __syncthreads();
@@ -650,13 +760,13 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
   const int tid = threadIdx.x;
   if (tid < 64) {
     const int h = tid / kWaves;
-    const int n = h < nrows ? seg_n[tid] : 0;
+    const int n = h < nrows ? sl.seg_n[tid] : 0;
     const int nc = n < cap ? n : cap;
     const int inc = wave_incl_scan(nc);
     const int row_end = __shfl(inc, (tid | (kWaves - 1)));
     const uint64_t over = __ballot(n > cap);
-    seg_off[tid] = inc - nc;
-    if (tid == 63) seg_off[64] = inc;
+    sl.seg_off[tid] = inc - nc;
+    if (tid == 63) sl.seg_off[64] = inc;
     if (tid % kWaves == 0 && h < nrows) {
       const int start = inc - nc;
       const bool ovf = ((over >> tid) & ((1ull << kWaves) - 1ull)) != 0;
@@ -664,36 +774,102 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
     }
   }
   __syncthreads();
-  const int ntot = seg_off[64];
+  const int ntot = sl.seg_off[64];
   const int64_t blk = ((int64_t)bg * w.nchunk + chunk) * w.blk_cap;
   uint32_t *kdst = w.ckey + blk;
   uint16_t *pdst = w.cpos + blk;
+  int base = 0;
+  if (ob) {
+    base = outbox_reserve(w, *ob, (ntot + 3) & ~3, 1);
+    kdst = ob->obk + base;
+    pdst = ob->obp + base;
+  }
   for (int i0 = 4 * tid; i0 < ntot; i0 += 4 * kBlock) {
     // Segment of item i0: the last t with seg_off[t] <= i0.
     int t = 0;
 #pragma unroll
     for (int step = 32; step > 0; step >>= 1)
-      if (seg_off[t + step] <= i0) t += step;
-    u32x4 kv;
-    uint32_t pv[2] = {0u, 0u};
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u;
-      uint32_t key = 0u, pos = 0u;
-      if (i < ntot) {
-        while (seg_off[t + 1] <= i) ++t;  // stops at t = 63: seg_off[64] = ntot > i
-        const int h = t / kWaves, v = t % kWaves;
-        const uint2 it = wlds[v].cand[h * cap + (i - seg_off[t])];
-        key = f2key(__uint_as_float(it.x));
-        pos = (uint32_t)(v * wk) + it.y;
-      }
-      kv[u] = key;
-      pv[u >> 1] |= pos << (16 * (u & 1));
-    }
-    __builtin_nontemporal_store(kv, (u32x4 *)(kdst + i0));
-    __builtin_nontemporal_store((unsigned long long)pv[0] | ((unsigned long long)pv[1] << 32),
-                                (unsigned long long *)(pdst + i0));
+      if (sl.seg_off[t + step] <= i0) t += step;
+    pack4(i0, ntot, [&](int i) {
+      while (sl.seg_off[t + 1] <= i) ++t;  // stops at t = 63: seg_off[64] = ntot > i
+      const int h = t / kWaves, v = t % kWaves;
+      const uint2 it = sl.wave[v].cand[h * cap + (i - sl.seg_off[t])];
+      return make_uint2(it.x, (uint32_t)(v * wk) + it.y);
+    }, kdst, pdst, ob != nullptr);
   }
+  if (ob && tid == 0) {
+    ob->dst[ob->nb] = blk;
+    ob->off[ob->nb] = base;
+    ob->cnt[ob->nb] = ntot;
+    ob->nb += 1;
+    ob->n = base + ((ntot + 3) & ~3);
+  }
+}
+
+template <bool PAGED, bool GRP, bool QUAD, bool LABEL, int NR>
+__global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
+  __shared__ StreamLds sl;
+  if (!w.persistent) {
+    // One unit per workgroup, empty chunks included.  Dispatch order
+    // (consecutive workgroups run together): in the paged layout the KV
+    // heads of a page block are adjacent in memory, so heads go fastest; in
+    // the contiguous layout a head's slab is swept chunk by chunk.
+    const int wid = (int)blockIdx.x;
+    int chunk, g0, b;
+    if (QUAD) {
+      const int nq = p.Hkv / kWaves;
+      chunk = (wid / nq) % w.nchunk;
+      b = wid / (nq * w.nchunk);
+      g0 = kWaves * (wid % nq);
+    } else if (PAGED) {
+      g0 = wid % p.Hkv;
+      chunk = (wid / p.Hkv) % w.nchunk;
+      b = wid / (p.Hkv * w.nchunk);
+    } else {
+      chunk = wid % w.nchunk;
+      g0 = (wid / w.nchunk) % p.Hkv;
+      b = wid / (w.nchunk * p.Hkv);
+    }
+    stream_unit<PAGED, GRP, QUAD, LABEL, NR>(p, w, b, g0, chunk, sl, nullptr);
+    return;
+  }
+  // Persistent: units from the queue, in the work list's order (sequence by
+  // sequence; within one, the same order as the static grid's).
+  extern __shared__ u32x4 stream_dyn[];
+  Outbox *ob = (Outbox *)stream_dyn;
+  static_assert(sizeof(Outbox) % 16 == 0, "outbox arrays stay 16-byte aligned");
+  if (threadIdx.x == 0) {
+    ob->obk = (uint32_t *)(ob + 1);
+    ob->obp = (uint16_t *)(ob->obk + kOutboxCap);
+    ob->n = 0;
+    ob->nb = 0;
+  }
+  const int total = w.unit_pre[p.B];
+  int b = 0;
+  for (;;) {
+    if (threadIdx.x == 0) sl.unit = atomicAdd(w.queue, 1);
+    __syncthreads();  // the unit, and (first pass) the outbox state
+    const int u = sl.unit;
+    if (u >= total) break;  // uniform
+    while (u >= w.unit_pre[b + 1]) ++b;
+    const int r = u - w.unit_pre[b];
+    int chunk, g0;
+    if (QUAD) {
+      const int nq = p.Hkv / kWaves;
+      chunk = r / nq;
+      g0 = kWaves * (r % nq);
+    } else if (PAGED) {
+      chunk = r / p.Hkv;
+      g0 = r % p.Hkv;
+    } else {
+      const int nch = (seq_len(p, b) + w.chunk_keys - 1) / w.chunk_keys;
+      g0 = r / nch;
+      chunk = r % nch;
+    }
+    stream_unit<PAGED, GRP, QUAD, LABEL, NR>(p, w, b, g0, chunk, sl, ob);
+    __syncthreads();  // LDS areas and outbox state are reused by the next unit
+  }
+  outbox_flush(w, *ob);
 }
 
 // ---------------------------------------------------------------------------
@@ -1318,14 +1494,18 @@ struct RowRaw {
   u32x4 v[BF16 ? 1 : 2];  // this lane's 8 channels of one value row
 };
 
+// Gathered rows are read once: nontemporal loads.  (Measured at the 128K
+// batch-16 workload: right after a 1 GiB buffer had been written, the
+// gather with plain loads took 0.117 ms instead of 0.061 ms, paying for the
+// write's cached lines it evicted; with nontemporal loads it took 0.062.)
 template <bool BF16>
 __device__ __forceinline__ void load_raw(const void *base, int64_t off, int col, RowRaw<BF16> &r) {
   if constexpr (BF16) {
-    r.v[0] = *(const u32x4 *)((const uint16_t *)base + off + 8 * col);
+    r.v[0] = __builtin_nontemporal_load((const u32x4 *)((const uint16_t *)base + off + 8 * col));
   } else {
     const u32x4 *q = (const u32x4 *)((const float *)base + off + 8 * col);
-    r.v[0] = q[0];
-    r.v[1] = q[1];
+    r.v[0] = __builtin_nontemporal_load(q);
+    r.v[1] = __builtin_nontemporal_load(q + 1);
   }
 }
 
@@ -1763,18 +1943,20 @@ hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
 
 // Launch with start/stop events attached to the kernel's own dispatch (no
 // extra packets on the stream), or a plain launch when they are null.
-static hipError_t launch_with_events(void (*kern)(Params, Work), dim3 grid, const Params &p,
-                                     const Work &w, hipStream_t st, hipEvent_t t0,
-                                     hipEvent_t t1) {
+static hipError_t launch_with_events(void (*kern)(Params, Work), dim3 grid, size_t lds,
+                                     const Params &p, const Work &w, hipStream_t st,
+                                     hipEvent_t t0, hipEvent_t t1) {
   if (!t0) {
-    kern<<<grid, kBlock, 0, st>>>(p, w);
+    kern<<<grid, kBlock, lds, st>>>(p, w);
     return hipGetLastError();
   }
   Params pa = p;
   Work wa = w;
   void *args[] = {&pa, &wa};
-  return hipExtLaunchKernel((const void *)kern, grid, dim3(kBlock), args, 0, st, t0, t1, 0);
+  return hipExtLaunchKernel((const void *)kern, grid, dim3(kBlock), args, lds, st, t0, t1, 0);
 }
+
+size_t stream_outbox_bytes() { return sizeof(Outbox) + (size_t)kOutboxCap * 6; }
 
 bool stream_by_head_quads(const Work &w) { return w.chunk_keys == w.wave_keys; }
 
@@ -1809,7 +1991,10 @@ hipError_t launch_score_stream(const Params &p, const Work &w, hipStream_t st, h
     else kern = gs ? k_score_stream<false, true, false, false, 0> : k_score_stream<false, false, false, false, 0>;
     wgs = (int64_t)w.nchunk * p.B * p.Hkv;
   }
-  return launch_with_events(kern, dim3((unsigned)wgs), p, w, st, t0, t1);
+  if (!w.persistent) return launch_with_events(kern, dim3((unsigned)wgs), 0, p, w, st, t0, t1);
+  // One workgroup per compute unit (w.stream_wgs), or one per unit of work.
+  const int64_t grid = wgs < w.stream_wgs ? wgs : w.stream_wgs;
+  return launch_with_events(kern, dim3((unsigned)grid), stream_outbox_bytes(), p, w, st, t0, t1);
 }
 
 size_t select_lds_bytes(int nchunk, int lds_cap) {
