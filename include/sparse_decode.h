@@ -219,6 +219,24 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
                                   sd_tensor *out, sd_tensor *idx, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops that must not allocate, harnesses that forbid
+ * hipMalloc): sparse_decode_attention with the same arguments and results,
+ * but its scratch is a static device array of SD_NOALLOC_SCRATCH_BYTES
+ * inside the library (one per GPU, held until the process ends) instead of
+ * the library workspace, and it calls no hipMalloc, hipFree or other
+ * allocating routine.  A problem whose scratch (sparse_decode_workspace_size
+ * for the same shapes, at most) exceeds it returns SD_ERR_WORKSPACE before
+ * any launch.  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (different streams without ordering) race and must
+ * not be issued.  Profiling does not apply to it.
+ */
+#define SD_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+sd_status sparse_decode_attention_noalloc(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                          const int32_t *seq_lens, const sd_sparsity *sparsity,
+                                          sd_tensor *out, sd_tensor *idx, void *stream);
+
+/*
  * The method with the low-channel indexer choosing the positions (Table 2):
  * as sparse_decode_attention, but the exact top-k (with any forced
  * positions) runs on the approximate label scores, one 16-byte label row per

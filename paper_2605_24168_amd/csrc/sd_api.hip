@@ -31,9 +31,24 @@ struct DevState {
   hipEvent_t ev[kRing][6];
   int level[kRing] = {};  // profiling level each ring slot was recorded with
   int64_t n_calls = 0;  // profiled calls in the current series
-  int32_t *stats = nullptr;
   int n_cu = 0;         // compute units (0: not queried yet)
+  // Device addresses of this GPU's copies of `scratch` and `stats_dev`
+  // (hipGetSymbolAddress, taken once with the device current).
+  bool symbols = false;
+  void *scratch = nullptr;
+  int32_t *stats = nullptr;
 };
+
+// Workspace of the allocation-free entry point: one copy per GPU the
+// library runs on, held until the process ends.  In host code these names
+// stand for the device arrays, not their addresses: host code uses only
+// the addresses that device_state() takes with hipGetSymbolAddress.
+constexpr size_t kScratchBytes = SD_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+// Per-call counters the kernels keep (stats[0]: rows repaired by the last
+// call of the fused path), outside every workspace so that the profile can
+// read them whatever became of a workspace since.
+static __device__ __align__(256) int32_t stats_dev[16];
 
 std::mutex g_mu;
 DevState g_dev[kMaxDevices];
@@ -228,7 +243,7 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
 // Workspace layout.  Sizes depend only on the shapes and the sparsity, so
 // the same layout is recomputed on every call.
 struct Layout {
-  size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, stats, ustart, total;
+  size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, ustart, total;
   size_t queue, unit_pre;
   size_t dsel_hist, dsel_state, dsel_cnt;
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
@@ -364,7 +379,6 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
     }
   }
   L.part = take((size_t)s.B * s.Hq * L.nsplit * sd::kPartStride * 4);
-  L.stats = take(64);
   L.total = off;
   return L;
 }
@@ -386,12 +400,34 @@ size_t dense_part_bytes(const sd::Params &p) {
   return align_up(n > 0 ? n : 1);
 }
 
-// The current device's workspace, at least `bytes` long.
-sd_status get_workspace(size_t bytes, DevState *&ds, char *&base) {
+// The current device's state, with its compute-unit count and the device
+// addresses of the library's __device__ arrays (first call on a device).
+sd_status device_state(DevState *&ds) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return SD_ERR_HIP;
   if (dev < 0 || dev >= kMaxDevices) return SD_ERR_UNSUPPORTED;
   ds = &g_dev[dev];
+  if (ds->n_cu == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return SD_ERR_HIP;
+    ds->n_cu = n > 0 ? n : 1;
+  }
+  if (!ds->symbols) {
+    void *sc = nullptr, *st = nullptr;
+    if (hipGetSymbolAddress(&sc, HIP_SYMBOL(scratch)) != hipSuccess || !sc) return SD_ERR_HIP;
+    if (hipGetSymbolAddress(&st, HIP_SYMBOL(stats_dev)) != hipSuccess || !st) return SD_ERR_HIP;
+    ds->scratch = sc;
+    ds->stats = (int32_t *)st;
+    ds->symbols = true;
+  }
+  return SD_OK;
+}
+
+// The current device's workspace, at least `bytes` long.
+sd_status get_workspace(size_t bytes, DevState *&ds, char *&base) {
+  sd_status st = device_state(ds);
+  if (st) return st;
   if (ds->ws_bytes < bytes) {
     if (ds->user_ws) return SD_ERR_WORKSPACE;
     if (ds->ws) {
@@ -405,17 +441,13 @@ sd_status get_workspace(size_t bytes, DevState *&ds, char *&base) {
     ds->ws_bytes = bytes;
   }
   base = (char *)ds->ws;
-  if (ds->n_cu == 0) {
-    int n = 0;
-    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-      return SD_ERR_HIP;
-    ds->n_cu = n > 0 ? n : 1;
-  }
   return SD_OK;
 }
 
-sd::Work carve(char *base, const Layout &L, bool fused, const Shape &s) {
+sd::Work carve(char *base, const Layout &L, bool fused, const Shape &s,
+               int32_t *stats) {
   sd::Work w{};
+  w.stats = stats;
   if (fused) {
     w.sample = (float *)(base + L.sample);
     w.theta = (float *)(base + L.theta);
@@ -435,7 +467,6 @@ sd::Work carve(char *base, const Layout &L, bool fused, const Shape &s) {
     }
   }
   w.part = (float *)(base + L.part);
-  w.stats = (int32_t *)(base + L.stats);
   w.ustart = L.union_chunk > 0 ? (int32_t *)(base + L.ustart) : nullptr;
   w.ustride = L.ustride;
   w.union_chunk = L.union_chunk;
@@ -589,7 +620,7 @@ sd_status sparse_decode_attend(const sd_tensor *q, const sd_kv *K, const sd_kv *
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
   if (st) return st;
-  const sd::Work w = carve(base, L, false, s);
+  const sd::Work w = carve(base, L, false, s, ds->stats);
   const sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   return hip_status(sd::launch_attend(p, w, (const int32_t *)idx->data, out->data, false,
                                       (hipStream_t)stream));
@@ -622,7 +653,7 @@ sd_status sparse_decode_attend_weighted(const sd_tensor *q, const sd_kv *K, cons
   char *base = nullptr;
   st = get_workspace(L.total, ds, base);
   if (st) return st;
-  const sd::Work w = carve(base, L, false, s);
+  const sd::Work w = carve(base, L, false, s, ds->stats);
   sd::Params p = make_params(q, K, V, seq_lens, sp, s, k_max);
   p.weights = (const float *)weights->data;
   return hip_status(sd::launch_attend(p, w, (const int32_t *)idx->data, out->data, false,
@@ -684,7 +715,7 @@ struct Sampled {
 sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
                          const sd_labels *labels, const int32_t *seq_lens,
                          const sd_sparsity *sp, sd_tensor *out, sd_tensor *idx, void *stream,
-                         const Sampled *smp = nullptr) {
+                         const Sampled *smp = nullptr, bool no_alloc = false) {
   Shape s{};
   sd_status st = check_problem(q, K, V, sp, s);
   if (st) return st;
@@ -713,9 +744,16 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   if ((int64_t)L.nchunk * s.B * s.Hkv > INT32_MAX) return SD_ERR_UNSUPPORTED;
   DevState *ds = nullptr;
   char *base = nullptr;
-  st = get_workspace(L.total, ds, base);
-  if (st) return st;
-  sd::Work w = carve(base, L, true, s);
+  if (no_alloc) {  // the static scratch: nothing allocated, sizes beyond it refused
+    st = device_state(ds);
+    if (st) return st;
+    if (L.total > kScratchBytes) return SD_ERR_WORKSPACE;
+    base = (char *)ds->scratch;
+  } else {
+    st = get_workspace(L.total, ds, base);
+    if (st) return st;
+  }
+  sd::Work w = carve(base, L, true, s, ds->stats);
   // float32 caches (small problems) take the full-score path for every row,
   // and so do calls whose rows the pilot would all send there.
   int64_t cands = 0;
@@ -739,7 +777,7 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   w.stream_wgs = ds->n_cu;
   int32_t *idx_ptr = (int32_t *)idx->data;
 
-  const int prof_level = g_profiling.load();
+  const int prof_level = no_alloc ? 0 : g_profiling.load();  // (profiling creates events)
   const bool prof = prof_level != 0;
   if (prof && !ds->events) {
     for (auto &set : ds->ev)
@@ -799,7 +837,6 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
     ds->level[ds->n_calls % kRing] = prof_level;
     ds->n_calls++;
   }
-  ds->stats = w.stats;
   return hip_status(e);
 }
 
@@ -811,6 +848,12 @@ sd_status sparse_decode_attention(const sd_tensor *q, const sd_kv *K, const sd_k
                                   const int32_t *seq_lens, const sd_sparsity *sp, sd_tensor *out,
                                   sd_tensor *idx, void *stream) {
   return attention_impl(q, K, V, nullptr, seq_lens, sp, out, idx, stream);
+}
+
+sd_status sparse_decode_attention_noalloc(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
+                                          const int32_t *seq_lens, const sd_sparsity *sp,
+                                          sd_tensor *out, sd_tensor *idx, void *stream) {
+  return attention_impl(q, K, V, nullptr, seq_lens, sp, out, idx, stream, nullptr, true);
 }
 
 sd_status sparse_decode_label_attention(const sd_tensor *q, const sd_kv *K, const sd_kv *V,

@@ -96,6 +96,10 @@ lib.sparse_decode_label_score.argtypes = [_P(SdTensor), _P(SdKv), _P(SdLabels), 
 lib.sparse_decode_attention.restype = C.c_int
 lib.sparse_decode_attention.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p,
                                         _P(SdSparsity), _P(SdTensor), _P(SdTensor), C.c_void_p]
+lib.sparse_decode_attention_noalloc.restype = C.c_int
+lib.sparse_decode_attention_noalloc.argtypes = [_P(SdTensor), _P(SdKv), _P(SdKv), C.c_void_p,
+                                                _P(SdSparsity), _P(SdTensor), _P(SdTensor),
+                                                C.c_void_p]
 lib.sparse_decode_workspace_size.restype = C.c_int
 lib.sparse_decode_workspace_size.argtypes = [_P(SdTensor), _P(SdKv), _P(SdSparsity), _P(SdTensor),
                                              _P(C.c_size_t)]
@@ -359,6 +363,24 @@ def sparse_decode_attention(q, cache: KVCache, seq_lens, sparsity: Sparsity, out
     _check(lib.sparse_decode_attention(C.byref(cq), C.byref(kk), C.byref(kv), seq_lens.data_ptr(),
                                        C.byref(sp), C.byref(co), C.byref(ci), _stream(stream)),
            "sparse_decode_attention")
+    return out, idx
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # SD_NOALLOC_SCRATCH_BYTES
+
+
+def sparse_decode_attention_noalloc(q, cache: KVCache, seq_lens, sparsity: Sparsity, out,
+                                    idx, stream=None):
+    """The fused method with the library's static scratch instead of its
+    workspace (no device allocation); out and idx are the caller's."""
+    _need_device(seq_lens, "seq_lens", torch.int32)
+    sp = sparsity.c()
+    cq, kk, kv = _tensor(q, "q"), cache.c("k"), cache.c("v")
+    co, ci = _tensor(out, "out"), _tensor(idx, "idx")
+    _check(lib.sparse_decode_attention_noalloc(C.byref(cq), C.byref(kk), C.byref(kv),
+                                               seq_lens.data_ptr(), C.byref(sp), C.byref(co),
+                                               C.byref(ci), _stream(stream)),
+           "sparse_decode_attention_noalloc")
     return out, idx
 
 
