@@ -370,13 +370,6 @@ def default_scale(d: int) -> float:
 # draw i of a row is a uint32 u, and it picks the floor(u |C| / 2^32)-th
 # position of C in ascending order.
 # ---------------------------------------------------------------------------
-def complement_position(kept: np.ndarray, L: int, rank: int) -> int:
-    """The rank-th (0-based) position of [0, L) outside the ascending set
-    ``kept``: by enumeration."""
-    rest = np.setdiff1d(np.arange(L, dtype=np.int64), np.asarray(kept, dtype=np.int64))
-    return int(rest[rank])
-
-
 def sampled_lists(idx: np.ndarray, seq_lens, draws: np.ndarray):
     """Index lists and weights of the sampled selection, from the exact
     selection's lists idx [B, R, k_max] (ascending, -1 padded) and the draws

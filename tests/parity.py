@@ -5,9 +5,9 @@ largest selection score (float64) and band = {j : |s_j - tau| <= 1e-3 *
 max(1, |tau|)}, the GPU set minus the band must equal the oracle set minus
 the band; swaps inside the band are counted, not failed.
 
-Outputs: float32 caches must match within 1e-4 of the row's largest output
-magnitude (max_i |gpu_i - ref_i| <= 1e-4 * max_i |ref_i|); bfloat16 within
-2e-2 absolute.  When the band swapped positions, the reference output is the
+Outputs: float32 caches must match element by element within 1e-4 relative,
+|gpu_i - ref_i| <= 1e-4 |ref_i| + 1e-6 (the absolute floor covers elements
+near zero); bfloat16 within 2e-2 absolute.  When the band swapped positions, the reference output is the
 oracle's attention over the GPU's own index set, so that a legitimate swap
 does not count as an output error.
 """
@@ -23,6 +23,7 @@ from oracle import oracle as O
 
 BAND_REL = 1e-3
 F32_OUT_REL = 1e-4
+F32_OUT_ABS = 1e-6
 BF16_OUT_ABS = 2e-2
 
 
@@ -80,14 +81,13 @@ def check_idx_rows(gpu_idx: np.ndarray, ora_idx: np.ndarray, ora_scores: np.ndar
 
 
 def out_errors(gpu_out: np.ndarray, ref_out: np.ndarray, dtype: str):
-    """Return (ok, worst_ratio, rel_l2): worst_ratio = max over rows of the error
-    divided by its allowance (<= 1 passes)."""
+    """Return (ok, worst_ratio, rel_l2): worst_ratio = max over elements of the
+    error divided by its allowance (<= 1 passes)."""
     g = gpu_out.astype(np.float64)
     r = ref_out.astype(np.float64)
     err = np.abs(g - r)
     if dtype == "f32":
-        allow = F32_OUT_REL * np.abs(r).max(axis=-1, keepdims=True)
-        allow = np.maximum(allow, 1e-30)
+        allow = F32_OUT_REL * np.abs(r) + F32_OUT_ABS
     else:
         allow = np.full_like(err, BF16_OUT_ABS)
     ratio = float((err / allow).max()) if err.size else 0.0

@@ -500,13 +500,15 @@ def test_invalid_arguments_are_rejected_before_launch(sd):
 
 
 # ---------------------------------------------------------------------------
-# Full-size workloads, as the benchmark runs them, on sampled sequences.
+# Full-size workloads, as the benchmark runs them: every sequence of the
+# 128K batch and of the ragged paged batch, a sampled one of the others.
 # ---------------------------------------------------------------------------
 
 slice_batch = P.slice_batch
 
 
-@pytest.mark.parametrize("cfg,sample", [(1, [0]), (2, [1]), (3, [0, 15]), (4, [3, 17]), (5, [0])])
+@pytest.mark.parametrize("cfg,sample", [(1, [0]), (2, [1]), (3, list(range(16))),
+                                        (4, list(range(32))), (5, [0])])
 def test_full_size_workloads_on_sampled_sequences(sd, cfg, sample):
     P.log(f"  generating workload {cfg} at full size")
     inp = synth.make_inputs(cfg, seed=0)
