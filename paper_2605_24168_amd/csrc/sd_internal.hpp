@@ -347,10 +347,16 @@ __device__ __forceinline__ f32x4 mfma_scores(const QFrag &qf, const KFrag &kf) {
 // Label scores (the low-channel indexer).  A key's label row is kLabels
 // bf16 channels, 16 bytes.  Every path computes a key's approximate score
 // the same way, so the stream, the fallback and the stand-alone scores agree
-// bit for bit: a fused multiply-add chain over the channels in order
-// (products of bf16 values are exact in float32).  In group-shared mode the
-// query side is first summed over the group's heads (in head order).
+// bit for bit.  Per-head rows: the query's label channels are bf16 values
+// too, so the score is four packed bf16 dot products (v_dot2c_f32_bf16:
+// two channel products added to a float32 accumulator, channel pairs in
+// order) straight from the label row's 32-bit words.  Group-shared rows:
+// the query side is first summed over the group's heads (in head order, in
+// float32), then a fused multiply-add chain over the channels in order
+// (products of bf16 values are exact in float32).
 // ---------------------------------------------------------------------------
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+
 __device__ __forceinline__ u32x4 load_labels(const uint16_t *base, int64_t off) {
   return __builtin_nontemporal_load((const u32x4 *)(base + off));
 }
@@ -367,6 +373,21 @@ __device__ __forceinline__ float label_dot(const float *ql, const float lab[kLab
   float s = 0.f;
 #pragma unroll
   for (int c = 0; c < kLabels; ++c) s = fmaf(ql[c], lab[c], s);
+  return s;
+}
+
+// Per-head rows: qp[e] holds the query's label channels 2e and 2e+1 as a
+// bf16 pair (channel 2e in the low half, as in the label row).
+// (Each word is copied to a scalar before the bit cast: a bit cast of a
+// vector element subscript compiled here to a read of element 0 only.)
+__device__ __forceinline__ float label_dot_packed(const uint32_t qp[4], u32x4 raw) {
+  float s = 0.f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t qw = qp[e], lw = raw[e];
+    s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, qw),
+                                        __builtin_bit_cast(bf16x2, lw), s, false);
+  }
   return s;
 }
 
@@ -389,32 +410,56 @@ __device__ __forceinline__ void q_label_row(const Params &p, int b, int g, int h
   }
 }
 
+// The same for a per-head row (h >= 0) as bf16 pairs (label_dot_packed).
+__device__ __forceinline__ void q_label_row_packed(const Params &p, int b, int g, int h,
+                                                   uint32_t qp[4]) {
+  const int32_t *ch = p.channels + (int64_t)g * kLabels;
+  const uint16_t *qh = (const uint16_t *)p.q + ((int64_t)b * p.Hq + (int64_t)g * p.G + h) * kHeadDim;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    int c0 = ch[2 * e], c1 = ch[2 * e + 1];
+    c0 = c0 < 0 ? 0 : (c0 >= kHeadDim ? kHeadDim - 1 : c0);
+    c1 = c1 < 0 ? 0 : (c1 >= kHeadDim ? kHeadDim - 1 : c1);
+    qp[e] = (uint32_t)qh[c0] | ((uint32_t)qh[c1] << 16);
+  }
+}
+
 // Label scores in the MFMA result layout (for the pilot and the full-score
 // paths): lane (s, col) holds rows 4s+r of its key col.  Rows beyond G are
 // zero; in group-shared mode row 0 of lane group 0 holds the group's score
 // and every other row is zero, so group_sum returns it unchanged.
 struct LabelRows {
-  float ql[4][kLabels];
+  float ql[4][kLabels];  // group-shared rows
+  uint32_t qp[4][4];     // per-head rows (label_dot_packed); zero beyond G
+  int packed;
   __device__ __forceinline__ void init(const Params &p, int b, int g) {
     const int s = lane_id() >> 4;
+    packed = !p.group_shared;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int h = 4 * s + r;
-      const bool use = p.group_shared ? (s == 0 && r == 0) : h < p.G;
-      if (use) {
-        q_label_row(p, b, g, p.group_shared ? -1 : h, ql[r]);
-      } else {
 #pragma unroll
-        for (int c = 0; c < kLabels; ++c) ql[r][c] = 0.f;
+      for (int e = 0; e < 4; ++e) qp[r][e] = 0u;
+#pragma unroll
+      for (int c = 0; c < kLabels; ++c) ql[r][c] = 0.f;
+      if (p.group_shared) {
+        if (s == 0 && r == 0) q_label_row(p, b, g, -1, ql[r]);
+      } else if (h < p.G) {
+        q_label_row_packed(p, b, g, h, qp[r]);
       }
     }
   }
   __device__ __forceinline__ f32x4 score(u32x4 raw) const {
-    float lab[kLabels];
-    unpack_labels(raw, lab);
     f32x4 acc;
+    if (packed) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[r] = label_dot(ql[r], lab);
+      for (int r = 0; r < 4; ++r) acc[r] = label_dot_packed(qp[r], raw);
+    } else {
+      float lab[kLabels];
+      unpack_labels(raw, lab);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[r] = label_dot(ql[r], lab);
+    }
     return acc;
   }
 };

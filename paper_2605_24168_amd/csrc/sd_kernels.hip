@@ -593,19 +593,26 @@ __device__ __forceinline__ void stream_unit(const Params &p, const Work &w, int 
       // The rows' query sides and thresholds in registers (rows past the
       // group's never pass).
       constexpr int NRr = NR > 0 ? NR : 1;
-      float qlr[NRr][kLabels], thr[NRr];
+      // Group-shared: the summed query side in float32; per-head rows: the
+      // query's label channels as bf16 pairs (label_dot_packed).
+      float qlr[GRP ? NRr : 1][kLabels], thr[NRr];
+      uint32_t qpr[GRP ? 1 : NRr][4];
       int cntr[NRr];
 #pragma unroll
       for (int h = 0; h < NRr; ++h) {
         cntr[h] = 0;
-        if (h < nrows) {
-          q_label_row(p, b, g, GRP ? -1 : h, qlr[h]);
-          thr[h] = w.theta[row0 + h];
-        } else {
+        if constexpr (GRP) {
+          if (h < nrows) q_label_row(p, b, g, -1, qlr[h]);
+          else
 #pragma unroll
-          for (int c = 0; c < kLabels; ++c) qlr[h][c] = 0.f;
-          thr[h] = __builtin_inff();
+            for (int c = 0; c < kLabels; ++c) qlr[h][c] = 0.f;
+        } else {
+          if (h < nrows) q_label_row_packed(p, b, g, h, qpr[h]);
+          else
+#pragma unroll
+            for (int e = 0; e < 4; ++e) qpr[h][e] = 0u;
         }
+        thr[h] = h < nrows ? w.theta[row0 + h] : __builtin_inff();
       }
       const int nt64 = (nvalid + 63) / 64;
       const int64_t lslab = (((int64_t)b * p.K.hkv + g) * p.K.ncap + w0) * kLabels;
@@ -627,14 +634,17 @@ __device__ __forceinline__ void stream_unit(const Params &p, const Work &w, int 
 #pragma unroll
         for (int u = 0; u < kLabelDepth; ++u) {
           const int ti = tb + u;
+          const u32x4 raw = lb[u];
           float lab[kLabels];
-          unpack_labels(lb[u], lab);
+          if constexpr (GRP) unpack_labels(raw, lab);
           lb[u] = lload(ti + kLabelDepth);
           const int jl = ti * 64 + l;
           const bool live = jl >= jlo && jl < jhi;
 #pragma unroll
           for (int h = 0; h < NRr; ++h) {
-            const float sc = label_dot(qlr[h], lab);
+            float sc;
+            if constexpr (GRP) sc = label_dot(qlr[h], lab);
+            else sc = label_dot_packed(qpr[h], raw);
             const bool pass = live && sc >= thr[h];
             const uint64_t m = __ballot(pass);
             if (m) {  // wave-uniform
@@ -1550,16 +1560,33 @@ __host__ __device__ inline bool attend_recompute(bool fused, const Params &p) {
   return !fused || p.group_shared || p.n_sink + p.n_local > 0 || p.labels != nullptr;
 }
 
-// Byte offsets of the dynamic LDS areas of k_attend (host and device agree).
+// Row index of position j of sequence b in a cache, 32 bits: j itself in
+// the contiguous layout, the pool row page * 16 + j % 16 in the paged one
+// (the block-table lookup done once); row_offset turns it into the element
+// offset of KV head g's row.
+__device__ __forceinline__ uint32_t kv_row(const KvView &kv, int b, int64_t j) {
+  if (!kv.paged) return (uint32_t)j;
+  const int64_t page = kv.block_table[(int64_t)b * kv.max_pages + (j >> 4)];
+  return (uint32_t)(page * kTile + (j & 15));
+}
+__device__ __forceinline__ int64_t row_offset(const KvView &kv, int b, int g, uint32_t r) {
+  if (!kv.paged) return (((int64_t)b * kv.hkv + g) * kv.ncap + r) * kHeadDim;
+  return ((int64_t)r * kv.hkv + g) * kHeadDim;
+}
+
+// Byte offsets of the dynamic LDS areas of k_attend (host and device agree):
+// per list entry its value row (and key row, when the logits are
+// recomputed) as 32-bit row indices, its weights, and its position where
+// entries can be skipped (recomputed logits) or are built (union).
 struct AttLds {
   int voff, koff, e, pos, hm, q, red, lred, total;
   __host__ __device__ AttLds(int split, int nh, bool recompute, bool uni = false) {
     const int nhb = nh < kAttHeads ? nh : kAttHeads;
     int o = 0;
-    voff = o; o += 8 * split;
-    koff = o; o += recompute ? 8 * split : 0;
+    voff = o; o += 4 * split;
+    koff = o; o += recompute ? 4 * split : 0;
     e = o; o += 4 * nh * split;
-    pos = o; o += 4 * split;
+    pos = o; o += (recompute || uni) ? 4 * split : 0;
     hm = o; o += uni ? 4 * split : 0;
     q = o; o += recompute ? 4 * nh * kHeadDim : 0;
     red = o; o += 4 * kWaves * nhb * kHeadDim;
@@ -1599,8 +1626,8 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   const bool recompute = UNI || attend_recompute(FUSED, p);
   const AttLds lay(split, nh, recompute, UNI);
   char *dyn = (char *)att_dyn;
-  int64_t *voff_l = (int64_t *)(dyn + lay.voff);
-  int64_t *koff_l = (int64_t *)(dyn + lay.koff);
+  uint32_t *voff_l = (uint32_t *)(dyn + lay.voff);  // value rows (kv_row)
+  uint32_t *koff_l = (uint32_t *)(dyn + lay.koff);  // key rows (recompute)
   float *e_l = (float *)(dyn + lay.e);
   int32_t *pos_l = (int32_t *)(dyn + lay.pos);
   uint32_t *hm_l = (uint32_t *)(dyn + lay.hm);  // UNI: each entry's head bits
@@ -1687,8 +1714,8 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     __syncthreads();
     for (int t = tid; t < n; t += kBlock) {
       const int64_t j = pos_l[t];
-      voff_l[t] = kv_offset(p.V, b, g, j);
-      koff_l[t] = kv_offset(p.K, b, g, j);
+      voff_l[t] = kv_row(p.V, b, j);
+      koff_l[t] = kv_row(p.K, b, j);
     }
   } else {
     // Resolve every entry to its row offsets once (page-table reads in
@@ -1697,10 +1724,10 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     for (int t = tid; t < n; t += kBlock) {
       int32_t j = irow[t];
       if (j < 0 || j >= L) j = -1;
-      pos_l[t] = j;
+      if (recompute) pos_l[t] = j;  // (fused lists hold only valid entries)
       const int64_t jc = j >= 0 ? j : 0;
-      voff_l[t] = kv_offset(p.V, b, g, jc);
-      if (recompute) koff_l[t] = kv_offset(p.K, b, g, jc);
+      voff_l[t] = kv_row(p.V, b, jc);
+      if (recompute) koff_l[t] = kv_row(p.K, b, jc);
     }
   }
   if (recompute && !BF16) {  // float32 queries for the vector-ALU logits
@@ -1729,7 +1756,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
     const int kcol = l & 15, quad = l >> 4;
     auto tile_off = [&](int ti) {
       const int t = ti * kTile + kcol;
-      return koff_l[t < n ? t : 0];
+      return row_offset(p.K, b, g, koff_l[t < n ? t : 0]);
     };
     for (int ti = wv; ti < ntile; ti += 2 * kWaves) {
       const int ti1 = ti + kWaves;
@@ -1763,7 +1790,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
         continue;
       }
       float kv[8];
-      load_row8<BF16>(p.K.base, koff_l[t], col, kv);
+      load_row8<BF16>(p.K.base, row_offset(p.K, b, g, koff_l[t]), col, kv);
       for (int h = 0; h < nh; ++h) {
         float d = 0.f;
 #pragma unroll
@@ -1833,7 +1860,7 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int t = tb + 4 * u + sub;
-        load_raw<BF16>(p.V.base, voff_l[t < n ? t : 0], col, buf[u]);
+        load_raw<BF16>(p.V.base, row_offset(p.V, b, g, voff_l[t < n ? t : 0]), col, buf[u]);
       }
     };
     auto consume = [&](int tb, const RowRaw<BF16> buf[U]) {
