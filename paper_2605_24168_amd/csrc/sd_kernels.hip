@@ -629,7 +629,6 @@ __device__ __forceinline__ void stream_unit(const Params &p, const Work &w, int 
       u32x4 lb[kLabelDepth];
 #pragma unroll
       for (int d = 0; d < kLabelDepth; ++d) lb[d] = lload(d);
-      const uint64_t below = (1ull << l) - 1ull;
       for (int tb = 0; tb < nlsteps; tb += kLabelDepth) {
 #pragma unroll
         for (int u = 0; u < kLabelDepth; ++u) {
@@ -645,13 +644,16 @@ __device__ __forceinline__ void stream_unit(const Params &p, const Work &w, int 
             float sc;
             if constexpr (GRP) sc = label_dot(qlr[h], lab);
             else sc = label_dot_packed(qpr[h], raw);
+            // In-order slot from the ballot's count of lower lanes; lanes that
+            // do not pass (or overflow the area) write their discard slot,
+            // so no branch or exec-mask change is needed.
             const bool pass = live && sc >= thr[h];
             const uint64_t m = __ballot(pass);
-            if (m) {  // wave-uniform
-              const int slot = cntr[h] + __popcll(m & below);
-              if (pass && slot < cap) wl.cand[h * cap + slot] = make_uint2(__float_as_uint(sc), (uint32_t)jl);
-              cntr[h] += __popcll(m);
-            }
+            const int slot = cntr[h] + (int)__builtin_amdgcn_mbcnt_hi(
+                (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+            const int e = (pass && slot < cap) ? h * cap + slot : kCandBuf + l;
+            wl.cand[e] = make_uint2(__float_as_uint(sc), (uint32_t)jl);
+            cntr[h] += __popcll(m);
           }
         }
       }
