@@ -789,11 +789,26 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   auto mark = [&](int i) -> hipError_t {
     return prof_level == 1 ? hipEventRecord(ev[i], stream_h) : hipSuccess;
   };
-  // Candidate keys the selection stages in LDS.  About 2.5 k are expected
-  // and the count varies by about 1/sqrt(r) (r >= 2.5 k m / L sample ranks,
-  // at least 50 at the budgets this serves), so 3.5 k + 1024 is more than
-  // five deviations of room; rows beyond it select from global memory.
-  const int64_t want = 7 * k_max / 2 + 1024;
+  // Candidate keys the selection stages in LDS: what a full-capacity row
+  // expects, f k (f the pilot's candidate factor: r n / (k m) for its rank
+  // r of m samples; 2.5 at 100x, 1.2 at 5x), plus three relative
+  // deviations of the count (about 1 / sqrt(r): the threshold is the r-th
+  // largest sample) and 256; rows beyond it select from global memory.
+  // Sized to the need, the selection fits four or more workgroups per
+  // compute unit where 3.5 k + 1024 keys fitted three (ragged paged batch
+  // of 8K-128K sequences at 50x: selection 60 -> 49 us).
+  double fcand = 2.5, rank = 50.0;
+  {
+    const int64_t n = s.ncap, m = n < sd::kSampleMax ? n : sd::kSampleMax;
+    const int64_t kk = sp->k_override ? k_max : sd::budget_rule(n, sp->ratio, sp->k_rounding);
+    if (n > 0 && kk > 0 && m < n) {
+      rank = (double)sd::pilot_rank(kk, m, n);
+      fcand = rank * n / ((double)kk * m);
+    }
+    if (fcand < 1.0) fcand = 1.0;
+    if (rank < 16.0) rank = 16.0;
+  }
+  const int64_t want = (int64_t)(fcand * (double)k_max * (1.0 + 3.0 / std::sqrt(rank))) + 256;
   const size_t pre_bytes = sd::select_lds_bytes(L.nchunk, 0);
   const int64_t room256 = (int64_t)sd::select_lds_budget(false) - (int64_t)pre_bytes;
   const bool wide = sd::select_wide(
