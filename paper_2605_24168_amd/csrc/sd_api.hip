@@ -355,7 +355,7 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
   if (fused) {
     const size_t blocks = (size_t)s.B * s.Hkv * L.nchunk * L.blk_cap;
     L.sample = take((size_t)rows * sd::kSampleMax * 4);
-    L.theta = take((size_t)rows * 4);
+    L.theta = take((size_t)rows * 8);  // thresholds, then largest samples
     L.dir = take((size_t)rows * L.nchunk * 8);
     L.ckey = take(blocks * 4);
     L.cpos = take(blocks * 2);
@@ -451,6 +451,7 @@ sd::Work carve(char *base, const Layout &L, bool fused, const Shape &s,
   if (fused) {
     w.sample = (float *)(base + L.sample);
     w.theta = (float *)(base + L.theta);
+    w.smax = w.theta + (int64_t)s.B * s.R;
     w.dir = (int2 *)(base + L.dir);
     w.ckey = (uint32_t *)(base + L.ckey);
     w.cpos = (uint16_t *)(base + L.cpos);

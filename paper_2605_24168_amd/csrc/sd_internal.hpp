@@ -80,6 +80,7 @@ struct Params {
 struct Work {
   float *sample;     // [rows][kSampleMax] pilot sample scores
   float *theta;      // [rows] candidate threshold
+  float *smax;       // [rows] largest pilot sample score
   int2 *dir;         // [rows][nchunk] (start, count) of the row's candidates in
                      // its chunk's block; count -1 = a staging area overflowed
   uint32_t *ckey;    // [B*Hkv][nchunk][blk_cap] order-preserving score keys

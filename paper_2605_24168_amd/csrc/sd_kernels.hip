@@ -25,6 +25,8 @@
 // overflowed.  Otherwise the row takes the exact fallback.
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "sd_internal.hpp"
 #include "sd_launch.hpp"
 
@@ -344,6 +346,7 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
     mx = key > mx ? key : mx;
   }
   block_key_range(mn, mx, range);  // also publishes keys
+  if (threadIdx.x == 0) w.smax[row] = key2f(mx);
   uint32_t T;
   int need_eq;
   // The r-th largest sample exactly; else (rare) two radix passes fix its
@@ -1123,6 +1126,292 @@ __device__ __forceinline__ void select_and_write_staged(const ChunkCands &src, i
   }
 }
 
+// ---------------------------------------------------------------------------
+// Candidate selection with the keys held in registers, for rows whose n
+// candidates fit NT * UMAX register slots and whose positions fit the LDS
+// array pos_l.  Wave w takes a contiguous share [i0, i1) of the item order,
+// lane l the items i0 + 64 u + l (slot u): every key and position load of
+// the row is issued before the first one returns, so the candidates cost one
+// memory latency.  The k-th largest key then comes from a bucket histogram
+// of the registers (exact three-pass radix over the key bits when a bucket
+// holds more than NT keys), and the compaction numbers the kept items with
+// wave ballots: in item order, the kept lanes of a slot writing consecutive
+// list entries.  hist must be zero on entry; every thread must call it.
+// ---------------------------------------------------------------------------
+template <int NT>
+constexpr int reg_select_slots() { return NT >= 1024 ? 40 : 32; }
+
+// x itself, hidden from the optimiser: values derived from x in one phase
+// are recomputed in the next instead of being kept alive across it.
+__device__ __forceinline__ uint32_t fresh(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Thread t owns the nb / NT bins [nb - (t+1) nb/NT, nb - t nb/NT), counted
+// from the top; the owner of the bin where the count from the top reaches
+// krem stores it in sh->digit and the count above it in sh->above.  Ends
+// with a barrier.
+template <int NT>
+__device__ __forceinline__ void find_rank_bin(const uint32_t *hist, int nb, int krem,
+                                              SelShared *sh) {
+  const int bpt = nb / NT;
+  const int hi = nb - (int)threadIdx.x * bpt;
+  int mine = 0;
+  for (int j = 1; j <= bpt; ++j) mine += (int)hist[hi - j];
+  int tot;
+  const int before = block_excl_scan<NT>(mine, sh->scan, &tot);
+  if (before < krem && krem <= before + mine) {
+    int cum = before;
+    for (int j = 1; j <= bpt; ++j) {
+      const int c = (int)hist[hi - j];
+      if (cum + c >= krem) {
+        sh->digit = (uint32_t)(hi - j);
+        sh->above = cum;
+        break;
+      }
+      cum += c;
+    }
+  }
+  __syncthreads();
+}
+
+// f(std::integral_constant<int, u>) for u = 0 .. N-1, unrolled in the
+// source: register arrays indexed by u keep constant indices from the start
+// and stay scalar registers (a loop unrolled later by the compiler can leave
+// them promoted to one vector value that every branch then copies whole).
+template <int I, int N, class F>
+__device__ __forceinline__ void unroll_for_from(F &f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    unroll_for_from<I + 1, N>(f);
+  }
+}
+template <int N, class F>
+__device__ __forceinline__ void unroll_for(F &&f) {
+  unroll_for_from<0, N>(f);
+}
+
+// LDS of select_regs besides hist, SelShared and BucketShared.
+template <int NT>
+struct RegSelShared {
+  uint32_t gt[NT / 64], eq[NT / 64];  // per wave: kept keys above T, keys equal to T
+  uint32_t wmax[NT / 64];             // per wave: its largest key
+  uint32_t sink[64];                  // target of the atomics of lanes without an item
+  uint8_t wave[NT];                   // the wave of each key collected in BucketShared
+};
+
+// kb_lo <= every candidate key (the row's threshold: the candidates passed
+// score >= theta) and kb_hi the key of the row's largest pilot sample: the
+// histogram's buckets cut [kb_lo, kb_hi] into equal runs of keys, those above
+// kb_hi joining the top one.  The mapping is known before the candidates
+// arrive, so the histogram is taken as they do; a k-th bucket with more
+// than NT keys (rare) falls back to the radix passes.
+template <int NT, int UMAX>
+__device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k, uint32_t kb_lo,
+                                            uint32_t kb_hi, uint32_t *pos_l, uint32_t *hist,
+                                            SelShared *sh, BucketShared<NT> *bs,
+                                            RegSelShared<NT> *rs, int32_t *irow, float *vrow,
+                                            bool weights, float scale) {
+  constexpr int NW = NT / 64;
+  const int lane = lane_id(), wv = wave_id();
+  const int per = (n + NW - 1) / NW;
+  const int i0 = min(n, wv * per), i1 = min(n, i0 + per);
+  const int U = (i1 - i0 + 63) >> 6;  // <= UMAX: the caller checked n <= NT * UMAX
+  const uint32_t span = kb_hi > kb_lo ? kb_hi - kb_lo : 0u;
+  const int shift = span < (uint32_t)kBuckets ? 0 : (32 - __builtin_clz(span)) - 11;
+  auto bucket = [&](uint32_t x) {
+    const uint32_t bk = (x > kb_lo ? x - kb_lo : 0u) >> shift;
+    return bk < (uint32_t)kBuckets - 1u ? (int)bk : kBuckets - 1;
+  };
+  if (threadIdx.x == 0) {
+    bs->n = 0;
+    sh->digit = 0u;  // (in range even if the candidates were fewer than k)
+    sh->above = 0;
+  }
+  // Lane j <= U: the chunk of item min(i0 + 64 j, i1 - 1) and that chunk's
+  // offset d (item i of chunk c sits at block entry d + i).
+  int cs = 0, ds = 0;
+  if (lane <= U && i1 > i0) {
+    cs = src.chunk_of(min(i0 + 64 * lane, i1 - 1));
+    ds = cs * src.cap + src.start[cs] - src.pre[cs];
+  }
+  // 1. Every load of the wave's candidates; lanes past its last item repeat
+  // the last item's (so that no branch splits the slots).
+  uint32_t key[UMAX], gp[UMAX];
+  unroll_for<UMAX>([&](auto uc) {
+    constexpr int u = decltype(uc)::value;
+    key[u] = 0u;
+    gp[u] = 0u;
+    if (u < U) {  // wave-uniform
+      const int ie = min(i0 + 64 * u + lane, i1 - 1);
+      const int cu = __builtin_amdgcn_readlane(cs, u), cn = __builtin_amdgcn_readlane(cs, u + 1);
+      int c = cu, d = __builtin_amdgcn_readlane(ds, u);
+      if (cn != cu) {  // the slot crosses chunk boundaries: count those at or below ie
+        for (int x = cu + 1; x <= cn; ++x) c += src.pre[x] <= ie ? 1 : 0;
+        d = c * src.cap + src.start[c] - src.pre[c];
+      }
+      const uint32_t e = (uint32_t)(d + ie);
+      key[u] = src.gkey[e];
+      gp[u] = src.gpos[e];
+      pos_l[ie] = (uint32_t)c * (uint32_t)src.ck;
+    }
+  });
+  // 2. Positions (chunk base + offset) and the histogram, as the loads land.
+  uint32_t mx = 0u;
+  unroll_for<UMAX>([&](auto uc) {
+    constexpr int u = decltype(uc)::value;
+    if (u < U) {
+      const int i = i0 + 64 * u + lane;
+      const bool valid = i < i1;
+      const uint32_t x = fresh(key[u]);
+      atomicAdd(valid ? &pos_l[i] : &rs->sink[lane], gp[u]);
+      atomicAdd(valid ? &hist[bucket(x)] : &rs->sink[lane], 1u);
+      mx = valid && x > mx ? x : mx;
+    }
+  });
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t t = (uint32_t)__shfl_xor((int)mx, o);
+    mx = t > mx ? t : mx;
+  }
+  if (lane == 0) rs->wmax[wv] = mx;
+  __syncthreads();
+  // 3. The k-th largest key T; need_eq of the keys equal to T are kept.
+  find_rank_bin<NT>(hist, kBuckets, k, sh);
+  const int bstar = (int)sh->digit;
+  const int krem = k - (int)sh->above;
+  const int m = (int)hist[bstar];
+  uint32_t T;
+  int need_eq;
+  if (m <= NT) {
+    // Keys above the k-th bucket per wave; the bucket's keys (and waves).
+    int gt_w = 0;
+    unroll_for<UMAX>([&](auto uc) {
+      constexpr int u = decltype(uc)::value;
+      if (u < U) {
+        const bool valid = i0 + 64 * u + lane < i1;
+        const uint32_t x = fresh(key[u]);
+        const int bk = bucket(x);
+        gt_w += __popcll(__ballot(valid && bk > bstar));
+        if (valid && bk == bstar) {
+          const int j = atomicAdd(&bs->n, 1);
+          bs->items[j] = x;
+          rs->wave[j] = (uint8_t)wv;
+        }
+      }
+    });
+    if (lane == 0) {
+      rs->gt[wv] = (uint32_t)gt_w;
+      rs->eq[wv] = 0u;
+    }
+    __syncthreads();
+    if ((int)threadIdx.x < m) {
+      const uint32_t x = bs->items[threadIdx.x];
+      int gt = 0, ge = 0;
+      for (int y = 0; y < m; ++y) {
+        const uint32_t v = bs->items[y];
+        gt += v > x ? 1 : 0;
+        ge += v >= x ? 1 : 0;
+      }
+      if (gt < krem && krem <= ge) {  // x is the krem-th largest (equal keys agree)
+        sh->digit = x;
+        sh->above = gt;
+      }
+    }
+    __syncthreads();
+    T = sh->digit;
+    need_eq = krem - (int)sh->above;
+    if ((int)threadIdx.x < m) {  // the bucket's keys join their waves' counts
+      const uint32_t x = bs->items[threadIdx.x];
+      if (x > T) atomicAdd(&rs->gt[rs->wave[threadIdx.x]], 1u);
+      if (x == T) atomicAdd(&rs->eq[rs->wave[threadIdx.x]], 1u);
+    }
+    __syncthreads();
+  } else {  // three radix passes over 11, 11 and 10 key bits
+    uint32_t prefix = 0, mask = 0;
+    int kr = k;
+#pragma unroll 1
+    for (int pass = 0; pass < 3; ++pass) {
+      const int sft = pass == 0 ? 21 : (pass == 1 ? 10 : 0);
+      const int nb = pass == 2 ? 1024 : 2048;
+      const uint32_t dmask = (uint32_t)nb - 1u;
+      __syncthreads();  // the previous readers of hist and sh are done
+      for (int j = threadIdx.x; j < nb; j += NT) hist[j] = 0;
+      __syncthreads();
+      unroll_for<UMAX>([&](auto uc) {
+        constexpr int u = decltype(uc)::value;
+        if (u < U) {
+          const uint32_t x = fresh(key[u]);
+          hist_add(hist, (x >> sft) & dmask, i0 + 64 * u + lane < i1 && (x & mask) == prefix);
+        }
+      });
+      __syncthreads();
+      find_rank_bin<NT>(hist, nb, kr, sh);
+      prefix |= sh->digit << sft;
+      mask |= dmask << sft;
+      kr -= (int)sh->above;
+    }
+    T = prefix;
+    need_eq = kr;
+    int gt_w = 0, eq_w = 0;
+    unroll_for<UMAX>([&](auto uc) {
+      constexpr int u = decltype(uc)::value;
+      if (u < U) {
+        const bool valid = i0 + 64 * u + lane < i1;
+        const uint32_t x = fresh(key[u]);
+        gt_w += __popcll(__ballot(valid && x > T));
+        eq_w += __popcll(__ballot(valid && x == T));
+      }
+    });
+    if (lane == 0) {
+      rs->gt[wv] = (uint32_t)gt_w;
+      rs->eq[wv] = (uint32_t)eq_w;
+    }
+    __syncthreads();
+  }
+  // 4. Each wave's first list slot and rank among the keys equal to T; the
+  // kept keys in item order, each slot's kept lanes on consecutive entries.
+  int gt_b = 0, eq_b = 0;
+  uint32_t kmax = 0u;
+#pragma unroll
+  for (int v = 0; v < NW; ++v) {
+    if (v < wv) {
+      gt_b += (int)rs->gt[v];
+      eq_b += (int)rs->eq[v];
+    }
+    kmax = rs->wmax[v] > kmax ? rs->wmax[v] : kmax;
+  }
+  int eq_run = eq_b, sel_run = gt_b + min(eq_b, need_eq);
+  const float vmax = key2f(kmax);
+  unroll_for<UMAX>([&](auto uc) {
+    constexpr int u = decltype(uc)::value;
+    if (u < U) {
+      const int i = i0 + 64 * u + lane;
+      const bool valid = i < i1;
+      const uint32_t x = fresh(key[u]);
+      const uint64_t eqm = __ballot(valid && x == T);
+      const bool kept = valid && (x > T || (x == T && eq_run + lanes_below(eqm) < need_eq));
+      const uint64_t km = __ballot(kept);
+      const int s = sel_run + lanes_below(km);
+      if (kept && s < k) {
+        irow[s] = (int32_t)pos_l[i];
+        if (vrow) {
+          const float v = key2f(x);
+          vrow[s] = weights ? expf(scale * (v - vmax)) : v;
+        }
+      }
+      eq_run += __popcll(eqm);
+      sel_run += __popcll(km);
+    }
+  });
+}
+
 // Per-head rows of the fused path: turn the kept scores (vrow[0..k), written
 // by this workgroup) into softmax weights exp(scale*(s - max s)) in place, so
 // that the attention is a plain weighted gather whose splits all share one
@@ -1139,7 +1428,7 @@ __device__ __forceinline__ void kept_scores_to_weights(float *vrow, int k, float
 // NT threads per workgroup: 256, or 1024 when the rows are too few to fill
 // the GPU one workgroup each (every per-thread loop is then 4x shorter).
 template <int MODE, int NT>
-__global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *dense, int64_t ld,
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_select(Params p, Work w, const float *dense, int64_t ld,
                                                int32_t *idx, float *vals, int lds_cap) {
   extern __shared__ uint32_t dyn[];
   __shared__ uint32_t hist[2048];
@@ -1147,6 +1436,7 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
   __shared__ float ftmp[NT / 64];
   __shared__ uint32_t range[NT / 64][2];
   __shared__ BucketShared<NT> bs;
+  __shared__ RegSelShared<NT> rsh;
   bool weights_done = false;
   const int row = blockIdx.x, b = row / p.R;
   const int L = seq_len(p, b);
@@ -1178,6 +1468,7 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
       int *start = pre + (nch + 1);   // nch
       uint32_t *lkey = (uint32_t *)(start + nch);  // lds_cap keys
       const int2 *drow = w.dir + (int64_t)row * w.nchunk;
+      for (int i = tid; i < kBuckets; i += NT) hist[i] = 0;  // (published by the scan's barriers)
       int carry = 0;
       for (int base = 0; base < nch; base += NT) {
         const int c = base + tid;
@@ -1195,6 +1486,12 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
       const int total = carry;
       const int64_t gblk = ((int64_t)b * p.Hkv + g) * w.nchunk * w.blk_cap;
       ChunkCands src{nullptr, pre, start, nch, w.ckey + gblk, w.cpos + gblk, ck, w.blk_cap};
+      constexpr int kSlots = reg_select_slots<NT>();
+      if (total <= lds_cap && total <= NT * kSlots && (int64_t)nch * w.blk_cap <= INT32_MAX) {
+        select_regs<NT, kSlots>(src, total, k, f2key(w.theta[row]), f2key(w.smax[row]), lkey,
+                                hist, &sh, &bs, &rsh, irow, vrow, weights, p.scale);
+        weights_done = true;
+      } else {
       // The flat copy goes to LDS when it fits, else to the row's fallback
       // score row, which an unflagged row does not use (the candidates are
       // distinct positions of [lo, hi), so total <= ncap).
@@ -1206,6 +1503,7 @@ __global__ __launch_bounds__(NT) void k_select(Params p, Work w, const float *de
       select_and_write_staged<NT>(src, total, k, mn, mx, hist, &sh, &bs, irow, vrow, weights,
                                   p.scale);
       weights_done = true;
+      }
     } else {
       select_and_write<NT>(DenseSrc{dense + (int64_t)row * ld + rp.lo, (uint32_t)rp.lo},
                            rp.hi - rp.lo, k, hist, &sh, irow, vrow);
@@ -2036,7 +2334,7 @@ bool select_wide(const Params &p, size_t lds_bytes) {
 
 size_t select_lds_budget(bool wide) {
   // Dynamic LDS left by the selection kernel's static LDS (hist, scan and
-  // bucket scratch: about 9.4 KB at 256 threads, 12.6 KB at 1024) under the
+  // bucket scratch: about 9.9 KB at 256 threads, 14.1 KB at 1024) under the
   // 160 KB of a workgroup.
   return wide ? 144 * 1024 : 150 * 1024;
 }
