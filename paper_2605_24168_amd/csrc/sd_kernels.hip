@@ -1234,7 +1234,7 @@ __device__ __forceinline__ __attribute__((address_space(1))) T *uniform_ptr(T *p
   return (__attribute__((address_space(1))) T *)(((uint64_t)hi << 32) | lo);
 }
 
-// LDS of select_regs besides hist, SelShared and BucketShared.
+// LDS of the register selection besides hist, SelShared and BucketShared.
 template <int NT>
 struct RegSelShared {
   uint32_t gt[NT / 64], eq[NT / 64];  // per wave: kept keys above T, keys equal to T
@@ -1243,47 +1243,64 @@ struct RegSelShared {
   uint8_t wave[NT];                   // the wave of each key collected in BucketShared
 };
 
-// kb_lo <= every candidate key (the row's threshold: the candidates passed
-// score >= theta) and kb_hi the key of the row's largest pilot sample: the
-// histogram's buckets cut [kb_lo, kb_hi] into equal runs of keys, those above
-// kb_hi joining the top one.  The mapping is known before the candidates
-// arrive, so the histogram is taken as they do; a k-th bucket with more
-// than NT keys (rare) falls back to the radix passes.
-template <int NT, int UMAX>
-__device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k, uint32_t kb_lo,
-                                            uint32_t kb_hi, uint32_t *pos_l, uint32_t *hist,
-                                            SelShared *sh, BucketShared<NT> *bs,
-                                            RegSelShared<NT> *rs, int32_t *irow, float *vrow,
-                                            bool weights, float scale) {
-  constexpr int NW = NT / 64;
-  const int lane = lane_id(), wv = wave_id();
-  const int per = (n + NW - 1) / NW;
-  const int i0 = min(n, wv * per), i1 = min(n, i0 + per);
-  const int U = (i1 - i0 + 63) >> 6;  // <= UMAX: the caller checked n <= NT * UMAX
-  const uint32_t span = kb_hi > kb_lo ? kb_hi - kb_lo : 0u;
-  const int shift = span < (uint32_t)kBuckets ? 0 : (32 - __builtin_clz(span)) - 11;
-  auto bucket = [&](uint32_t x) {
-    const uint32_t bk = (x > kb_lo ? x - kb_lo : 0u) >> shift;
-    return bk < (uint32_t)kBuckets - 1u ? (int)bk : kBuckets - 1;
-  };
-  if (threadIdx.x == 0) {
-    bs->n = 0;
-    sh->digit = 0u;  // (in range even if the candidates were fewer than k)
-    sh->above = 0;
+// Histogram buckets over keys: bucket b holds the keys lo + [b, b+1) << shift,
+// those below lo joining bucket 0 and those past the last bucket the top one.
+struct KeyBuckets {
+  uint32_t lo;
+  int shift;
+  // Buckets from lo, with `span` keys to spread over them.
+  __device__ __forceinline__ static KeyBuckets make(uint32_t lo, uint32_t span) {
+    KeyBuckets kb;
+    kb.lo = lo;
+    kb.shift = span < (uint32_t)kBuckets ? 0 : (32 - __builtin_clz(span)) - 11;
+    return kb;
   }
-  // Lane j <= U: the chunk of item min(i0 + 64 j, i1 - 1) and that chunk's
-  // offset d (item i of chunk c sits at block entry d + i).
+  __device__ __forceinline__ int of(uint32_t x) const {
+    const uint32_t bk = (x > lo ? x - lo : 0u) >> shift;
+    return bk < (uint32_t)kBuckets - 1u ? (int)bk : kBuckets - 1;
+  }
+};
+
+// A wave's contiguous share [i0, i1) of the items [ia, ib): lane l holds the
+// items i0 + 64 u + l, slots u < U.
+struct RegShare {
+  int i0, i1, U;
+};
+template <int NT>
+__device__ __forceinline__ RegShare reg_share(int ia, int ib) {
+  constexpr int NW = NT / 64;
+  const int n = ib - ia, per = (n + NW - 1) / NW;
+  RegShare s;
+  s.i0 = ia + min(n, wave_id() * per);
+  s.i1 = ia + min(n, wave_id() * per + per);
+  s.U = (s.i1 - s.i0 + 63) >> 6;
+  return s;
+}
+
+// The candidates of a share into registers (key[u]) and their positions
+// (chunk base + offset) into pos_l[i - ia].  Every load is issued before the
+// first returns; lanes past the share's end repeat its last item (so that no
+// branch splits a slot).  Lane j first finds the chunk of the share's item
+// i0 + 64 j; a slot within one chunk then takes its chunk and block offset
+// from that lane (scalar registers), a slot across chunk boundaries counts
+// the boundaries at or below each item.  As the loads land, on_key(key,
+// valid) runs for every slot (the first histogram); returns the lane's
+// largest key.  sink: 64 LDS words for the atomics of lanes without an item.
+template <int UMAX, class OnKey>
+__device__ __forceinline__ uint32_t reg_load(const ChunkCands &src, const RegShare &sh, int ia,
+                                             uint32_t (&key)[UMAX], uint32_t *pos_l,
+                                             uint32_t *sink, OnKey on_key) {
+  const int lane = lane_id(), i0 = sh.i0, i1 = sh.i1, U = sh.U;
   int cs = 0, ds = 0;
   if (lane <= U && i1 > i0) {
     cs = src.chunk_of(min(i0 + 64 * lane, i1 - 1));
     ds = cs * src.cap + src.start[cs] - src.pre[cs];
   }
-  // 1. Every load of the wave's candidates; lanes past its last item repeat
-  // the last item's (so that no branch splits the slots).  The blocks' base
-  // addresses are the row's (scalar registers: 32-bit offsets per lane).
+  // The blocks' base addresses are the row's (scalar registers: 32-bit
+  // offsets per lane).
   const auto gkey = uniform_ptr(src.gkey);
   const auto gpos = uniform_ptr(src.gpos);
-  uint32_t key[UMAX], gp[UMAX];
+  uint32_t gp[UMAX];
   unroll_for<UMAX>([&](auto uc) {
     constexpr int u = decltype(uc)::value;
     key[u] = 0u;
@@ -1299,10 +1316,9 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
       const uint32_t e = (uint32_t)(d + ie);
       key[u] = gkey[e];
       gp[u] = gpos[e];
-      pos_l[ie] = (uint32_t)c * (uint32_t)src.ck;
+      pos_l[ie - ia] = (uint32_t)c * (uint32_t)src.ck;
     }
   });
-  // 2. Positions (chunk base + offset) and the histogram, as the loads land.
   uint32_t mx = 0u;
   unroll_for<UMAX>([&](auto uc) {
     constexpr int u = decltype(uc)::value;
@@ -1310,10 +1326,87 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
       const int i = i0 + 64 * u + lane;
       const bool valid = i < i1;
       const uint32_t x = fresh(key[u]);
-      atomicAdd(valid ? &pos_l[i] : &rs->sink[lane], gp[u]);
-      atomicAdd(valid ? &hist[bucket(x)] : &rs->sink[lane], 1u);
+      atomicAdd(valid ? &pos_l[i - ia] : &sink[lane], gp[u]);
+      on_key(x, valid);
       mx = valid && x > mx ? x : mx;
     }
+  });
+  return mx;
+}
+
+// The kept keys of a share in item order: those above T, and those equal to
+// T while fewer than need_eq of them came before (eq_b before the wave).
+// Slot sel0 (the wave's first entry) onwards, each slot's kept lanes on
+// consecutive list entries; with vrow, the kept scores or (weights) their
+// softmax weights against vmax.  Entries at or past k are not written.
+template <int UMAX>
+__device__ __forceinline__ void reg_emit(const uint32_t (&key)[UMAX], const RegShare &sh, int ia,
+                                         uint32_t T, int need_eq, int eq_b, int sel0, int k,
+                                         const uint32_t *pos_l, int32_t *irow, float *vrow,
+                                         bool weights, float vmax, float c2) {
+  const int lane = lane_id();
+  const auto lst = uniform_ptr(irow);
+  const auto val = uniform_ptr(vrow);
+  auto emit = [&](auto vals, auto wts) {
+    int eq_run = eq_b, sel_run = sel0;
+    unroll_for<UMAX>([&](auto uc) {
+      constexpr int u = decltype(uc)::value;
+      if (u < sh.U) {
+        const int i = sh.i0 + 64 * u + lane;
+        const bool valid = i < sh.i1;
+        const uint32_t x = fresh(key[u]);
+        const uint64_t eqm = __ballot(valid && x == T);
+        const bool kept = valid && (x > T || (x == T && eq_run + lanes_below(eqm) < need_eq));
+        const uint64_t km = __ballot(kept);
+        const int s = sel_run + lanes_below(km);
+        if (kept && s < k) {
+          lst[s] = (int32_t)pos_l[i - ia];
+          if constexpr (decltype(vals)::value) {
+            const float v = key2f(x);
+            val[s] = decltype(wts)::value ? kept_weight(v, vmax, c2) : v;
+          }
+        }
+        eq_run += __popcll(eqm);
+        sel_run += __popcll(km);
+      }
+    });
+  };
+  if (!vrow) emit(std::false_type{}, std::false_type{});
+  else if (weights) emit(std::true_type{}, std::true_type{});
+  else emit(std::true_type{}, std::false_type{});
+}
+
+// Candidate selection of a row by one workgroup, the keys held in registers
+// (n <= NT * UMAX, positions in pos_l).  kb_lo <= every candidate key (the
+// row's threshold: the candidates passed score >= theta) and kb_hi the key
+// of the row's largest pilot sample: the first histogram's buckets cut
+// [kb_lo, kb_hi] into equal runs of keys, those above kb_hi joining the top
+// one.  The mapping is known before the candidates arrive, so the histogram
+// is taken as they do.  One more pass over the registers counts each wave's
+// keys above the k-th bucket and collects the bucket's keys (typically a
+// few dozen); an exact rank among them gives the threshold key T.  A k-th
+// bucket of more than NT keys (rare) falls back to three radix passes over
+// the key bits.  hist must be zero on entry; every thread must call it.
+template <int NT, int UMAX>
+__device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k, uint32_t kb_lo,
+                                            uint32_t kb_hi, uint32_t *pos_l, uint32_t *hist,
+                                            SelShared *sh, BucketShared<NT> *bs,
+                                            RegSelShared<NT> *rs, int32_t *irow, float *vrow,
+                                            bool weights, float scale) {
+  constexpr int NW = NT / 64;
+  const int lane = lane_id(), wv = wave_id();
+  const RegShare shr = reg_share<NT>(0, n);  // U <= UMAX: the caller checked n <= NT * UMAX
+  const int i0 = shr.i0, i1 = shr.i1, U = shr.U;
+  const KeyBuckets kb = KeyBuckets::make(kb_lo, kb_hi > kb_lo ? kb_hi - kb_lo : 0u);
+  if (threadIdx.x == 0) {
+    bs->n = 0;
+    sh->digit = 0u;  // (in range even if the candidates were fewer than k)
+    sh->above = 0;
+  }
+  // 1-2. The candidates, their positions and the histogram.
+  uint32_t key[UMAX];
+  uint32_t mx = reg_load<UMAX>(src, shr, 0, key, pos_l, rs->sink, [&](uint32_t x, bool valid) {
+    atomicAdd(valid ? &hist[kb.of(x)] : &rs->sink[lane_id()], 1u);
   });
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -1337,7 +1430,7 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
       if (u < U) {
         const bool valid = i0 + 64 * u + lane < i1;
         const uint32_t x = fresh(key[u]);
-        const int bk = bucket(x);
+        const int bk = kb.of(x);
         gt_w += __popcll(__ballot(valid && bk > bstar));
         if (valid && bk == bstar) {
           const int j = atomicAdd(&bs->n, 1);
@@ -1415,8 +1508,8 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
     }
     __syncthreads();
   }
-  // 4. Each wave's first list slot and rank among the keys equal to T; the
-  // kept keys in item order, each slot's kept lanes on consecutive entries.
+  // 4. Each wave's first list slot and rank among the keys equal to T, then
+  // the kept keys in item order.
   int gt_b = 0, eq_b = 0;
   uint32_t kmax = 0u;
 #pragma unroll
@@ -1427,37 +1520,8 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
     }
     kmax = rs->wmax[v] > kmax ? rs->wmax[v] : kmax;
   }
-  const int sel0 = gt_b + min(eq_b, need_eq);
-  const float vmax = key2f(kmax), c2 = weight_factor(scale);
-  const auto lst = uniform_ptr(irow);
-  const auto val = uniform_ptr(vrow);
-  auto emit = [&](auto vals, auto wts) {
-    int eq_run = eq_b, sel_run = sel0;
-    unroll_for<UMAX>([&](auto uc) {
-      constexpr int u = decltype(uc)::value;
-      if (u < U) {
-        const int i = i0 + 64 * u + lane;
-        const bool valid = i < i1;
-        const uint32_t x = fresh(key[u]);
-        const uint64_t eqm = __ballot(valid && x == T);
-        const bool kept = valid && (x > T || (x == T && eq_run + lanes_below(eqm) < need_eq));
-        const uint64_t km = __ballot(kept);
-        const int s = sel_run + lanes_below(km);
-        if (kept && s < k) {
-          lst[s] = (int32_t)pos_l[i];
-          if constexpr (decltype(vals)::value) {
-            const float v = key2f(x);
-            val[s] = decltype(wts)::value ? kept_weight(v, vmax, c2) : v;
-          }
-        }
-        eq_run += __popcll(eqm);
-        sel_run += __popcll(km);
-      }
-    });
-  };
-  if (!vrow) emit(std::false_type{}, std::false_type{});
-  else if (weights) emit(std::true_type{}, std::true_type{});
-  else emit(std::true_type{}, std::false_type{});
+  reg_emit<UMAX>(key, shr, 0, T, need_eq, eq_b, gt_b + min(eq_b, need_eq), k, pos_l, irow, vrow,
+                 weights, key2f(kmax), weight_factor(scale));
 }
 
 // Per-head rows of the fused path: turn the kept scores (vrow[0..k), written
