@@ -1339,15 +1339,17 @@ __device__ __forceinline__ uint32_t reg_load(const ChunkCands &src, const RegSha
 // Slot sel0 (the wave's first entry) onwards, each slot's kept lanes on
 // consecutive list entries; with vrow, the kept scores or (weights) their
 // softmax weights against vmax.  Entries at or past k are not written.
+// ties: whether the wave holds a key equal to T (else a key is kept iff it
+// is above T, and the tie count is skipped).
 template <int UMAX>
 __device__ __forceinline__ void reg_emit(const uint32_t (&key)[UMAX], const RegShare &sh, int ia,
                                          uint32_t T, int need_eq, int eq_b, int sel0, int k,
-                                         const uint32_t *pos_l, int32_t *irow, float *vrow,
-                                         bool weights, float vmax, float c2) {
+                                         bool ties, const uint32_t *pos_l, int32_t *irow,
+                                         float *vrow, bool weights, float vmax, float c2) {
   const int lane = lane_id();
   const auto lst = uniform_ptr(irow);
   const auto val = uniform_ptr(vrow);
-  auto emit = [&](auto vals, auto wts) {
+  auto emit = [&](auto vals, auto wts, auto tie) {
     int eq_run = eq_b, sel_run = sel0;
     unroll_for<UMAX>([&](auto uc) {
       constexpr int u = decltype(uc)::value;
@@ -1355,8 +1357,12 @@ __device__ __forceinline__ void reg_emit(const uint32_t (&key)[UMAX], const RegS
         const int i = sh.i0 + 64 * u + lane;
         const bool valid = i < sh.i1;
         const uint32_t x = fresh(key[u]);
-        const uint64_t eqm = __ballot(valid && x == T);
-        const bool kept = valid && (x > T || (x == T && eq_run + lanes_below(eqm) < need_eq));
+        bool kept = valid && x > T;
+        if constexpr (decltype(tie)::value) {
+          const uint64_t eqm = __ballot(valid && x == T);
+          kept = kept || (valid && x == T && eq_run + lanes_below(eqm) < need_eq);
+          eq_run += __popcll(eqm);
+        }
         const uint64_t km = __ballot(kept);
         const int s = sel_run + lanes_below(km);
         if (kept && s < k) {
@@ -1366,14 +1372,17 @@ __device__ __forceinline__ void reg_emit(const uint32_t (&key)[UMAX], const RegS
             val[s] = decltype(wts)::value ? kept_weight(v, vmax, c2) : v;
           }
         }
-        eq_run += __popcll(eqm);
         sel_run += __popcll(km);
       }
     });
   };
-  if (!vrow) emit(std::false_type{}, std::false_type{});
-  else if (weights) emit(std::true_type{}, std::true_type{});
-  else emit(std::true_type{}, std::false_type{});
+  auto emit_ties = [&](auto vals, auto wts) {
+    if (ties) emit(vals, wts, std::true_type{});
+    else emit(vals, wts, std::false_type{});
+  };
+  if (!vrow) emit_ties(std::false_type{}, std::false_type{});
+  else if (weights) emit_ties(std::true_type{}, std::true_type{});
+  else emit_ties(std::true_type{}, std::false_type{});
 }
 
 // Candidate selection of a row by one workgroup, the keys held in registers
@@ -1422,6 +1431,8 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
   const int m = (int)hist[bstar];
   uint32_t T;
   int need_eq;
+  int gt_b = 0, eq_b = 0;  // kept keys of the waves before this one: above T, equal to T
+  bool ties = false;
   if (m <= NT) {
     // Keys above the k-th bucket per wave; the bucket's keys (and waves).
     int gt_w = 0;
@@ -1439,10 +1450,7 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
         }
       }
     });
-    if (lane == 0) {
-      rs->gt[wv] = (uint32_t)gt_w;
-      rs->eq[wv] = 0u;
-    }
+    if (lane == 0) rs->gt[wv] = (uint32_t)gt_w;
     __syncthreads();
     if ((int)threadIdx.x < m) {
       const uint32_t x = bs->items[threadIdx.x];
@@ -1460,12 +1468,17 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
     __syncthreads();
     T = sh->digit;
     need_eq = krem - (int)sh->above;
-    if ((int)threadIdx.x < m) {  // the bucket's keys join their waves' counts
-      const uint32_t x = bs->items[threadIdx.x];
-      if (x > T) atomicAdd(&rs->gt[rs->wave[threadIdx.x]], 1u);
-      if (x == T) atomicAdd(&rs->eq[rs->wave[threadIdx.x]], 1u);
+    // The bucket's keys of the waves before this one (above T, equal to
+    // T), and whether this wave holds a key equal to T.
+    for (int j0 = 0; j0 < m; j0 += 64) {
+      const int j = j0 + lane;
+      const bool in = j < m;
+      const uint32_t x = in ? bs->items[j] : 0u;
+      const int v = in ? (int)rs->wave[j] : NW;
+      gt_b += __popcll(__ballot(in && v < wv && x > T));
+      eq_b += __popcll(__ballot(in && v < wv && x == T));
+      ties = ties || __ballot(in && v == wv && x == T) != 0;
     }
-    __syncthreads();
   } else {  // three radix passes over 11, 11 and 10 key bits
     uint32_t prefix = 0, mask = 0;
     int kr = k;
@@ -1507,21 +1520,21 @@ __device__ __forceinline__ void select_regs(const ChunkCands &src, int n, int k,
       rs->eq[wv] = (uint32_t)eq_w;
     }
     __syncthreads();
+#pragma unroll
+    for (int v = 0; v < NW; ++v)
+      if (v < wv) eq_b += (int)rs->eq[v];
+    ties = eq_w > 0;
   }
-  // 4. Each wave's first list slot and rank among the keys equal to T, then
-  // the kept keys in item order.
-  int gt_b = 0, eq_b = 0;
+  // 4. Each wave's first list slot (the kept keys of the waves before it),
+  // then its kept keys in item order.
   uint32_t kmax = 0u;
 #pragma unroll
   for (int v = 0; v < NW; ++v) {
-    if (v < wv) {
-      gt_b += (int)rs->gt[v];
-      eq_b += (int)rs->eq[v];
-    }
+    if (v < wv) gt_b += (int)rs->gt[v];
     kmax = rs->wmax[v] > kmax ? rs->wmax[v] : kmax;
   }
-  reg_emit<UMAX>(key, shr, 0, T, need_eq, eq_b, gt_b + min(eq_b, need_eq), k, pos_l, irow, vrow,
-                 weights, key2f(kmax), weight_factor(scale));
+  reg_emit<UMAX>(key, shr, 0, T, need_eq, eq_b, gt_b + min(eq_b, need_eq), k, ties, pos_l, irow,
+                 vrow, weights, key2f(kmax), weight_factor(scale));
 }
 
 // Per-head rows of the fused path: turn the kept scores (vrow[0..k), written

@@ -213,6 +213,34 @@ def test_fused_ties_at_the_threshold_go_to_the_lower_position(sd, debug):
     assert ok, f"output error {ratio:.3g} x allowance"
 
 
+def test_fused_crowded_k_th_bucket_takes_the_radix_passes(sd):
+    # Twenty sampled keys far above the rest stretch the selection's first
+    # histogram (its range runs up to the largest pilot sample), and 700
+    # nearly equal keys above every other key hold the k-th largest (40
+    # distinct bf16 values among them), so the k-th bucket holds hundreds of
+    # keys and the selection falls back to radix passes over the key bits.
+    inp = make("w5", seed=33)
+    G = inp.Hq // inp.Hkv
+    L = int(inp.seq_lens[0])
+    qs = synth.bf16_to_f32(inp.q[0, :G]).astype(np.float64).sum(axis=0)
+    u = qs / np.linalg.norm(qs)
+    k = inp.k.copy()
+    top = float((synth.bf16_to_f32(k[0, 0]).astype(np.float64) @ qs).max())
+    sampled = (np.arange(100, 120) * L) // min(L, 2048)  # pilot sample positions
+    far = (u * 4.0 * top / np.linalg.norm(qs)).astype(np.float32)
+    k[0, 0, sampled] = synth.bf16_bits(np.repeat(far[None, :], len(sampled), axis=0))
+    c = 1.5 * top / np.linalg.norm(qs) * (1.0 + 2e-3 * np.arange(700) / 700.0)
+    k[0, 0, 30000:30700] = synth.bf16_bits((c[:, None] * u[None, :]).astype(np.float32))
+    inp = dataclasses.replace(inp, k=k)
+    out, idx, _ = gpu_fused(sd, inp)
+    ora = O.sparse_attention(inp)
+    np.testing.assert_array_equal(idx, ora["idx"])
+    ok, ratio, _ = P.out_errors(out, ora["out"], inp.dtype)
+    assert ok, f"output error {ratio:.3g} x allowance"
+    k0 = int(P.budgets(inp)[0])
+    assert set(idx[0, 0, :k0]) <= set(range(30000, 30700)) | set(sampled.tolist())
+
+
 def test_fused_low_sparsity_takes_the_fallback_for_every_row(sd):
     # At 2x with 4 heads per KV head a scoring wave's expected candidates
     # would overfill the staging areas, so the call scores every row in full
