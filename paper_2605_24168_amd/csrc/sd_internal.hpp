@@ -8,6 +8,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace sd {
 
 constexpr int kHeadDim = 128;
@@ -522,6 +524,46 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
     if (l >= o) v += t;
   }
   return v;
+}
+
+// x itself, hidden from the optimiser: values derived from x in one phase
+// are recomputed in the next instead of being kept alive across it.
+__device__ __forceinline__ uint32_t fresh(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Inclusive prefix sum over the wave's 64 lanes by DPP lane shifts within
+// rows of 16 (1, 2, 4, 8) and the two row broadcasts (no LDS round trips).
+__device__ __forceinline__ int wave_incl_scan_dpp(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15, rows 1, 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31, rows 2, 3
+  return v;
+}
+
+// f(std::integral_constant<int, u>) for u = 0 .. N-1, unrolled in the
+// source: register arrays indexed by u keep constant indices from the start
+// and stay scalar registers (a loop unrolled later by the compiler can leave
+// them promoted to one vector value that every branch then copies whole).
+template <int I, int N, class F>
+__device__ __forceinline__ void unroll_for_from(F &f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    unroll_for_from<I + 1, N>(f);
+  }
+}
+template <int N, class F>
+__device__ __forceinline__ void unroll_for(F &&f) {
+  unroll_for_from<0, N>(f);
 }
 
 // Exclusive prefix sum over the block in thread order; *total gets the sum.
