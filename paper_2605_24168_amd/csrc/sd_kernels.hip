@@ -77,17 +77,24 @@ __device__ __forceinline__ void scorer_init(const Params &p, int b, int g,
 constexpr int kPilotTiles = 4;
 
 // LABEL: the samples are scored by the low-channel indexer (label tiles).
-template <bool LABEL>
+// QUAD (paged caches with a multiple of 4 KV heads): grid = (kSampleMax /
+// (kPilotTiles * kTile), B*Hkv/4), and wave v of a workgroup takes KV head
+// 4q + v over the same sample tiles as its neighbours: the four heads of a
+// sampled position are adjacent in a page (256 B each), so their rows are
+// requested together instead of by four workgroups at different times.
+template <bool LABEL, bool QUAD>
 __global__ __launch_bounds__(kBlock) void k_pilot_score(Params p, Work w) {
-  const int bg = blockIdx.y, b = bg / p.Hkv, g = bg % p.Hkv;
+  const int hq = QUAD ? p.Hkv / kWaves : p.Hkv;
+  const int by = blockIdx.y, b = by / hq;
+  const int g = QUAD ? (by % hq) * kWaves + wave_id() : by % hq;
   const int L = seq_len(p, b);
   const RowPlan rp = row_plan(p, b, L);  // samples come from the top-k range only
   const int mid = rp.hi - rp.lo;
   const int m = mid < kSampleMax ? mid : kSampleMax;
   const int ntiles = (m + kTile - 1) / kTile;
   const int l = lane_id(), col = l & 15, s = l >> 4;
-  const int t0 = blockIdx.x * kWaves + wave_id();
-  const int stride = gridDim.x * kWaves;
+  const int t0 = QUAD ? (int)blockIdx.x : (int)blockIdx.x * kWaves + wave_id();
+  const int stride = QUAD ? (int)gridDim.x : (int)gridDim.x * kWaves;
   if (t0 >= ntiles) return;  // wave-uniform; no barriers in this kernel
   QFrag qf;
   LabelRows lr;
@@ -2344,9 +2351,15 @@ static inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1
 
 hipError_t launch_pilot(const Params &p, const Work &w, hipStream_t st) {
   if (!w.force_repair) {
-    const dim3 g1(kSampleMax / (kPilotTiles * kTile * kWaves), p.B * p.Hkv);
-    if (p.labels) k_pilot_score<true><<<g1, kBlock, 0, st>>>(p, w);
-    else k_pilot_score<false><<<g1, kBlock, 0, st>>>(p, w);
+    if (p.K.paged && p.Hkv % kWaves == 0) {
+      const dim3 g4(kSampleMax / (kPilotTiles * kTile), p.B * p.Hkv / kWaves);
+      if (p.labels) k_pilot_score<true, true><<<g4, kBlock, 0, st>>>(p, w);
+      else k_pilot_score<false, true><<<g4, kBlock, 0, st>>>(p, w);
+    } else {
+      const dim3 g1(kSampleMax / (kPilotTiles * kTile * kWaves), p.B * p.Hkv);
+      if (p.labels) k_pilot_score<true, false><<<g1, kBlock, 0, st>>>(p, w);
+      else k_pilot_score<false, false><<<g1, kBlock, 0, st>>>(p, w);
+    }
   }
   k_pilot_select<<<p.B * p.R, kBlock, 0, st>>>(p, w);
   return hipGetLastError();
