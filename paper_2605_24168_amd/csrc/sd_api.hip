@@ -244,7 +244,7 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
 // the same layout is recomputed on every call.
 struct Layout {
   size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, ustart, total;
-  size_t queue, unit_pre;
+  size_t queue, unit_pre, seq_order;
   size_t dsel_hist, dsel_state, dsel_cnt;
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
   int dsel_parts;        // pieces per row of the multi-workgroup fallback selection (0: none)
@@ -364,6 +364,7 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
     L.sigma = take((size_t)rows * k_max * 4);
     L.queue = take(4);
     L.unit_pre = take((size_t)(s.B + 1) * 4);
+    L.seq_order = take((size_t)s.B * 4);
     L.dsel_parts = dsel_parts_for(s);
     if (L.dsel_parts) {
       L.dsel_hist = take((size_t)rows * 2048 * 4);
@@ -460,6 +461,7 @@ sd::Work carve(char *base, const Layout &L, bool fused, const Shape &s,
     w.sigma = (float *)(base + L.sigma);
     w.queue = (int32_t *)(base + L.queue);
     w.unit_pre = (int32_t *)(base + L.unit_pre);
+    w.seq_order = (int32_t *)(base + L.seq_order);
     w.unit_heads = L.chunk_keys == L.wave_keys ? s.Hkv / sd::kWaves : s.Hkv;
     if (L.dsel_parts) {
       w.dsel_hist = (uint32_t *)(base + L.dsel_hist);
@@ -776,6 +778,9 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   // chunk, several per compute unit.
   w.persistent = labels ? 0 : 1;
   w.stream_wgs = ds->n_cu;
+  // (the length order is written by the pilot, which a call forced onto the
+  // fallback skips: its rows keep the batch order)
+  if (w.force_repair) w.seq_order = nullptr;
   int32_t *idx_ptr = (int32_t *)idx->data;
 
   const int prof_level = no_alloc ? 0 : g_profiling.load();  // (profiling creates events)

@@ -127,7 +127,17 @@ struct Work {
   int32_t unit_heads;
   int32_t *queue;
   int32_t *unit_pre;
+  // Sequences by descending length (ties: lower index first), written by
+  // k_pilot_select; the selection and the attention take their rows in
+  // that order, so that the longest rows start first.  Null: batch order.
+  int32_t *seq_order;
 };
+
+// Row of workgroup i of a launch over rows (rows_per_b rows per sequence) in
+// the order of w.seq_order (the identity when it is null).
+__device__ __forceinline__ int ordered_row(const Work &w, int i, int rows_per_b) {
+  return w.seq_order ? w.seq_order[i / rows_per_b] * rows_per_b + i % rows_per_b : i;
+}
 
 // Scratch of the dense decode kernels.
 struct DenseWork {

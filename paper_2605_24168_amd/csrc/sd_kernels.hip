@@ -283,6 +283,8 @@ struct LdsKeys {
 // so it stages no candidates) when every row is forced to, or when its
 // expected candidates per wave, r * min(L, wave_keys) / m, exceed half of
 // its staging area (low sparsity).
+constexpr int kOrderBatchMax = 2048;  // batches ordered by length (lengths staged in hist)
+
 __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
   __shared__ uint32_t keys[kSampleMax];
   __shared__ uint32_t hist[2048];
@@ -306,6 +308,25 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
       w.unit_pre[p.B] = carry;
       w.queue[0] = 0;
     }
+  }
+  if (row == 0) {
+    // Sequences by descending length (ties: lower index first): rank each
+    // by counting the ones before it, over the lengths staged in LDS (batch
+    // order for very large batches).
+    const int nb = p.B <= kOrderBatchMax ? p.B : 0;
+    int *lens = (int *)hist;  // (free until the row's own selection below)
+    for (int bb = (int)threadIdx.x; bb < nb; bb += kBlock) lens[bb] = seq_len(p, bb);
+    __syncthreads();
+    for (int bb = (int)threadIdx.x; bb < p.B; bb += kBlock) {
+      int rank = bb;
+      if (nb) {
+        const int Lb = lens[bb];
+        rank = 0;
+        for (int o = 0; o < nb; ++o) rank += (lens[o] > Lb || (lens[o] == Lb && o < bb)) ? 1 : 0;
+      }
+      w.seq_order[rank] = bb;
+    }
+    __syncthreads();  // (hist is the selection's again)
   }
   const int L = seq_len(p, b);
   const RowPlan rp = row_plan(p, b, L);
@@ -1529,7 +1550,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_
   __shared__ BucketShared<NT> bs;
   __shared__ RegSelShared<NT> rsh;
   bool weights_done = false;
-  const int row = blockIdx.x, b = row / p.R;
+  const int row = MODE == 0 ? ordered_row(w, (int)blockIdx.x, p.R) : (int)blockIdx.x;
+  const int b = row / p.R;
   const int L = seq_len(p, b);
   // The row's list: its forced sinks, the exact top-k of [lo, hi), then its
   // forced local window.
@@ -2002,8 +2024,9 @@ __global__ __launch_bounds__(kBlock) void k_attend(Params p, Work w, const int32
   constexpr int U = (BF16 && !GRP) ? 8 : 4;  // positions per 16-lane group per step
   constexpr int HB = GRP ? HBU : 1;  // heads accumulated per pass
 
-  const int s = blockIdx.x, row = blockIdx.y;
   const int rows_per_b = UNI ? p.Hkv : p.R;  // union rows are the groups
+  const int s = blockIdx.x, row = FUSED ? ordered_row(w, (int)blockIdx.y, rows_per_b)
+                                        : (int)blockIdx.y;
   const int b = row / rows_per_b, r = row % rows_per_b;
   constexpr bool grp = GRP;
   const int nh = grp ? p.G : 1;
