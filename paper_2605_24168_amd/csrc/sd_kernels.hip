@@ -440,8 +440,10 @@ struct StreamLds {
   int seg_off[kWaves * (kMaxGroup + 1)];  // their offsets in the block(s)
   int wave_tot[kWaves];                   // QUAD: entries of each wave's block
   int unit;                               // the unit taken from the queue
-  Outbox ob;
 };
+// (Under a third of the 160 KB of a compute unit: three label-stream
+// workgroups fit on one.)
+static_assert(sizeof(StreamLds) <= 163840 / 3, "three label-stream workgroups per compute unit");
 
 // Write the outbox's blocks to the candidate blocks (16- and 8-byte stores)
 // and empty it.  Every thread of the block must call it.  Plain stores: the
@@ -646,43 +648,69 @@ __device__ __forceinline__ void stream_unit(const Params &p, const Work &w, int 
       }
       const int nt64 = (nvalid + 63) / 64;
       const int64_t lslab = (((int64_t)b * p.K.hkv + g) * p.K.ncap + w0) * kLabels;
-      const int64_t page_el = (int64_t)kTile * p.K.hkv * kLabels;
+      // (a page's label block is below 2^31 bytes: 32 x 32 -> 64-bit products)
+      const uint32_t page_el = (uint32_t)(kTile * p.K.hkv * kLabels);
+      const uint32_t head_el = (uint32_t)(g * kTile * kLabels);
       auto lload = [&](int ti) -> u32x4 {
         ti = ti < nt64 ? ti : nt64 - 1;
         int j = ti * 64 + l;
         j = j < last ? j : last;
-        const int64_t off = PAGED ? pg[j >> 4] * page_el + ((int64_t)g * kTile + (j & 15)) * kLabels
+        const int64_t off = PAGED ? (int64_t)((uint64_t)(uint32_t)pg[j >> 4] * page_el +
+                                              (head_el + (uint32_t)(j & 15) * kLabels))
                                   : lslab + (int64_t)j * kLabels;
         return load_labels(p.labels, off);
       };
       const int nlsteps = (nt64 + kLabelDepth - 1) / kLabelDepth * kLabelDepth;
       u32x4 lb[kLabelDepth];
+      // The first tiles are issued after the rows' operands and in tile
+      // order, so that the loop's first use of a tile waits for that tile
+      // only: a load issued after it would make the wait (placed once for
+      // the loop's entry and every step) cover every tile in flight.
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int d = 0; d < kLabelDepth; ++d) lb[d] = lload(d);
+      for (int d = 0; d < kLabelDepth; ++d) {
+        lb[d] = lload(d);
+        __builtin_amdgcn_sched_barrier(0);
+      }
       for (int tb = 0; tb < nlsteps; tb += kLabelDepth) {
 #pragma unroll
         for (int u = 0; u < kLabelDepth; ++u) {
           const int ti = tb + u;
-          const u32x4 raw = lb[u];
-          float lab[kLabels];
-          if constexpr (GRP) unpack_labels(raw, lab);
+          // Every row's score of this lane's key first, then the load that
+          // reuses the tile's registers: issued before the tile's last use,
+          // it would need other registers and a copy back (with a wait for
+          // the load) at the end of the step.
+          float sc[NRr];
+          {
+            const u32x4 raw = lb[u];
+            float lab[kLabels];
+            if constexpr (GRP) unpack_labels(raw, lab);
+#pragma unroll
+            for (int h = 0; h < NRr; ++h) {
+              if constexpr (GRP) sc[h] = label_dot(qlr[h], lab);
+              else sc[h] = label_dot_packed(qpr[h], raw);
+            }
+          }
+          __builtin_amdgcn_sched_barrier(0);
           lb[u] = lload(ti + kLabelDepth);
           const int jl = ti * 64 + l;
-          const bool live = jl >= jlo && jl < jhi;
+          const bool live = (jl >= jlo) & (jl < jhi);
+          const uint64_t live_m = __builtin_amdgcn_ballot_w64(live);
 #pragma unroll
           for (int h = 0; h < NRr; ++h) {
-            float sc;
-            if constexpr (GRP) sc = label_dot(qlr[h], lab);
-            else sc = label_dot_packed(qpr[h], raw);
-            // In-order slot from the ballot's count of lower lanes; lanes that
-            // do not pass (or overflow the area) write their discard slot,
-            // so no branch or exec-mask change is needed.
-            const bool pass = live && sc >= thr[h];
-            const uint64_t m = __ballot(pass);
-            const int slot = cntr[h] + (int)__builtin_amdgcn_mbcnt_hi(
-                (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-            const int e = (pass && slot < cap) ? h * cap + slot : kCandBuf + l;
-            wl.cand[e] = make_uint2(__float_as_uint(sc), (uint32_t)jl);
+            // In-order entry from the ballot's count of lower lanes, counted
+            // from the row's next free entry; lanes that do not pass (or run
+            // past the row's area) write their discard slot, so no branch
+            // or exec-mask change is needed.  (Ballots of the compares
+            // themselves, and no short-circuit: no round trips through
+            // vector registers, no masked regions.)
+            const bool ge = sc[h] >= thr[h];
+            const uint64_t m = __builtin_amdgcn_ballot_w64(ge) & live_m;
+            const int at = (int)__builtin_amdgcn_mbcnt_hi(
+                (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, (uint32_t)(h * cap + cntr[h])));
+            const bool ok = live & ge & (at < (h + 1) * cap);
+            const int e = ok ? at : kCandBuf + l;
+            wl.cand[e] = make_uint2(__float_as_uint(sc[h]), (uint32_t)jl);
             cntr[h] += __popcll(m);
           }
         }
