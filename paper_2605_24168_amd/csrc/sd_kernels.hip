@@ -38,6 +38,17 @@ struct Scorer {
   QFrag qf;
   LabelRows lr;
   float *q_lds;
+  // The loaded operand of one tile (bf16 keys or labels), so that several
+  // tiles can be in flight: load() issues the loads, from_raw() scores.
+  using Raw = std::conditional_t<LABEL, u32x4, KFrag>;
+  __device__ __forceinline__ void load(const Params &p, int b, int g, int64_t j, Raw &r) const {
+    if constexpr (LABEL) r = load_labels(p.labels, label_offset(p.K, b, g, j));
+    else load_k_bf16(p.K, kv_offset(p.K, b, g, j), r);
+  }
+  __device__ __forceinline__ f32x4 from_raw(const Raw &r) const {
+    if constexpr (LABEL) return lr.score(r);
+    else return mfma_scores(qf, r);
+  }
   __device__ __forceinline__ f32x4 score(const Params &p, int b, int g, int64_t j) const {
     if constexpr (LABEL) {
       return lr.score(load_labels(p.labels, label_offset(p.K, b, g, j)));
@@ -958,11 +969,10 @@ __device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_
   const int64_t end = fill_tail ? p.ncap : (int64_t)L;
   const int64_t ntiles = (end + kTile - 1) / kTile;
   const int l = lane_id(), col = l & 15, s = l >> 4;
-  for (int64_t t = (int64_t)part * kWaves + wave_id(); t < ntiles; t += (int64_t)parts * kWaves) {
+  const int64_t t0 = (int64_t)part * kWaves + wave_id(), step = (int64_t)parts * kWaves;
+  auto put = [&](int64_t t, f32x4 acc) {
     const int64_t j = t * kTile + col;
     const bool in_seq = j < L;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    if (t * kTile < L) acc = sc.score(p, b, g, in_seq ? j : (int64_t)L - 1);
     const float ninf = -__builtin_inff();
     if (!p.group_shared) {
 #pragma unroll
@@ -974,6 +984,49 @@ __device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_
       const float gs = group_sum(acc);
       if (s == 0 && j < end) dst[row0 * ld + j] = in_seq ? gs : ninf;
     }
+  };
+  if constexpr (BF16 || LABEL) {
+    if (L > 0 && t0 < ntiles) {  // wave-uniform
+      // kD tiles in flight per wave: one tile's loads are a single round
+      // trip (4 KB of keys, or 256 B of label rows), and one at a time left
+      // the fallback waiting on latency.  Positions past the sequence read
+      // its last key again (their scores are replaced by -inf), and the
+      // step count is rounded up to whole rounds with clamped loads, so
+      // every step issues the same loads and the waits stay exact.
+      constexpr int kD = LABEL ? 8 : 3;
+      const int64_t n = (ntiles - t0 + step - 1) / step;
+      const int64_t nsteps = (n + kD - 1) / kD * kD;
+      auto ld_tile = [&](int64_t i, typename Scorer<BF16, LABEL>::Raw &r) {
+        const int64_t j = (t0 + i * step) * kTile + col;
+        sc.load(p, b, g, j < L ? j : (int64_t)L - 1, r);
+      };
+      typename Scorer<BF16, LABEL>::Raw buf[kD];
+#pragma unroll
+      for (int d = 0; d < kD; ++d) {
+        ld_tile(d, buf[d]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      for (int64_t i0 = 0; i0 < nsteps; i0 += kD) {
+#pragma unroll
+        for (int u = 0; u < kD; ++u) {
+          const int64_t i = i0 + u;
+          // (the tile is scored before the load that reuses its registers)
+          const f32x4 acc = sc.from_raw(buf[u]);
+          __builtin_amdgcn_sched_barrier(0);
+          ld_tile(i + kD, buf[u]);
+          const int64_t t = t0 + i * step;
+          if (i < n && t * kTile < L) put(t, acc);
+          else if (i < n) put(t, f32x4{0.f, 0.f, 0.f, 0.f});
+        }
+      }
+      return;
+    }
+  }
+  for (int64_t t = t0; t < ntiles; t += step) {
+    const int64_t j = t * kTile + col;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    if (t * kTile < L) acc = sc.score(p, b, g, j < L ? j : (int64_t)L - 1);
+    put(t, acc);
   }
 }
 
@@ -2501,15 +2554,20 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
   return hipGetLastError();
 }
 
-// Workgroups per (sequence, KV head) of the fallback scoring: kRepairParts,
-// or, when every row is forced onto the fallback and the groups are few,
-// enough for about 2048 in all (with one sequence each wave would otherwise
-// score a long run of tiles one after another, each waiting for its loads;
-// without forcing, flagged rows are rare and the extra workgroups would only
-// cost their launch).
+// Workgroups per (sequence, KV head) of the fallback scoring.  Without
+// forcing, flagged rows are rare and most calls only check the flags, so
+// about 1024 workgroups in all, up to kRepairParts per group: a launch of
+// 2048 or 4096 workgroups that only check the flags took 4.4 and 6.9 us at
+// the 128K batch-16 and the ragged paged workloads.  When every row is
+// forced onto the fallback and the groups are few, enough for about 2048 in
+// all (with one sequence each wave would otherwise score a long run of
+// tiles one after another, each waiting for its loads).
 int repair_parts(const Params &p, const Work &w) {
-  if (!w.force_repair) return kRepairParts;
   const int groups = p.B * p.Hkv;
+  if (!w.force_repair) {
+    const int parts = (1024 + groups - 1) / groups;
+    return parts < kRepairParts ? parts : kRepairParts;
+  }
   int parts = (2048 + groups - 1) / groups;
   parts = parts < kRepairParts ? kRepairParts : parts;
   return parts > 256 ? 256 : parts;
