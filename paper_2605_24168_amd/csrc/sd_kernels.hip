@@ -959,7 +959,14 @@ __global__ __launch_bounds__(kBlock) void k_score_stream(Params p, Work w) {
 // fill_tail, -inf for L_b <= j < ncap.  Every thread of the block must call
 // it (the f32 scorer stages the queries in LDS behind a barrier).
 // ---------------------------------------------------------------------------
-template <bool BF16, bool LABEL>
+// Tiles in flight per wave in the pipelined full scoring: one tile's loads
+// are a single round trip (4 KB of keys, or 256 B of label rows).
+constexpr int dense_depth(bool label) { return label ? 8 : 3; }
+
+// PIPE: several tiles in flight per wave (a separate instance, launched when
+// the waves have enough tiles for it: its registers would cost occupancy to
+// the short waves too).
+template <bool BF16, bool LABEL, bool PIPE = false>
 __device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_t ld, int b, int g,
                                              int part, int parts, bool fill_tail, float *q_lds) {
   const int L = seq_len(p, b);
@@ -985,16 +992,17 @@ __device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_
       if (s == 0 && j < end) dst[row0 * ld + j] = in_seq ? gs : ninf;
     }
   };
-  if constexpr (BF16 || LABEL) {
-    if (L > 0 && t0 < ntiles) {  // wave-uniform
-      // kD tiles in flight per wave: one tile's loads are a single round
-      // trip (4 KB of keys, or 256 B of label rows), and one at a time left
-      // the fallback waiting on latency.  Positions past the sequence read
-      // its last key again (their scores are replaced by -inf), and the
-      // step count is rounded up to whole rounds with clamped loads, so
-      // every step issues the same loads and the waits stay exact.
-      constexpr int kD = LABEL ? 8 : 3;
-      const int64_t n = (ntiles - t0 + step - 1) / step;
+  if constexpr ((BF16 || LABEL) && PIPE) {
+    // kD tiles in flight per wave (one at a time left the fallback waiting
+    // on latency).  Positions past the sequence read its last key again
+    // (their scores are replaced by -inf), and the step count is rounded up
+    // to whole rounds with clamped loads, so every step issues the same
+    // loads and the waits stay exact.  A wave with fewer than two rounds of
+    // tiles keeps the plain loop: the rounding and the loads issued past its
+    // last tile would cost it more than they hide.
+    constexpr int kD = dense_depth(LABEL);
+    const int64_t n = t0 < ntiles ? (ntiles - t0 + step - 1) / step : 0;
+    if (L > 0 && n >= 2 * kD) {  // wave-uniform
       const int64_t nsteps = (n + kD - 1) / kD * kD;
       auto ld_tile = [&](int64_t i, typename Scorer<BF16, LABEL>::Raw &r) {
         const int64_t j = (t0 + i * step) * kTile + col;
@@ -1031,12 +1039,12 @@ __device__ __forceinline__ void dense_scores(const Params &p, float *dst, int64_
 }
 
 // sparse_decode_score: grid = (parts, B*Hkv).
-template <bool BF16, bool LABEL>
+template <bool BF16, bool LABEL, bool PIPE>
 __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, int64_t ld) {
   __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
   const int bg = blockIdx.y;
-  dense_scores<BF16, LABEL>(p, dst, ld, bg / p.Hkv, bg % p.Hkv, blockIdx.x, gridDim.x, true,
-                            q_lds);
+  dense_scores<BF16, LABEL, PIPE>(p, dst, ld, bg / p.Hkv, bg % p.Hkv, blockIdx.x, gridDim.x,
+                                  true, q_lds);
 }
 
 // Exact fallback, scoring.  grid = (parts, B*Hkv), parts at least
@@ -1047,7 +1055,7 @@ __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, in
 // per-chunk counts (part 0 records them in w.flags for the selection) and,
 // when a row of the group is flagged, scores its part of the group into
 // w.dense.
-template <bool BF16, bool LABEL>
+template <bool BF16, bool LABEL, bool PIPE>
 __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
   __shared__ int cnt[kMaxGroup], bad[kMaxGroup];
@@ -1088,7 +1096,8 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
     if (part == 0) w.flags[row0 + tid] = flag ? 1 : 0;
   }
   __syncthreads();
-  if (any) dense_scores<BF16, LABEL>(p, w.dense, p.ncap, b, g, part, (int)gridDim.x, false, q_lds);
+  if (any)
+    dense_scores<BF16, LABEL, PIPE>(p, w.dense, p.ncap, b, g, part, (int)gridDim.x, false, q_lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -2588,11 +2597,33 @@ hipError_t launch_dense_select(const Params &p, const Work &w, int32_t *idx, hip
   return hipGetLastError();
 }
 
+// Whether the full scoring of `parts` workgroups per (sequence, KV head)
+// takes the instance with several tiles in flight: bf16 keys or labels,
+// every wave with at least two rounds of tiles, and groups of more than one
+// row.  (With one row per group, MHA, the forced fallback of Table 2's label
+// shape at 2x took 0.377 instead of 0.338 ms at batch 1 and 1.23 instead of
+// 1.13 ms at batch 4; with groups of four rows it went from 0.257 to 0.246
+// ms at batch 1, and the 128K batch-16 key fallback from 1.10 to 1.04 ms.)
+static bool dense_pipelined(const Params &p, int parts) {
+  const int64_t tiles = (p.ncap + kTile - 1) / kTile;
+  const int64_t per_wave = (tiles + (int64_t)parts * kWaves - 1) / ((int64_t)parts * kWaves);
+  return (p.labels || p.bf16) && (p.group_shared || p.G > 1) &&
+         per_wave >= 2 * dense_depth(p.labels != nullptr);
+}
+
 hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st) {
-  const dim3 grid(repair_parts(p, w), p.B * p.Hkv);
-  if (p.labels) k_repair_score<true, true><<<grid, kBlock, 0, st>>>(p, w);
-  else if (p.bf16) k_repair_score<true, false><<<grid, kBlock, 0, st>>>(p, w);
-  else k_repair_score<false, false><<<grid, kBlock, 0, st>>>(p, w);
+  const int parts = repair_parts(p, w);
+  const dim3 grid(parts, p.B * p.Hkv);
+  const bool pipe = dense_pipelined(p, parts);
+  if (p.labels) {
+    if (pipe) k_repair_score<true, true, true><<<grid, kBlock, 0, st>>>(p, w);
+    else k_repair_score<true, true, false><<<grid, kBlock, 0, st>>>(p, w);
+  } else if (p.bf16) {
+    if (pipe) k_repair_score<true, false, true><<<grid, kBlock, 0, st>>>(p, w);
+    else k_repair_score<true, false, false><<<grid, kBlock, 0, st>>>(p, w);
+  } else {
+    k_repair_score<false, false, false><<<grid, kBlock, 0, st>>>(p, w);
+  }
   return hipGetLastError();
 }
 
@@ -2706,10 +2737,18 @@ hipError_t launch_attend(const Params &p, const Work &w, const int32_t *idx, voi
 }
 
 hipError_t launch_score_dense(const Params &p, float *scores, hipStream_t st) {
-  const dim3 grid(cdiv(p.ncap, kDenseChunk), p.B * p.Hkv);
-  if (p.labels) k_score_dense<true, true><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
-  else if (p.bf16) k_score_dense<true, false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
-  else k_score_dense<false, false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  const int parts = (int)cdiv(p.ncap, kDenseChunk);
+  const dim3 grid(parts, p.B * p.Hkv);
+  const bool pipe = dense_pipelined(p, parts);
+  if (p.labels) {
+    if (pipe) k_score_dense<true, true, true><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+    else k_score_dense<true, true, false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  } else if (p.bf16) {
+    if (pipe) k_score_dense<true, false, true><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+    else k_score_dense<true, false, false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  } else {
+    k_score_dense<false, false, false><<<grid, kBlock, 0, st>>>(p, scores, p.ncap);
+  }
   return hipGetLastError();
 }
 
