@@ -415,9 +415,10 @@ __global__ __launch_bounds__(kBlock) void k_pilot_select(Params p, Work w) {
 // cost far more than their bytes on this memory system (about 1.7 us per
 // MB of candidates measured at the 128K batch-16 workload), while one burst
 // at the end, after the reads, costs little.
-// Otherwise (label rows: that stream is bound by the vector ALUs and wants
-// several workgroups per compute unit) one workgroup per unit, on a static
-// grid that includes empty chunks, writes its block directly.
+// Otherwise (label rows: one workgroup per compute unit leaves that stream
+// too few loads in flight and its latency chains unhidden, measured 50%
+// slower) one workgroup per unit, several per compute unit, on a static grid
+// that includes empty chunks, writes its block directly.
 // The streaming loop issues no global stores, so its load waits stay exact.
 // ---------------------------------------------------------------------------
 constexpr int kDepth = 3;        // tiles in flight per wave
