@@ -537,7 +537,7 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, copy this many MiB device to device once (a plain "
                          "copy of known size that scales hardware traffic counters)")
-    ap.add_argument("--extra-workloads", default="4",
+    ap.add_argument("--extra-workloads", default="4,5,2,1",
                     help="comma-separated workloads measured after the default line's, without "
                          "the CPU oracle leg, and reported under extra_workloads ('' to skip)")
     ap.add_argument("--calls", type=int, default=30,
