@@ -2628,7 +2628,15 @@ hipError_t launch_repair(const Params &p, const Work &w, hipStream_t st) {
   return hipGetLastError();
 }
 
-constexpr int kAttendWorkgroups = 1024;   // enough to fill the chip
+// Workgroups to aim for when rows are split.  Fused calls: two per CU; with
+// 1024, few rows were cut into pieces short enough for their latency chains
+// and the merge to dominate (1M-key group-shared batch of 8 rows: attention
+// 36 -> 30 us at 512; Table 2's label shape at batch 1 and 4, 2-5% faster).
+// Unfused calls (the weighted backend over caller lists, key and value rows
+// per entry) keep four per CU: their low-sparsity lists are bandwidth-bound,
+// and at 512 Table 1's batch 1 took 0.281 instead of 0.177 ms at 2x.
+constexpr int kAttendWorkgroupsFused = 512;
+constexpr int kAttendWorkgroups = 1024;
 constexpr int kAttendLdsMax = 60 * 1024;  // dynamic LDS of one attend workgroup
 constexpr int kAttendMinEntries = 64;     // fewest list entries worth a workgroup of their own
 constexpr int kAttendRowsWhole = 256;     // this many rows fill the chip unsplit
@@ -2636,14 +2644,16 @@ constexpr int kAttendRowsWhole = 256;     // this many rows fill the chip unspli
 // Positions per attend workgroup: a row is not split when there are enough
 // rows to give every CU a workgroup and the whole list fits one workgroup's
 // LDS (a split then costs the merge launch, more than the extra parallelism
-// saves); otherwise rows are split into about kAttendWorkgroups workgroups
+// saves); otherwise rows are split into about kAttendWorkgroupsFused
+// (fused) or kAttendWorkgroups (unfused) workgroups
 // in all, at least 64 positions each, within the LDS budget.
 int attend_split(const Params &p, int k_max_positions, bool fused) {
   const int64_t rows = (int64_t)p.B * p.R;
   const int64_t k_max = k_max_positions > 0 ? k_max_positions : 1;
   const int nh = p.group_shared ? p.G : 1;
   const bool rc = attend_recompute(fused, p);
-  int64_t nsplit = (kAttendWorkgroups + rows - 1) / rows;
+  const int64_t target = fused ? kAttendWorkgroupsFused : kAttendWorkgroups;
+  int64_t nsplit = (target + rows - 1) / rows;
   if (rows >= kAttendRowsWhole && k_max <= 4096 &&  // (bounded: the LDS sum stays in int)
       AttLds((int)((k_max + 63) / 64 * 64), nh, rc).total <= kAttendLdsMax)
     nsplit = 1;
