@@ -313,7 +313,10 @@ sd_status sparse_decode_profile_mean(sd_profile *out, int32_t *n_calls);
  * sparse_decode_attention takes the exact fallback path; flags & 4 / & 8
  * turn the group-deduplicated attention off / on wherever it applies
  * (per-head rows with recomputed logits, bf16, 2 or more heads per group),
- * overriding the cost rule.  0 restores normal. */
+ * overriding the cost rule; flags & 16 / & 32 turn the candidate selection
+ * over several workgroups per row off / on wherever it applies (calls with
+ * fewer than 256 rows, no group-deduplicated attention), overriding its
+ * cost rule (rows expecting 8K candidates or more).  0 restores normal. */
 sd_status sparse_decode_set_debug(int32_t flags);
 
 /* Measurement helper, not a step of the method: one streaming read of

@@ -245,9 +245,10 @@ int wave_keys_for(const Shape &s, const sd_sparsity *sp, int group_shared, bool 
 struct Layout {
   size_t sample, theta, dir, ckey, cpos, flags, dense, sigma, part, ustart, total;
   size_t queue, unit_pre, seq_order;
-  size_t dsel_hist, dsel_state, dsel_cnt;
+  size_t dsel_hist, dsel_state, dsel_cnt, psel_rec;
   int nchunk, wave_keys, chunk_keys, blk_cap, nsplit;
   int dsel_parts;        // pieces per row of the multi-workgroup fallback selection (0: none)
+  int psel_parts;        // pieces per row of the multi-workgroup candidate selection (0: none)
   int ustride;           // chunk starts per row of the union attention (0: none)
   int union_chunk;       // positions per union-attention workgroup (0: per-row lists)
 };
@@ -291,7 +292,22 @@ int dsel_parts_for(const Shape &s) {
   return parts >= 2 ? (int)parts : 0;
 }
 
+// Pieces per row for the candidate selection over several workgroups: rows
+// too few for the 1024-thread selection to fill the GPU one each get about
+// 256 workgroups in all, at most kPselPartsMax per row and at least one
+// chunk and at most kPselChunksMax chunks per piece; 0 when that leaves
+// fewer than two pieces.
+int psel_parts_for(const Shape &s, int nchunk) {
+  const int64_t rows = (int64_t)s.B * s.R;
+  if (rows <= 0 || rows >= sd::kSelectWideRows || nchunk <= 0) return 0;
+  int64_t parts = std::min<int64_t>(sd::kPselPartsMax, 256 / rows);
+  parts = std::min<int64_t>(parts, nchunk);
+  if (parts < 2 || (nchunk + parts - 1) / parts > sd::kPselChunksMax) return 0;
+  return (int)parts;
+}
+
 constexpr int64_t kManyCandidates = 48 * 1024;
+constexpr int64_t kPieceCandidates = 8 * 1024;  // fewest candidates per row worth the pieces
 
 // Whether the pilot would send a row of the full capacity to the exact
 // fallback (its rule: the expected candidates of a scoring wave would fill
@@ -371,6 +387,8 @@ Layout layout_for(const Shape &s, int64_t k_max, bool fused, const sd_sparsity *
       L.dsel_state = take((size_t)rows * 4 * 4);
       L.dsel_cnt = take((size_t)rows * sd::kDselPartsMax * 8);
     }
+    L.psel_parts = psel_parts_for(s, L.nchunk);
+    if (L.psel_parts) L.psel_rec = take((size_t)rows * L.psel_parts * sd::kPselStride * 4);
     if (uni_ok) {  // present whenever the call could use it (see union_pays)
       const int uc = sd::union_chunk(shape_only);
       L.ustride = (int)((s.ncap + uc - 1) / uc) + 1;
@@ -468,6 +486,7 @@ sd::Work carve(char *base, const Layout &L, bool fused, const Shape &s,
       w.dsel_state = (int32_t *)(base + L.dsel_state);
       w.dsel_cnt = (int2 *)(base + L.dsel_cnt);
     }
+    if (L.psel_parts) w.psel_rec = (uint32_t *)(base + L.psel_rec);
   }
   w.part = (float *)(base + L.part);
   w.ustart = L.union_chunk > 0 ? (int32_t *)(base + L.ustart) : nullptr;
@@ -823,6 +842,18 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   if (pre_bytes >= budget) return SD_ERR_UNSUPPORTED;
   const int64_t lds_room = (int64_t)((budget - pre_bytes) / 4);
   const int lds_cap = (int)(want < lds_room ? want : lds_room);
+  // Few rows with many candidates each select them over several workgroups
+  // per row (unless the union attention needs each row's list read back by
+  // the selection).  The pieces' two kernels take about 16-18 us whatever
+  // the count; one workgroup per row takes 13 us for 2.5K candidates and 26
+  // us for 25K (1M-key group-shared batch of 8 rows: 26 -> 18 us).  Debug
+  // flags 16 / 32 turn the pieces off / on wherever they can apply.
+  {
+    const int dbg = g_debug.load();
+    const bool can = L.psel_parts > 0 && wide && !w.force_repair && L.union_chunk == 0;
+    const bool pays = cands >= kPieceCandidates;
+    if (can && !(dbg & 16) && (pays || (dbg & 32))) w.psel_parts = L.psel_parts;
+  }
   hipError_t e = mark(0);
   // (the pilot's thresholds and flags serve only the scoring stream)
   if (e == hipSuccess && !w.force_repair) e = sd::launch_pilot(p, w, stream_h);

@@ -26,6 +26,11 @@ constexpr int kSampleMax = 2048;   // pilot samples per row
 constexpr int kPartStride = kHeadDim + 2;  // (m, l, o[128]) per split partial
 constexpr int kDselPartsMax = 64;  // pieces of a row in the multi-workgroup fallback selection
 constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the fallback scoring
+constexpr int kPselPartsMax = 32;  // pieces of a row in the multi-workgroup candidate selection
+constexpr int kPselChunksMax = 64; // chunks per piece (at most)
+constexpr int kPselSlots = 4;      // candidates per thread a piece holds (1024 threads)
+constexpr int kPselRunMax = 4096;  // keys of the k-th run of 32 buckets a piece collects
+constexpr int kPselStride = 128;   // u32 per piece record (see Work::psel_rec)
 constexpr int kSelectWideRows = 256; // fewer rows: 1024-thread selection workgroups
 constexpr size_t kSelectShareLds = 70 * 1024;  // more dynamic LDS: one workgroup per CU
 constexpr int kDenseWaveKeysMax = 8192; // keys per work item of the dense decode kernel
@@ -117,6 +122,14 @@ struct Work {
   int32_t *dsel_state;  // [rows][4]: key prefix, its mask, rank still to place
   int2 *dsel_cnt;       // [rows][kDselPartsMax] (keys above, keys equal to) the threshold
   int32_t dsel_parts;
+  // Candidate selection over several workgroups per row (rows too few to
+  // fill the GPU one workgroup each): psel_parts pieces of consecutive
+  // chunks per row, 0 = one workgroup per row.  Record of piece j of a row:
+  // psel_rec[(row * psel_parts + j) * kPselStride + ...]: [0, 64) its
+  // candidates per run of 32 value buckets, [64] its candidate count, [65]
+  // its largest key.
+  uint32_t *psel_rec;
+  int32_t psel_parts;
   // Persistent scoring stream: one workgroup per compute unit takes units
   // (chunks) from a queue; k_pilot_select writes the work list and resets
   // the queue.  unit_pre[b] = units of the sequences before b (B + 1

@@ -1628,9 +1628,396 @@ __device__ __forceinline__ void kept_scores_to_weights(float *vrow, int k, float
   for (int i = threadIdx.x; i < k; i += NT) vrow[i] = kept_weight(vrow[i], m, c2);
 }
 
+// ---------------------------------------------------------------------------
+// Candidate selection of few rows over several workgroups each (rows too few
+// to fill the GPU one workgroup each).  A row's chunks are cut into
+// w.psel_parts pieces of consecutive chunks.  The value buckets are those of
+// select_regs (equal runs of keys from the row's threshold to its largest
+// pilot sample, known before the candidates), taken 32 at a time as "runs".
+//
+// k_psel_hist: each piece counts its candidates per run, writes the counts,
+// its candidate count and its largest key to its record, and copies its
+// keys grouped by run, the highest run first, into the row's fallback score
+// row from position c0 * chunk_keys (c0 its first chunk).  An unflagged row
+// does not use that row, and a piece's candidates are distinct positions of
+// its chunks, so the copy stays inside it.
+//
+// k_select then runs one workgroup per piece (piece_select): each sums the
+// pieces' run counts to find the run holding the k-th largest key, loads
+// that run's keys from every piece's copy (piece j's start there: its count
+// above the run) while its own candidates load, counts them per bucket for
+// the k-th bucket, ranks that bucket's keys for the threshold key T and the
+// number of keys equal to T that are kept, and writes its own kept
+// candidates in position order at the offset the pieces before it leave
+// (keys equal to T kept in position order across pieces).  The list is the
+// one a single workgroup writes.  Two dependent rounds of global loads,
+// where a single workgroup takes passes over all of a row's candidates.
+// grid: B*R*psel_parts workgroups (row-major), kBlock threads.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int piece_chunk(int nch, int parts, int j) {
+  return (int)((int64_t)j * nch / parts);
+}
+
+// The chunks [c0, c0 + nc) of a row: prefix sums of their candidate counts
+// (pre, nc + 1 entries) and their first block entries (start).  Run by the
+// block's first wave (nc <= 64).
+__device__ __forceinline__ void piece_directory(const Work &w, int row, int c0, int nc, int *pre,
+                                                int *start) {
+  const int lane = (int)threadIdx.x;
+  const int2 d = lane < nc ? w.dir[(int64_t)row * w.nchunk + c0 + lane] : make_int2(0, 0);
+  const int v = d.y > 0 ? d.y : 0;
+  const int inc = wave_incl_scan_dpp(v);
+  if (lane < nc) {
+    pre[lane] = inc - v;
+    start[lane] = d.x;
+  }
+  if (lane == 63) pre[nc] = inc;
+}
+
+__global__ __launch_bounds__(kBlock) void k_psel_hist(Params p, Work w) {
+  static_assert(kPselStride >= 66 && kBuckets == 64 * 32, "piece record: 64 runs of 32 buckets");
+  __shared__ uint32_t runs[64];
+  __shared__ int pre[kPselChunksMax + 1], start[kPselChunksMax];
+  __shared__ uint32_t kmax_sh;
+  const int parts = w.psel_parts;
+  const int row = (int)blockIdx.x / parts, piece = (int)blockIdx.x % parts;
+  const int b = row / p.R;
+  const int L = seq_len(p, b);
+  const RowPlan rp = row_plan(p, b, L);
+  if (rp.kh <= 0 || w.flags[row]) return;  // (no piece work for the row)
+  const int tid = threadIdx.x;
+  const int ck = w.chunk_keys;
+  const int nch = (L + ck - 1) / ck;
+  const int c0 = piece_chunk(nch, parts, piece);
+  const int nc = piece_chunk(nch, parts, piece + 1) - c0;  // <= kPselChunksMax (host)
+  if (tid < 64) {
+    runs[tid] = 0u;
+    if (tid == 0) kmax_sh = 0u;
+    piece_directory(w, row, c0, nc, pre, start);
+  }
+  __syncthreads();
+  const int n = pre[nc];
+  const int rr = row % p.R;
+  const int g = p.group_shared ? rr : rr / p.G;
+  const int64_t gblk = (((int64_t)b * p.Hkv + g) * w.nchunk + c0) * w.blk_cap;
+  const ChunkCands src{nullptr, pre, start, nc, w.ckey + gblk, w.cpos + gblk, ck, w.blk_cap};
+  const uint32_t lo = f2key(w.theta[row]), hi = f2key(w.smax[row]);
+  const KeyBuckets kb = KeyBuckets::make(lo, hi > lo ? hi - lo : 0u);
+  constexpr int kBatch = kBlock * kSelU;
+  auto load_keys = [&](int base, uint32_t (&key)[kSelU]) {
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u) {
+      const int i = base + u * kBlock + tid;
+      key[u] = i < n ? src.gkey[src.slot(src.chunk_of(i), i)] : 0u;
+    }
+  };
+  // The first batch stays in registers for the copy.
+  uint32_t key0[kSelU];
+  load_keys(0, key0);
+  uint32_t mx = 0u;
+  auto count = [&](int base, const uint32_t (&key)[kSelU]) {
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u)
+      if (base + u * kBlock + tid < n) {
+        atomicAdd(&runs[kb.of(key[u]) >> 5], 1u);
+        mx = key[u] > mx ? key[u] : mx;
+      }
+  };
+  count(0, key0);
+  for (int base = kBatch; base < n; base += kBatch) {
+    uint32_t key[kSelU];
+    load_keys(base, key);
+    count(base, key);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t t = (uint32_t)__shfl_xor((int)mx, o);
+    mx = t > mx ? t : mx;
+  }
+  if (lane_id() == 0) atomicMax(&kmax_sh, mx);
+  __syncthreads();
+  // The record; then each run's first slot in the copy, from the top run.
+  if (tid < 64) {
+    uint32_t *rec = w.psel_rec + ((int64_t)row * parts + piece) * kPselStride;
+    const uint32_t c = runs[63 - tid];
+    rec[63 - tid] = c;
+    if (tid == 0) {
+      rec[64] = (uint32_t)n;
+      rec[65] = kmax_sh;
+    }
+    const int inc = wave_incl_scan_dpp((int)c);
+    runs[63 - tid] = (uint32_t)inc - c;
+  }
+  __syncthreads();
+  uint32_t *copy = (uint32_t *)(w.dense + (int64_t)row * p.ncap) + (int64_t)c0 * ck;
+  auto scatter = [&](int base, const uint32_t (&key)[kSelU]) {
+#pragma unroll
+    for (int u = 0; u < kSelU; ++u)
+      if (base + u * kBlock + tid < n) copy[atomicAdd(&runs[kb.of(key[u]) >> 5], 1u)] = key[u];
+  };
+  scatter(0, key0);
+  for (int base = kBatch; base < n; base += kBatch) {
+    uint32_t key[kSelU];
+    load_keys(base, key);
+    scatter(base, key);
+  }
+}
+
+// Dynamic LDS of piece_select (NT threads).
+constexpr size_t psel_lds_bytes(int NT) {
+  return (size_t)(16 + kPselPartsMax * 64 + 64 + 2 * kPselPartsMax + 1 + 32 + 2 * kPselChunksMax + 1 +
+                  kPselRunMax + NT * kPselSlots) * 4 +
+         (size_t)kPselRunMax;
+}
+
+// Piece blockIdx.y of a row's candidate selection over w.psel_parts
+// workgroups (see k_psel_hist).  Returns false, having written nothing, when
+// the row is better selected by one workgroup: a piece holds more than
+// NT * kPselSlots candidates, the k-th run more than kPselRunMax, the k-th
+// bucket more than NT, or the candidates are fewer than k.  Every thread
+// must call it.
+template <int NT>
+__device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int row, int L, int k,
+                                             int32_t *irow, float *vrow, bool weights,
+                                             uint32_t *dyn, BucketShared<NT> *bs,
+                                             RegSelShared<NT> *rs) {
+  constexpr int NW = NT / 64;
+  const int P = w.psel_parts, piece = (int)blockIdx.y;
+  const int tid = threadIdx.x, lane = lane_id(), wv = wave_id();
+  int *ctl = (int *)dyn;                            // 16 words, below
+  uint32_t *suf = dyn + 16;                         // [P][64] counts from the top run down
+  uint32_t *colsum = suf + kPselPartsMax * 64;      // [64] run counts of the row
+  int *aq = (int *)(colsum + 64);                   // [P] candidates above the k-th run
+  int *ro = aq + kPselPartsMax;                     // [P + 1] k-th run's keys before the piece
+  uint32_t *fh = (uint32_t *)(ro + kPselPartsMax + 1);  // [32] the run's bucket counts
+  int *pre = (int *)(fh + 32);                      // [kPselChunksMax + 1]
+  int *start = pre + kPselChunksMax + 1;            // [kPselChunksMax]
+  uint32_t *runk = (uint32_t *)(start + kPselChunksMax);  // [kPselRunMax] the run's keys
+  uint32_t *pos_l = runk + kPselRunMax;             // [NT * kPselSlots] own positions
+  uint8_t *runq = (uint8_t *)(pos_l + NT * kPselSlots);  // [kPselRunMax] their pieces
+  enum { kRun, kAboveRun, kKmax, kR, kOk, kBstar, kKrem, kM, kT, kAboveT, kGtBefore, kEqBefore, kNb };
+  const uint32_t *rec0 = w.psel_rec + (int64_t)row * P * kPselStride;
+  const int ck = w.chunk_keys;
+  const int nch = (L + ck - 1) / ck;
+  const int c0 = piece_chunk(nch, P, piece);
+  const int nc = piece_chunk(nch, P, piece + 1) - c0;
+  const uint32_t lo = f2key(w.theta[row]), hi = f2key(w.smax[row]);
+  const KeyBuckets kb = KeyBuckets::make(lo, hi > lo ? hi - lo : 0u);
+  auto give_up = [&]() {
+    __syncthreads();  // (the caller reuses this LDS)
+    return false;
+  };
+  // 1. The own chunks' directory; every piece's run counts (per piece, the
+  // counts from the top run down to each run: one wave per piece, lane l on
+  // run 63 - l), their sums over the pieces, each piece's candidate count
+  // and largest key.
+  static_assert(kPselPartsMax * 64 <= 2 * NT, "two pieces per wave at most");
+  uint32_t c2[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int q = wv + h * NW;
+    c2[h] = q < P ? rec0[(int64_t)q * kPselStride + 63 - lane] : 0u;
+  }
+  int nv = 0;
+  uint32_t kv = 0u;
+  if (tid < P) {
+    nv = (int)rec0[(int64_t)tid * kPselStride + 64];
+    kv = rec0[(int64_t)tid * kPselStride + 65];
+  }
+  if (wv == 0) {
+    piece_directory(w, row, c0, nc, pre, start);
+    colsum[lane] = 0u;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int q = wv + h * NW;
+    if (q < P) {
+      suf[q * 64 + 63 - lane] = (uint32_t)wave_incl_scan_dpp((int)c2[h]);
+      atomicAdd(&colsum[63 - lane], c2[h]);
+    }
+  }
+  __syncthreads();
+  // 2. The run holding the k-th largest key (first wave, lane l on run
+  // 63 - l); each piece's candidates above it and the run's keys before it.
+  if (wv == 0) {
+    int nmax = nv, ntot = nv;
+    uint32_t km = kv;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const int a = __shfl_xor(nmax, o);
+      nmax = a > nmax ? a : nmax;
+      ntot += __shfl_xor(ntot, o);
+      const uint32_t t = (uint32_t)__shfl_xor((int)km, o);
+      km = t > km ? t : km;
+    }
+    const uint32_t v = colsum[63 - lane];
+    const int inc = wave_incl_scan_dpp((int)v);
+    const uint64_t hit = __ballot(inc >= k);
+    const bool ok = nmax <= NT * kPselSlots && ntot >= k && hit != 0;
+    const int l = hit ? __ffsll((unsigned long long)hit) - 1 : 0;
+    const int run = 63 - l;
+    const int above_run = __builtin_amdgcn_readlane(inc - (int)v, l);
+    int above = 0, rq = 0;
+    if (lane < P) {
+      above = run < 63 ? (int)suf[lane * 64 + run + 1] : 0;
+      rq = (int)suf[lane * 64 + run] - above;
+      aq[lane] = above;
+    }
+    const int ri = wave_incl_scan_dpp(rq);
+    if (lane < P) ro[lane] = ri - rq;
+    if (lane < 32) fh[lane] = 0u;
+    if (lane == 63) {
+      ro[P] = ri;
+      ctl[kR] = ri;
+    }
+    if (lane == 0) {
+      ctl[kOk] = ok ? 1 : 0;
+      ctl[kRun] = run;
+      ctl[kAboveRun] = above_run;
+      ctl[kKmax] = (int)km;
+      ctl[kNb] = 0;
+      ctl[kGtBefore] = 0;
+      ctl[kEqBefore] = 0;
+    }
+  }
+  __syncthreads();
+  const int R = ctl[kR], run = ctl[kRun];
+  if (!ctl[kOk] || R > kPselRunMax) return give_up();
+  // 3. The run's keys from the pieces' copies, while the own candidates
+  // load; the run's bucket counts.
+  const float *drow = w.dense + (int64_t)row * p.ncap;
+  constexpr int kRunU = kPselRunMax / NT;
+  uint32_t rk[kRunU];
+  int rqi[kRunU];
+#pragma unroll
+  for (int u = 0; u < kRunU; ++u) {
+    const int i = u * NT + tid;
+    rk[u] = 0u;
+    rqi[u] = 0;
+    if (i < R) {
+      int q = 0, qh = P - 1;  // the last piece whose run keys start at or before i
+      while (q < qh) {
+        const int mid = (q + qh + 1) >> 1;
+        if (ro[mid] <= i) q = mid; else qh = mid - 1;
+      }
+      rqi[u] = q;
+      rk[u] = ((const uint32_t *)drow)[(int64_t)piece_chunk(nch, P, q) * ck + aq[q] + (i - ro[q])];
+    }
+  }
+  const int n_own = pre[nc];
+  const int rr = row % p.R;
+  const int g = p.group_shared ? rr : rr / p.G;
+  const int64_t gblk = (((int64_t)(row / p.R) * p.Hkv + g) * w.nchunk + c0) * w.blk_cap;
+  const ChunkCands src{nullptr, pre, start, nc, w.ckey + gblk, w.cpos + gblk, ck, w.blk_cap};
+  const RegShare shr = reg_share<NT>(0, n_own);
+  uint32_t key[kPselSlots];
+  reg_load<kPselSlots>(src, shr, 0, key, pos_l, rs->sink, [](uint32_t, bool) {});
+#pragma unroll
+  for (int u = 0; u < kRunU; ++u) {
+    const int i = u * NT + tid;
+    if (i < R) {
+      runk[i] = rk[u];
+      runq[i] = (uint8_t)rqi[u];
+      atomicAdd(&fh[kb.of(rk[u]) - run * 32], 1u);
+    }
+  }
+  __syncthreads();
+  // 4. The k-th bucket (first wave, lane j summing bucket 31 - j of the run).
+  if (wv == 0) {
+    const uint32_t v = lane < 32 ? fh[31 - lane] : 0u;
+    const int inc = wave_incl_scan_dpp((int)v) + ctl[kAboveRun];
+    const uint64_t hit = __ballot(lane < 32 && inc >= k);
+    const int l = __ffsll((unsigned long long)hit) - 1;
+    if (lane == l) {
+      ctl[kOk] = (int)v <= NT ? 1 : 0;
+      ctl[kBstar] = run * 32 + 31 - l;
+      ctl[kKrem] = k - (inc - (int)v);
+      ctl[kM] = (int)v;
+    }
+  }
+  __syncthreads();
+  if (!ctl[kOk]) return give_up();
+  const int bstar = ctl[kBstar], krem = ctl[kKrem], m = ctl[kM];
+  // 5. The k-th bucket's keys; the own positions become row positions.
+  for (int i = tid; i < R; i += NT) {
+    const uint32_t x = runk[i];
+    if (kb.of(x) == bstar) bs->items[atomicAdd(&ctl[kNb], 1)] = x;
+  }
+  for (int i = tid; i < n_own; i += NT) pos_l[i] += (uint32_t)(c0 * ck);
+  __syncthreads();
+  // 6. The krem-th largest of them: T (equal keys agree).
+  if (tid < m) {
+    const uint32_t x = bs->items[tid];
+    int gt = 0, ge = 0;
+    for (int y = 0; y < m; ++y) {
+      const uint32_t v = bs->items[y];
+      gt += v > x ? 1 : 0;
+      ge += v >= x ? 1 : 0;
+    }
+    if (gt < krem && krem <= ge) {
+      ctl[kT] = (int)x;
+      ctl[kAboveT] = gt;
+    }
+  }
+  __syncthreads();
+  const uint32_t T = (uint32_t)ctl[kT];
+  const int need_eq = krem - ctl[kAboveT];
+  // 7. Kept keys before this piece (above T, equal to T: the pieces'
+  // candidates above the run, and the run's keys) and before each wave.
+  {
+    int gt_p = tid < piece ? aq[tid] : 0, eq_p = 0;
+    for (int i = tid; i < R; i += NT) {
+      const uint32_t x = runk[i];
+      const bool before = (int)runq[i] < piece;
+      gt_p += before && x > T ? 1 : 0;
+      eq_p += before && x == T ? 1 : 0;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      gt_p += __shfl_xor(gt_p, o);
+      eq_p += __shfl_xor(eq_p, o);
+    }
+    if (lane == 0 && (gt_p | eq_p)) {
+      atomicAdd(&ctl[kGtBefore], gt_p);
+      atomicAdd(&ctl[kEqBefore], eq_p);
+    }
+  }
+  int gt_w = 0, eq_w = 0;
+  unroll_for<kPselSlots>([&](auto uc) {
+    constexpr int u = decltype(uc)::value;
+    if (u < shr.U) {
+      const bool valid = shr.i0 + 64 * u + lane < shr.i1;
+      const uint32_t x = fresh(key[u]);
+      gt_w += __popcll(__ballot(valid && x > T));
+      eq_w += __popcll(__ballot(valid && x == T));
+    }
+  });
+  if (lane == 0) {
+    rs->gt[wv] = (uint32_t)gt_w;
+    rs->eq[wv] = (uint32_t)eq_w;
+  }
+  __syncthreads();
+  int gt_b = ctl[kGtBefore], eq_b = ctl[kEqBefore];
+#pragma unroll
+  for (int v = 0; v < NW; ++v)
+    if (v < wv) {
+      gt_b += (int)rs->gt[v];
+      eq_b += (int)rs->eq[v];
+    }
+  // 8. The own kept keys in position order.
+  reg_emit<kPselSlots>(key, shr, 0, T, need_eq, eq_b, gt_b + min(eq_b, need_eq), k, eq_w > 0,
+                       pos_l, irow, vrow, weights, key2f((uint32_t)ctl[kKmax]),
+                       weight_factor(p.scale));
+  return true;
+}
+
 // NT threads per workgroup: 256, or 1024 when the rows are too few to fill
 // the GPU one workgroup each (every per-thread loop is then 4x shorter).
-template <int MODE, int NT>
+// PIECES: the launch has w.psel_parts workgroups per row (gridDim.y), and
+// rows it can select in pieces are (a separate instance, so that the
+// one-workgroup instances keep their register allocation).
+template <int MODE, int NT, bool PIECES = false>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_select(Params p, Work w, const float *dense, int64_t ld,
                                                int32_t *idx, float *vals, int lds_cap) {
   extern __shared__ uint32_t dyn[];
@@ -1658,11 +2045,19 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_
   const int tid = threadIdx.x;
   if (k > 0) {
     if (MODE == 0 && w.flags[row]) {  // the exact fallback: full scores
+      if (blockIdx.y > 0) return;  // (one workgroup per row)
       if (tid == 0) atomicAdd(&w.stats[0], 1);
       if (!w.dsel_parts)  // (else the k_dsel kernels wrote the selection)
         select_and_write<NT>(DenseSrc{w.dense + (int64_t)row * p.ncap + rp.lo, (uint32_t)rp.lo},
                              rp.hi - rp.lo, k, hist, &sh, irow, vrow);
+    } else if (MODE == 0 && [&] {
+                 if constexpr (PIECES)
+                   return piece_select<NT>(p, w, row, L, k, irow, vrow, weights, dyn, &bs, &rsh);
+                 return false;
+               }()) {
+      weights_done = true;  // (the pieces wrote weights when they were asked for)
     } else if (MODE == 0) {
+      if (blockIdx.y > 0) return;  // the row is selected by its first piece alone
       // Candidates: at least k of them and no overflow (else flagged).
       const int ck = w.chunk_keys;
       const int nch = (L + ck - 1) / ck;
@@ -1714,6 +2109,7 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_
     }
     if (weights && !weights_done) kept_scores_to_weights<NT>(vrow, k, p.scale, ftmp);
   }
+  if (blockIdx.y > 0) return;  // (the rest of the list: the row's first piece)
   // Forced positions (their scores, for the stand-alone selection), then
   // the padding.
   for (int i = tid; i < rp.ns + rp.nl; i += NT) {
@@ -2557,7 +2953,12 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
   // The kept scores / weights only serve an attention that does not
   // recompute its logits.
   float *vals = attend_recompute(true, p) ? nullptr : w.sigma;
-  if (wide)
+  if (w.psel_parts > 0) {  // (wide: the host asks for pieces only then)
+    k_psel_hist<<<rows * (unsigned)w.psel_parts, kBlock, 0, st>>>(p, w);
+    const size_t plds = psel_lds_bytes(1024);
+    k_select<0, 1024, true><<<dim3(rows, (unsigned)w.psel_parts), 1024, lds > plds ? lds : plds, st>>>(
+        p, w, nullptr, 0, idx, vals, lds_cap);
+  } else if (wide)
     k_select<0, 1024><<<rows, 1024, lds, st>>>(p, w, nullptr, 0, idx, vals, lds_cap);
   else
     k_select<0, kBlock><<<rows, kBlock, lds, st>>>(p, w, nullptr, 0, idx, vals, lds_cap);
