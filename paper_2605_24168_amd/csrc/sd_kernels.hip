@@ -1056,6 +1056,18 @@ __global__ __launch_bounds__(kBlock) void k_score_dense(Params p, float *dst, in
 // per-chunk counts (part 0 records them in w.flags for the selection) and,
 // when a row of the group is flagged, scores its part of the group into
 // w.dense.
+// LDS of piece_hist.
+struct PieceHistLds {
+  uint32_t runs[64];
+  int pre[kPselChunksMax + 1], start[kPselChunksMax];
+  uint32_t kmax;
+};
+
+// One piece of a row's candidate selection over several workgroups (defined
+// with the selection below).
+__device__ __forceinline__ void piece_hist(const Params &p, const Work &w, int row, int piece,
+                                           PieceHistLds &sh);
+
 template <bool BF16, bool LABEL, bool PIPE>
 __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
   __shared__ float q_lds[BF16 ? 1 : kMaxGroup * kHeadDim];
@@ -1097,6 +1109,15 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
     if (part == 0) w.flags[row0 + tid] = flag ? 1 : 0;
   }
   __syncthreads();
+  // The pieces of the group's unflagged rows (candidate selection over
+  // several workgroups per row), one task per workgroup of the group.
+  if (w.psel_parts > 0 && k > 0) {
+    __shared__ PieceHistLds ph;
+    for (int t = part; t < nrows * w.psel_parts; t += (int)gridDim.x) {
+      const int r = t / w.psel_parts;
+      if (!(bad[r] || cnt[r] < k)) piece_hist(p, w, (int)row0 + r, t % w.psel_parts, ph);
+    }
+  }
   if (any)
     dense_scores<BF16, LABEL, PIPE>(p, w.dense, p.ncap, b, g, part, (int)gridDim.x, false, q_lds);
 }
@@ -1635,7 +1656,8 @@ __device__ __forceinline__ void kept_scores_to_weights(float *vrow, int k, float
 // select_regs (equal runs of keys from the row's threshold to its largest
 // pilot sample, known before the candidates), taken 32 at a time as "runs".
 //
-// k_psel_hist: each piece counts its candidates per run, writes the counts,
+// piece_hist (in k_repair_score's launch, which settles the rows' flags):
+// each piece counts its candidates per run, writes the counts,
 // its candidate count and its largest key to its record, and copies its
 // keys grouped by run, the highest run first, into the row's fallback score
 // row from position c0 * chunk_keys (c0 its first chunk).  An unflagged row
@@ -1652,7 +1674,6 @@ __device__ __forceinline__ void kept_scores_to_weights(float *vrow, int k, float
 // (keys equal to T kept in position order across pieces).  The list is the
 // one a single workgroup writes.  Two dependent rounds of global loads,
 // where a single workgroup takes passes over all of a row's candidates.
-// grid: B*R*psel_parts workgroups (row-major), kBlock threads.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int piece_chunk(int nch, int parts, int j) {
   return (int)((int64_t)j * nch / parts);
@@ -1674,33 +1695,32 @@ __device__ __forceinline__ void piece_directory(const Work &w, int row, int c0, 
   if (lane == 63) pre[nc] = inc;
 }
 
-__global__ __launch_bounds__(kBlock) void k_psel_hist(Params p, Work w) {
+// Piece `piece` of an unflagged row with a positive budget: its record and
+// its run-grouped copy (see above).  Every thread of the block must call it
+// (kBlock threads).
+__device__ __forceinline__ void piece_hist(const Params &p, const Work &w, int row, int piece,
+                                           PieceHistLds &sh) {
   static_assert(kPselStride >= 66 && kBuckets == 64 * 32, "piece record: 64 runs of 32 buckets");
-  __shared__ uint32_t runs[64];
-  __shared__ int pre[kPselChunksMax + 1], start[kPselChunksMax];
-  __shared__ uint32_t kmax_sh;
   const int parts = w.psel_parts;
-  const int row = (int)blockIdx.x / parts, piece = (int)blockIdx.x % parts;
   const int b = row / p.R;
   const int L = seq_len(p, b);
-  const RowPlan rp = row_plan(p, b, L);
-  if (rp.kh <= 0 || w.flags[row]) return;  // (no piece work for the row)
   const int tid = threadIdx.x;
   const int ck = w.chunk_keys;
   const int nch = (L + ck - 1) / ck;
   const int c0 = piece_chunk(nch, parts, piece);
   const int nc = piece_chunk(nch, parts, piece + 1) - c0;  // <= kPselChunksMax (host)
+  __syncthreads();  // (sh's previous readers are done)
   if (tid < 64) {
-    runs[tid] = 0u;
-    if (tid == 0) kmax_sh = 0u;
-    piece_directory(w, row, c0, nc, pre, start);
+    sh.runs[tid] = 0u;
+    if (tid == 0) sh.kmax = 0u;
+    piece_directory(w, row, c0, nc, sh.pre, sh.start);
   }
   __syncthreads();
-  const int n = pre[nc];
+  const int n = sh.pre[nc];
   const int rr = row % p.R;
   const int g = p.group_shared ? rr : rr / p.G;
   const int64_t gblk = (((int64_t)b * p.Hkv + g) * w.nchunk + c0) * w.blk_cap;
-  const ChunkCands src{nullptr, pre, start, nc, w.ckey + gblk, w.cpos + gblk, ck, w.blk_cap};
+  const ChunkCands src{nullptr, sh.pre, sh.start, nc, w.ckey + gblk, w.cpos + gblk, ck, w.blk_cap};
   const uint32_t lo = f2key(w.theta[row]), hi = f2key(w.smax[row]);
   const KeyBuckets kb = KeyBuckets::make(lo, hi > lo ? hi - lo : 0u);
   constexpr int kBatch = kBlock * kSelU;
@@ -1719,7 +1739,7 @@ __global__ __launch_bounds__(kBlock) void k_psel_hist(Params p, Work w) {
 #pragma unroll
     for (int u = 0; u < kSelU; ++u)
       if (base + u * kBlock + tid < n) {
-        atomicAdd(&runs[kb.of(key[u]) >> 5], 1u);
+        atomicAdd(&sh.runs[kb.of(key[u]) >> 5], 1u);
         mx = key[u] > mx ? key[u] : mx;
       }
   };
@@ -1734,26 +1754,26 @@ __global__ __launch_bounds__(kBlock) void k_psel_hist(Params p, Work w) {
     const uint32_t t = (uint32_t)__shfl_xor((int)mx, o);
     mx = t > mx ? t : mx;
   }
-  if (lane_id() == 0) atomicMax(&kmax_sh, mx);
+  if (lane_id() == 0) atomicMax(&sh.kmax, mx);
   __syncthreads();
   // The record; then each run's first slot in the copy, from the top run.
   if (tid < 64) {
     uint32_t *rec = w.psel_rec + ((int64_t)row * parts + piece) * kPselStride;
-    const uint32_t c = runs[63 - tid];
+    const uint32_t c = sh.runs[63 - tid];
     rec[63 - tid] = c;
     if (tid == 0) {
       rec[64] = (uint32_t)n;
-      rec[65] = kmax_sh;
+      rec[65] = sh.kmax;
     }
     const int inc = wave_incl_scan_dpp((int)c);
-    runs[63 - tid] = (uint32_t)inc - c;
+    sh.runs[63 - tid] = (uint32_t)inc - c;
   }
   __syncthreads();
   uint32_t *copy = (uint32_t *)(w.dense + (int64_t)row * p.ncap) + (int64_t)c0 * ck;
   auto scatter = [&](int base, const uint32_t (&key)[kSelU]) {
 #pragma unroll
     for (int u = 0; u < kSelU; ++u)
-      if (base + u * kBlock + tid < n) copy[atomicAdd(&runs[kb.of(key[u]) >> 5], 1u)] = key[u];
+      if (base + u * kBlock + tid < n) copy[atomicAdd(&sh.runs[kb.of(key[u]) >> 5], 1u)] = key[u];
   };
   scatter(0, key0);
   for (int base = kBatch; base < n; base += kBatch) {
@@ -1771,7 +1791,7 @@ constexpr size_t psel_lds_bytes(int NT) {
 }
 
 // Piece blockIdx.y of a row's candidate selection over w.psel_parts
-// workgroups (see k_psel_hist).  Returns false, having written nothing, when
+// workgroups (see piece_hist).  Returns false, having written nothing, when
 // the row is better selected by one workgroup: a piece holds more than
 // NT * kPselSlots candidates, the k-th run more than kPselRunMax, the k-th
 // bucket more than NT, or the candidates are fewer than k.  Every thread
@@ -2954,7 +2974,6 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
   // recompute its logits.
   float *vals = attend_recompute(true, p) ? nullptr : w.sigma;
   if (w.psel_parts > 0) {  // (wide: the host asks for pieces only then)
-    k_psel_hist<<<rows * (unsigned)w.psel_parts, kBlock, 0, st>>>(p, w);
     const size_t plds = psel_lds_bytes(1024);
     k_select<0, 1024, true><<<dim3(rows, (unsigned)w.psel_parts), 1024, lds > plds ? lds : plds, st>>>(
         p, w, nullptr, 0, idx, vals, lds_cap);
@@ -2976,8 +2995,13 @@ hipError_t launch_select_candidates(const Params &p, const Work &w, int32_t *idx
 int repair_parts(const Params &p, const Work &w) {
   const int groups = p.B * p.Hkv;
   if (!w.force_repair) {
-    const int parts = (1024 + groups - 1) / groups;
-    return parts < kRepairParts ? parts : kRepairParts;
+    int parts = (1024 + groups - 1) / groups;
+    parts = parts < kRepairParts ? parts : kRepairParts;
+    // With the candidate selection in pieces, a workgroup per piece of the
+    // group's rows (their histograms run in this launch), up to 64.
+    const int tasks = (p.group_shared ? 1 : p.G) * w.psel_parts;
+    const int want = tasks < 64 ? tasks : 64;
+    return parts > want ? parts : want;
   }
   int parts = (2048 + groups - 1) / groups;
   parts = parts < kRepairParts ? kRepairParts : parts;

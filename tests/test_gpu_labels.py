@@ -235,3 +235,17 @@ def test_label_indexer_full_size_on_sampled_sequences(sd, cfg, ratio, sample):
     sub = P.slice_batch(inp, sample)
     sub_lab = lab if inp.layout == "paged" else lab[sample]
     check(sub, ch, sub_lab, out[sample], idx[sample], f"labels full workload {cfg}")
+
+
+@pytest.mark.parametrize("name", ["w2", "w4", "w5"])
+def test_label_indexer_selection_in_pieces(sd, name):
+    # Few rows: the candidate selection over several workgroups per row
+    # (debug flag 32; flag 4 keeps per-head lists, which it needs) writes
+    # the lists of one workgroup per row (flag 16) bit for bit, and matches
+    # the oracle.
+    inp, ch, lab = make(name, seed=5, B=2) if name != "w5" else make(name, seed=5)
+    out, idx, _ = _with_debug(sd, 32 | 4, lambda: run(sd, inp, ch, lab))
+    out2, idx2, _ = _with_debug(sd, 16 | 4, lambda: run(sd, inp, ch, lab))
+    np.testing.assert_array_equal(idx, idx2)
+    np.testing.assert_array_equal(out, out2)
+    check(inp, ch, lab, out, idx, f"labels in pieces {name}")
