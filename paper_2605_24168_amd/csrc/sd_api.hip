@@ -308,6 +308,7 @@ int psel_parts_for(const Shape &s, int nchunk) {
 
 constexpr int64_t kManyCandidates = 48 * 1024;
 constexpr int64_t kPieceCandidates = 8 * 1024;  // fewest candidates per row worth the pieces
+constexpr int64_t kPieceItems = 3 * 1024;       // most expected candidates per piece
 
 // Whether the pilot would send a row of the full capacity to the exact
 // fallback (its rule: the expected candidates of a scoring wave would fill
@@ -844,14 +845,18 @@ sd_status attention_impl(const sd_tensor *q, const sd_kv *K, const sd_kv *V,
   const int lds_cap = (int)(want < lds_room ? want : lds_room);
   // Few rows with many candidates each select them over several workgroups
   // per row (unless the union attention needs each row's list read back by
-  // the selection).  The pieces' two kernels take about 16-18 us whatever
-  // the count; one workgroup per row takes 13 us for 2.5K candidates and 26
-  // us for 25K (1M-key group-shared batch of 8 rows: 26 -> 18 us).  Debug
-  // flags 16 / 32 turn the pieces off / on wherever they can apply.
+  // the selection).  The pieces take about 12-16 us whatever the count; one
+  // workgroup per row takes 13 us for 2.5K candidates and 26 us for 25K
+  // (1M-key group-shared batch of 8 rows: 26 -> 12 us).  A piece holds at
+  // most kPselItemsMax candidates (beyond, the row goes back to one
+  // workgroup after the pieces' work: 128 label rows of 16K candidates in
+  // two pieces each took 30 us more), so the expected count per piece must
+  // stay well below it.  Debug flags 16 / 32 turn the pieces off / on
+  // wherever they can apply.
   {
     const int dbg = g_debug.load();
     const bool can = L.psel_parts > 0 && wide && !w.force_repair && L.union_chunk == 0;
-    const bool pays = cands >= kPieceCandidates;
+    const bool pays = cands >= kPieceCandidates && cands <= (int64_t)L.psel_parts * kPieceItems;
     if (can && !(dbg & 16) && (pays || (dbg & 32))) w.psel_parts = L.psel_parts;
   }
   hipError_t e = mark(0);

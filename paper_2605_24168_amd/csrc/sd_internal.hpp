@@ -29,6 +29,7 @@ constexpr int kRepairParts = 16;   // work items per (sequence, KV head) of the 
 constexpr int kPselPartsMax = 32;  // pieces of a row in the multi-workgroup candidate selection
 constexpr int kPselChunksMax = 64; // chunks per piece (at most)
 constexpr int kPselSlots = 4;      // candidates per thread a piece holds (1024 threads)
+constexpr int kPselItemsMax = 1024 * kPselSlots;  // candidates of a piece, at most
 constexpr int kPselRunMax = 4096;  // keys of the k-th run of 32 buckets a piece collects
 constexpr int kPselStride = 128;   // u32 per piece record (see Work::psel_rec)
 constexpr int kSelectWideRows = 256; // fewer rows: 1024-thread selection workgroups

@@ -1717,6 +1717,11 @@ __device__ __forceinline__ void piece_hist(const Params &p, const Work &w, int r
   }
   __syncthreads();
   const int n = sh.pre[nc];
+  uint32_t *rec = w.psel_rec + ((int64_t)row * parts + piece) * kPselStride;
+  if (n > kPselItemsMax) {  // the row goes back to one workgroup: its count is all it needs
+    if (tid == 0) rec[64] = (uint32_t)n;
+    return;
+  }
   const int rr = row % p.R;
   const int g = p.group_shared ? rr : rr / p.G;
   const int64_t gblk = (((int64_t)b * p.Hkv + g) * w.nchunk + c0) * w.blk_cap;
@@ -1758,7 +1763,6 @@ __device__ __forceinline__ void piece_hist(const Params &p, const Work &w, int r
   __syncthreads();
   // The record; then each run's first slot in the copy, from the top run.
   if (tid < 64) {
-    uint32_t *rec = w.psel_rec + ((int64_t)row * parts + piece) * kPselStride;
     const uint32_t c = sh.runs[63 - tid];
     rec[63 - tid] = c;
     if (tid == 0) {
@@ -1793,7 +1797,8 @@ constexpr size_t psel_lds_bytes(int NT) {
 // Piece blockIdx.y of a row's candidate selection over w.psel_parts
 // workgroups (see piece_hist).  Returns false, having written nothing, when
 // the row is better selected by one workgroup: a piece holds more than
-// NT * kPselSlots candidates, the k-th run more than kPselRunMax, the k-th
+// kPselItemsMax candidates (its record then holds its count alone), the
+// k-th run more than kPselRunMax, the k-th
 // bucket more than NT, or the candidates are fewer than k.  Every thread
 // must call it.
 template <int NT>
@@ -1832,6 +1837,7 @@ __device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int
   // run 63 - l), their sums over the pieces, each piece's candidate count
   // and largest key.
   static_assert(kPselPartsMax * 64 <= 2 * NT, "two pieces per wave at most");
+  static_assert(NT * kPselSlots == kPselItemsMax, "a piece's candidates fit the registers");
   uint32_t c2[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -1874,7 +1880,7 @@ __device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int
     const uint32_t v = colsum[63 - lane];
     const int inc = wave_incl_scan_dpp((int)v);
     const uint64_t hit = __ballot(inc >= k);
-    const bool ok = nmax <= NT * kPselSlots && ntot >= k && hit != 0;
+    const bool ok = nmax <= kPselItemsMax && ntot >= k && hit != 0;
     const int l = hit ? __ffsll((unsigned long long)hit) - 1 : 0;
     const int run = 63 - l;
     const int above_run = __builtin_amdgcn_readlane(inc - (int)v, l);
