@@ -12,9 +12,12 @@
 //                   above the threshold in LDS in position order (ballots,
 //                   no atomics) and writes one packed block per workgroup
 //   k_repair_score  flags the rows whose candidates cannot prove exactness
-//                   and scores their groups in full (the exact fallback)
-//   k_select        exact top-k: over the candidates, or over the full
-//                   scores for a flagged row
+//                   and scores their groups in full (the exact fallback);
+//                   with few rows, also the per-piece run counts of the
+//                   candidate selection in pieces
+//   k_select        exact top-k: over the candidates (with few rows of many
+//                   candidates, one workgroup per piece of a row), or over
+//                   the full scores for a flagged row
 //   k_attend        gathers the kept value rows, split over workgroups
 //   k_merge         combines the splits' (max, sum, output) partials by
 //                   log-sum-exp (only when a row is split)

@@ -154,3 +154,25 @@ def test_sampled_full_size_on_sampled_sequences(sd):
     sample = [0, 15]
     check(P.slice_batch(inp, sample), draws[sample], out[sample], idx[sample], w[sample],
           "sampled full workload 3")
+
+
+def test_sampled_selection_with_the_exact_part_in_pieces(sd):
+    # Few rows: the exact part selected over several workgroups per row
+    # (debug flag 32) gives the lists, weights and output of one workgroup
+    # per row (flag 16) bit for bit, and the oracle's.
+    inp = make("w2", seed=9)
+    draws = random_draws(inp, 64, seed=9)
+    sd.set_debug(32)
+    try:
+        out, idx, w = run(sd, inp, draws)
+    finally:
+        sd.set_debug(0)
+    sd.set_debug(16)
+    try:
+        out2, idx2, w2 = run(sd, inp, draws)
+    finally:
+        sd.set_debug(0)
+    np.testing.assert_array_equal(idx, idx2)
+    np.testing.assert_array_equal(w, w2)
+    np.testing.assert_array_equal(out, out2)
+    check(inp, draws, out, idx, w, "sampled, exact part in pieces")
