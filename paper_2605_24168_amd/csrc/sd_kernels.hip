@@ -1112,13 +1112,15 @@ __global__ __launch_bounds__(kBlock) void k_repair_score(Params p, Work w) {
     if (part == 0) w.flags[row0 + tid] = flag ? 1 : 0;
   }
   __syncthreads();
-  // The pieces of the group's unflagged rows (candidate selection over
-  // several workgroups per row), one task per workgroup of the group.
-  if (w.psel_parts > 0 && k > 0) {
+  // The pieces of the group's rows (candidate selection over several
+  // workgroups per row), one task per workgroup of the group; none when a
+  // row of the group is flagged, since the group's full scoring below then
+  // writes the score rows the pieces would copy their keys to.
+  if (w.psel_parts > 0 && k > 0 && !any) {
     __shared__ PieceHistLds ph;
     for (int t = part; t < nrows * w.psel_parts; t += (int)gridDim.x) {
       const int r = t / w.psel_parts;
-      if (!(bad[r] || cnt[r] < k)) piece_hist(p, w, (int)row0 + r, t % w.psel_parts, ph);
+      piece_hist(p, w, (int)row0 + r, t % w.psel_parts, ph);
     }
   }
   if (any)
@@ -1853,6 +1855,12 @@ __device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int
     nv = (int)rec0[(int64_t)tid * kPselStride + 64];
     kv = rec0[(int64_t)tid * kPselStride + 65];
   }
+  // The rows of the KV group: with one of them flagged, the pieces of the
+  // group wrote nothing (the repair's full scoring of the group takes their
+  // copy space), and the row goes back to one workgroup.
+  const int grows = p.group_shared ? 1 : p.G;
+  const int64_t grow0 = (int64_t)(row / p.R) * p.R + (p.group_shared ? row % p.R : (row % p.R) / p.G * p.G);
+  const int gflag = tid < grows ? w.flags[grow0 + tid] : 0;
   if (wv == 0) {
     piece_directory(w, row, c0, nc, pre, start);
     colsum[lane] = 0u;
@@ -1883,7 +1891,7 @@ __device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int
     const uint32_t v = colsum[63 - lane];
     const int inc = wave_incl_scan_dpp((int)v);
     const uint64_t hit = __ballot(inc >= k);
-    const bool ok = nmax <= kPselItemsMax && ntot >= k && hit != 0;
+    const bool ok = nmax <= kPselItemsMax && ntot >= k && hit != 0 && __ballot(gflag != 0) == 0;
     const int l = hit ? __ffsll((unsigned long long)hit) - 1 : 0;
     const int run = 63 - l;
     const int above_run = __builtin_amdgcn_readlane(inc - (int)v, l);

@@ -131,3 +131,30 @@ def test_pieces_repeat_calls_of_different_shapes(sd):
         out_b, idx_b = run(sd, inp, PIECES_OFF)
         np.testing.assert_array_equal(idx_a, idx_b)
         np.testing.assert_array_equal(out_a, out_b)
+
+
+def test_pieces_beside_rows_on_the_exact_fallback(sd):
+    # A cluster of 400 keys close to head 0's query overflows that row's
+    # staging area, so it takes the exact fallback (its first piece selects
+    # it from full scores) while the call's other rows are selected in
+    # pieces; lists and outputs equal the one-workgroup call's and the
+    # oracle's.
+    inp = synth.make_inputs(2, seed=15, B=1, N=12000, ratio=50.0, Hq=64, Hkv=8)
+    rng = np.random.default_rng(15)
+    q0 = synth.bf16_to_f32(inp.q[0, 0]).astype(np.float64)
+    base = 3.0 * q0 / np.linalg.norm(q0) * np.sqrt(inp.d)
+    clus = base[None, :] + 0.3 * rng.standard_normal((400, inp.d))
+    k = inp.k.copy()
+    k[0, 0, 100:500] = synth.bf16_bits(clus.astype(np.float32))
+    inp = dataclasses.replace(inp, k=k)
+    sd.set_profiling(True)
+    try:
+        out_a, idx_a = run(sd, inp, PIECES_ON)
+        prof = sd.last_profile()
+    finally:
+        sd.set_profiling(False)
+    assert prof["repaired_rows"] >= 1
+    out_b, idx_b = run(sd, inp, PIECES_OFF)
+    np.testing.assert_array_equal(idx_a, idx_b)
+    np.testing.assert_array_equal(out_a, out_b)
+    check_oracle(inp, out_a, idx_a, "fallback row beside pieces")
