@@ -1795,7 +1795,7 @@ __device__ __forceinline__ void piece_hist(const Params &p, const Work &w, int r
 // Dynamic LDS of piece_select (NT threads).
 constexpr size_t psel_lds_bytes(int NT) {
   return (size_t)(16 + kPselPartsMax * 64 + 64 + 2 * kPselPartsMax + 1 + 32 + 2 * kPselChunksMax + 1 +
-                  kPselRunMax + NT * kPselSlots) * 4 +
+                  2 * kPselRunMax + NT * kPselSlots) * 4 +
          (size_t)kPselRunMax;
 }
 
@@ -1803,13 +1803,16 @@ constexpr size_t psel_lds_bytes(int NT) {
 // workgroups (see piece_hist).  Returns false, having written nothing, when
 // the row is better selected by one workgroup: a piece holds more than
 // kPselItemsMax candidates (its record then holds its count alone), the
-// k-th run more than kPselRunMax, the k-th
-// bucket more than NT, or the candidates are fewer than k.  Every thread
-// must call it.
+// k-th run more than kPselRunMax keys, a row of its KV group is flagged,
+// or the candidates are fewer than k.  Every piece decides this before any
+// of them reads another's copy, so the row's first piece, selecting it
+// alone, may then use the row's score row as scratch.  hist, sh: the
+// selection's LDS (the radix passes of a crowded k-th bucket).  Every
+// thread must call it.
 template <int NT>
 __device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int row, int L, int k,
                                              int32_t *irow, float *vrow, bool weights,
-                                             uint32_t *dyn, BucketShared<NT> *bs,
+                                             uint32_t *dyn, uint32_t *hist, SelShared *sh,
                                              RegSelShared<NT> *rs) {
   constexpr int NW = NT / 64;
   const int P = w.psel_parts, piece = (int)blockIdx.y;
@@ -1823,7 +1826,8 @@ __device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int
   int *pre = (int *)(fh + 32);                      // [kPselChunksMax + 1]
   int *start = pre + kPselChunksMax + 1;            // [kPselChunksMax]
   uint32_t *runk = (uint32_t *)(start + kPselChunksMax);  // [kPselRunMax] the run's keys
-  uint32_t *pos_l = runk + kPselRunMax;             // [NT * kPselSlots] own positions
+  uint32_t *bkeys = runk + kPselRunMax;             // [kPselRunMax] the k-th bucket's keys
+  uint32_t *pos_l = bkeys + kPselRunMax;            // [NT * kPselSlots] own positions
   uint8_t *runq = (uint8_t *)(pos_l + NT * kPselSlots);  // [kPselRunMax] their pieces
   enum { kRun, kAboveRun, kKmax, kR, kOk, kBstar, kKrem, kM, kT, kAboveT, kGtBefore, kEqBefore, kNb };
   const uint32_t *rec0 = w.psel_rec + (int64_t)row * P * kPselStride;
@@ -1967,34 +1971,44 @@ __device__ __forceinline__ bool piece_select(const Params &p, const Work &w, int
     const uint64_t hit = __ballot(lane < 32 && inc >= k);
     const int l = __ffsll((unsigned long long)hit) - 1;
     if (lane == l) {
-      ctl[kOk] = (int)v <= NT ? 1 : 0;
       ctl[kBstar] = run * 32 + 31 - l;
       ctl[kKrem] = k - (inc - (int)v);
       ctl[kM] = (int)v;
     }
   }
   __syncthreads();
-  if (!ctl[kOk]) return give_up();
-  const int bstar = ctl[kBstar], krem = ctl[kKrem], m = ctl[kM];
+  const int bstar = ctl[kBstar], krem = ctl[kKrem], m = ctl[kM];  // m <= R
   // 5. The k-th bucket's keys; the own positions become row positions.
   for (int i = tid; i < R; i += NT) {
     const uint32_t x = runk[i];
-    if (kb.of(x) == bstar) bs->items[atomicAdd(&ctl[kNb], 1)] = x;
+    if (kb.of(x) == bstar) bkeys[atomicAdd(&ctl[kNb], 1)] = x;
   }
   for (int i = tid; i < n_own; i += NT) pos_l[i] += (uint32_t)(c0 * ck);
   __syncthreads();
-  // 6. The krem-th largest of them: T (equal keys agree).
-  if (tid < m) {
-    const uint32_t x = bs->items[tid];
-    int gt = 0, ge = 0;
-    for (int y = 0; y < m; ++y) {
-      const uint32_t v = bs->items[y];
-      gt += v > x ? 1 : 0;
-      ge += v >= x ? 1 : 0;
+  // 6. The krem-th largest of them: T (equal keys agree), by an exact rank
+  // count, or by three radix passes over the key bits when the bucket holds
+  // more keys than the workgroup has threads.
+  if (m <= NT) {
+    if (tid < m) {
+      const uint32_t x = bkeys[tid];
+      int gt = 0, ge = 0;
+      for (int y = 0; y < m; ++y) {
+        const uint32_t v = bkeys[y];
+        gt += v > x ? 1 : 0;
+        ge += v >= x ? 1 : 0;
+      }
+      if (gt < krem && krem <= ge) {
+        ctl[kT] = (int)x;
+        ctl[kAboveT] = gt;
+      }
     }
-    if (gt < krem && krem <= ge) {
-      ctl[kT] = (int)x;
-      ctl[kAboveT] = gt;
+  } else {
+    uint32_t t;
+    int eq;
+    radix_select<NT>(LdsKeys{bkeys}, m, krem, hist, sh, t, eq);
+    if (tid == 0) {
+      ctl[kT] = (int)t;
+      ctl[kAboveT] = krem - eq;
     }
   }
   __syncthreads();
@@ -2089,7 +2103,8 @@ __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(4))) void k_
                              rp.hi - rp.lo, k, hist, &sh, irow, vrow);
     } else if (MODE == 0 && [&] {
                  if constexpr (PIECES)
-                   return piece_select<NT>(p, w, row, L, k, irow, vrow, weights, dyn, &bs, &rsh);
+                   return piece_select<NT>(p, w, row, L, k, irow, vrow, weights, dyn, hist, &sh,
+                                           &rsh);
                  return false;
                }()) {
       weights_done = true;  // (the pieces wrote weights when they were asked for)

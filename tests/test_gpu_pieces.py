@@ -10,8 +10,9 @@ flags 32 / 16 turn the pieces on / off whatever the row's candidates), and
 match the oracle: few rows with one to
 several chunks per piece, ragged paged batches, group-shared rows, forced
 windows, exactly tied keys straddling the pieces (a k-th bucket within the
-workgroup's width, and one beyond it, which the row's first piece then
-selects alone) and low sparsity.
+workgroup's width, ranked by an exact count, and one beyond it, ranked by
+radix passes over its keys), low sparsity, and a row on the exact fallback
+beside rows in pieces.
 """
 import dataclasses
 
@@ -110,7 +111,7 @@ def test_pieces_equal_one_workgroup_per_row(sd, name):
 def test_pieces_with_tied_keys_across_pieces(sd, period):
     # Period 50: about 400 positions share the k-th key, the bucket's keys
     # are ranked across pieces.  Period 7: about 2900 do, more than the
-    # workgroup's width, and the row's first piece selects it alone.
+    # workgroup's width: radix passes over the bucket's keys rank them.
     inp = tied(synth.make_inputs(2, seed=12, B=2, N=20007), period)
     out_a, idx_a = run(sd, inp, PIECES_ON)
     out_b, idx_b = run(sd, inp, PIECES_OFF)
